@@ -1,0 +1,202 @@
+"""Seeded synthetic inputs shared by the CPU oracle's tests and the GPU path.
+
+This module only draws random numbers and lays them out: model shapes,
+weights, token ids, context lengths, paged-pool block tables and raw
+attention operands.  It contains none of the decoder's arithmetic, so both
+sides of a parity test can take their inputs from here without sharing any
+part of the computation under test.
+
+The workloads stand in for the paper's RL rollout traces (its Evaluation
+section, experimental setup), which are not available: long-horizon decode
+over a batch whose context lengths differ by orders of magnitude
+(Background, workload evolution).  Every generator is a pure function of its
+seed, drawn with numpy's PCG64 ``default_rng``.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, List
+
+import numpy as np
+
+PAGE_TOKENS = 16
+
+
+@dataclasses.dataclass(frozen=True)
+class ModelShape:
+    """Shape of a Llama-style pre-norm decoder (RMSNorm, RoPE, GQA, SwiGLU)."""
+
+    n_layers: int
+    d_model: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    ffn_dim: int
+    vocab: int
+    rms_eps: float = 1e-6
+    rope_base: float = 10000.0
+
+    @property
+    def q_dim(self) -> int:
+        return self.n_q_heads * self.head_dim
+
+    @property
+    def kv_dim(self) -> int:
+        return self.n_kv_heads * self.head_dim
+
+
+# The 2-layer fp32 decoder used for end-to-end parity.
+TINY = ModelShape(n_layers=2, d_model=256, n_q_heads=4, n_kv_heads=2, head_dim=64,
+                  ffn_dim=688, vocab=1024)
+# The 8B-shaped decoder (Llama-3-8B-like shape) used for throughput work.
+EIGHT_B = ModelShape(n_layers=32, d_model=4096, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                     ffn_dim=14336, vocab=128256)
+# A small bf16 decoder with the 8B model's head geometry (head_dim 128, GQA 4),
+# small enough for a float64 oracle to run in seconds.
+SMALL_BF16 = ModelShape(n_layers=2, d_model=512, n_q_heads=8, n_kv_heads=2, head_dim=128,
+                        ffn_dim=1408, vocab=2048)
+
+
+def round_to_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to the nearest bfloat16 (ties to even); float32 result."""
+    a = np.ascontiguousarray(x, dtype=np.float32)
+    bits = a.view(np.uint32).astype(np.uint64)
+    rounded = ((bits + 0x7FFF + ((bits >> 16) & 1)) >> 16) << 16
+    return rounded.astype(np.uint32).view(np.float32).reshape(a.shape)
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """uint16 bit patterns of float32 values that are already bf16-representable."""
+    a = np.ascontiguousarray(x, dtype=np.float32)
+    return (a.view(np.uint32) >> 16).astype(np.uint16)
+
+
+def layer_matrix_names() -> List[str]:
+    return ["wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down"]
+
+
+def make_weights(shape: ModelShape, seed: int = 0, bf16: bool = False,
+                 std: float = 0.02) -> Dict[str, object]:
+    """Seeded random weights in the nn.Linear ``[out, in]`` layout.
+
+    Every matrix is drawn N(0, std) in the fixed order: embedding, then per
+    layer q, k, v, o, gate, up, down, then the LM head.  Norm gains are 1.0.
+    With ``bf16`` the float32 draws are rounded to bf16 (RNE); both sides
+    then use exactly the same representable values.
+    """
+    rng = np.random.default_rng(seed)
+    s = shape
+
+    def draw(rows, cols):
+        w = (rng.standard_normal((rows, cols), dtype=np.float32) * np.float32(std))
+        return round_to_bf16(w) if bf16 else w
+
+    weights: Dict[str, object] = {"embed": draw(s.vocab, s.d_model), "layers": []}
+    for _ in range(s.n_layers):
+        layer = {
+            "wq": draw(s.q_dim, s.d_model),
+            "wk": draw(s.kv_dim, s.d_model),
+            "wv": draw(s.kv_dim, s.d_model),
+            "wo": draw(s.d_model, s.q_dim),
+            "w_gate": draw(s.ffn_dim, s.d_model),
+            "w_up": draw(s.ffn_dim, s.d_model),
+            "w_down": draw(s.d_model, s.ffn_dim),
+            "attn_norm": np.ones(s.d_model, dtype=np.float32),
+            "ffn_norm": np.ones(s.d_model, dtype=np.float32),
+        }
+        weights["layers"].append(layer)
+    weights["lm_head"] = draw(s.vocab, s.d_model)
+    weights["final_norm"] = np.ones(s.d_model, dtype=np.float32)
+    return weights
+
+
+def random_tokens(n: int, vocab: int, seed: int) -> np.ndarray:
+    return np.random.default_rng(seed).integers(0, vocab, size=n, dtype=np.int64).astype(np.int32)
+
+
+# ---------------------------------------------------------------------------
+# Context-length distributions of the decode workloads.
+# ---------------------------------------------------------------------------
+
+def lengths_uniform(batch: int, lo: int, hi: int, seed: int) -> np.ndarray:
+    """Integer lengths uniform on [lo, hi] inclusive."""
+    return np.random.default_rng(seed).integers(lo, hi + 1, size=batch).astype(np.int64)
+
+
+def lengths_lognormal(batch: int, median: float, sigma: float, lo: int, hi: int,
+                      seed: int) -> np.ndarray:
+    """Lognormal lengths (given median and log-sigma), clamped to [lo, hi]."""
+    x = np.random.default_rng(seed).lognormal(np.log(median), sigma, size=batch)
+    return np.clip(np.floor(x), lo, hi).astype(np.int64)
+
+
+def lengths_pareto(batch: int, alpha: float, xmin: int, cap: int, seed: int) -> np.ndarray:
+    """Pareto type I lengths by inverse CDF, floor(xmin * U^(-1/alpha)), capped."""
+    u = np.random.default_rng(seed).random(batch)
+    u = np.maximum(u, np.finfo(np.float64).tiny)
+    return np.minimum(np.floor(xmin * u ** (-1.0 / alpha)), cap).astype(np.int64)
+
+
+# ---------------------------------------------------------------------------
+# Isolated paged decode attention operands.
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class PagedAttentionCase:
+    """Operands of one isolated paged decode-attention call.
+
+    ``k_pool`` is ``[n_pages][Hkv][16][Dh]``; ``v_pool`` holds the same
+    logical ``[n_pages][Hkv][16][Dh]`` values (the GPU side stores V pages
+    transposed, which is a layout choice of that side).  ``block_table[b]``
+    lists the physical pages of sequence b in logical order; only the first
+    ``ceil(lens[b]/16)`` entries are meaningful and the rest are -1.
+    """
+
+    q: np.ndarray           # [B, Hq, Dh] float32 (bf16-representable when bf16)
+    k_pool: np.ndarray      # [P, Hkv, 16, Dh] float32
+    v_pool: np.ndarray      # [P, Hkv, 16, Dh] float32
+    block_table: np.ndarray  # [B, max_pages] int32
+    lens: np.ndarray        # [B] int64, number of cached keys per sequence
+
+
+def paged_attention_case(batch: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                         lens: np.ndarray, n_pool_pages: int, seed: int, bf16: bool = True,
+                         poison_tail: bool = True) -> PagedAttentionCase:
+    """Random Q/K/V ~ N(0,1) and block tables drawn from a random page permutation.
+
+    The pages of sequence b are the next ceil(lens[b]/16) entries of one
+    random permutation of the pool, so no page is shared.  Slots beyond a
+    sequence's length in its last page are filled with NaN when
+    ``poison_tail`` is set: a correct kernel never reads them.
+    """
+    rng = np.random.default_rng(seed)
+    lens = np.asarray(lens, dtype=np.int64)
+    npages = (lens + PAGE_TOKENS - 1) // PAGE_TOKENS
+    if int(npages.sum()) > n_pool_pages:
+        raise ValueError("pool too small for the requested lengths")
+    perm = rng.permutation(n_pool_pages).astype(np.int32)
+    max_pages = int(npages.max()) if batch else 0
+    bt = np.full((batch, max(max_pages, 1)), -1, dtype=np.int32)
+    cursor = 0
+    for b in range(batch):
+        bt[b, :npages[b]] = perm[cursor:cursor + npages[b]]
+        cursor += int(npages[b])
+    used = perm[:cursor]
+    k_pool = np.zeros((n_pool_pages, n_kv_heads, PAGE_TOKENS, head_dim), dtype=np.float32)
+    v_pool = np.zeros_like(k_pool)
+    kdraw = rng.standard_normal((cursor, n_kv_heads, PAGE_TOKENS, head_dim), dtype=np.float32)
+    vdraw = rng.standard_normal((cursor, n_kv_heads, PAGE_TOKENS, head_dim), dtype=np.float32)
+    q = rng.standard_normal((batch, n_q_heads, head_dim), dtype=np.float32)
+    if bf16:
+        kdraw, vdraw, q = round_to_bf16(kdraw), round_to_bf16(vdraw), round_to_bf16(q)
+    k_pool[used] = kdraw
+    v_pool[used] = vdraw
+    if poison_tail:
+        for b in range(batch):
+            tail = int(lens[b] % PAGE_TOKENS)
+            if tail:
+                last = bt[b, npages[b] - 1]
+                k_pool[last, :, tail:, :] = np.nan
+                v_pool[last, :, tail:, :] = np.nan
+    return PagedAttentionCase(q=q, k_pool=k_pool, v_pool=v_pool, block_table=bt, lens=lens)
