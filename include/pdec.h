@@ -1,0 +1,245 @@
+/*
+ * pdec.h: C ABI of the MI355X (gfx950) batched paged-decode library.
+ *
+ * The library runs the batched autoregressive decode step of a rollout
+ * worker: every step reads the model weights once for the whole active batch
+ * and each trajectory's own KV history (paper: Introduction; Design
+ * Principles, "Specialization in Heterogeneous Pools").  The worker hosts a
+ * resident set of trajectories and decides locally about batching and memory
+ * (Design, "Separating Departure from Placement").  KV state lives in
+ * fixed-size pages addressed through per-trajectory block tables.
+ *
+ * Conventions shared by every call:
+ *   - Every function returns an int status (PDEC_OK or a negative code) unless
+ *     stated otherwise.  last_error() returns a per-thread message for the
+ *     last failure.
+ *   - On any error no device work has been enqueued and the host-side state
+ *     (sequence lengths, block tables, free pages) is unchanged.
+ *   - Device memory (weights, KV pool, workspace, tokens, logits) is owned by
+ *     the caller and must outlive the engine.  The library owns host metadata
+ *     and a small pinned staging ring only.
+ *   - All device work of one engine is enqueued, asynchronously, on the one
+ *     HIP stream the engine holds (engine_create / engine_set_stream).  No
+ *     call waits for the device, except where a pinned staging slot is reused
+ *     and the copy that last used it has not yet run.
+ *   - "host" pointers are ordinary CPU memory; "dev" pointers are device
+ *     memory of the current HIP device.
+ *   - Sequence ids are opaque int32 handles; an id becomes stale when its
+ *     sequence is freed, and stale ids are rejected with PDEC_BAD_SEQ.
+ */
+#ifndef PDEC_H
+#define PDEC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PDEC_OK 0
+#define PDEC_INVALID_ARG (-1)
+#define PDEC_OUT_OF_PAGES (-2)
+#define PDEC_BAD_SEQ (-3)
+#define PDEC_SEQ_TOO_LONG (-4)
+#define PDEC_HIP_ERROR (-5)
+#define PDEC_UNSUPPORTED (-6)
+
+/* Tokens per KV page. */
+#define PDEC_PAGE_TOKENS 16
+
+/* Storage type of weights and KV pages.  Activations between kernels, the
+ * residual stream, norms, softmax statistics and every accumulator are fp32
+ * on both paths; the BF16 path feeds bf16-rounded activations to its matrix
+ * cores. */
+#define PDEC_F32 0
+#define PDEC_BF16 1
+
+/* Llama-style pre-norm decoder: RMSNorm, rotary position embedding
+ * (rotate-half pairing), grouped-query attention with contiguous groups
+ * (query head h reads KV head h / (n_q_heads / n_kv_heads)), SwiGLU FFN,
+ * final RMSNorm and an untied LM head.  No biases. */
+typedef struct pdec_model_cfg {
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;  /* 64 or 128 */
+  int32_t ffn_dim;
+  int32_t vocab;
+  float rms_eps;
+  float rope_base;
+  int32_t dtype;     /* PDEC_F32 or PDEC_BF16 */
+} pdec_model_cfg;
+
+/* Device pointers to the weights, all row-major in the nn.Linear [out][in]
+ * layout and stored in cfg->dtype, except the norm gains (always fp32).
+ * The per-layer members are HOST arrays of n_layers DEVICE pointers; the
+ * arrays are copied by engine_create and may be freed afterwards. */
+typedef struct pdec_weights {
+  const void* embed;             /* [vocab][d_model] */
+  const void* lm_head;           /* [vocab][d_model] */
+  const float* final_norm;       /* [d_model] */
+  const float* const* attn_norm; /* n_layers x [d_model] */
+  const void* const* wq;         /* n_layers x [n_q_heads*head_dim][d_model] */
+  const void* const* wk;         /* n_layers x [n_kv_heads*head_dim][d_model] */
+  const void* const* wv;         /* n_layers x [n_kv_heads*head_dim][d_model] */
+  const void* const* wo;         /* n_layers x [d_model][n_q_heads*head_dim] */
+  const float* const* ffn_norm;  /* n_layers x [d_model] */
+  const void* const* w_gate;     /* n_layers x [ffn_dim][d_model] */
+  const void* const* w_up;       /* n_layers x [ffn_dim][d_model] */
+  const void* const* w_down;     /* n_layers x [d_model][ffn_dim] */
+} pdec_weights;
+
+typedef struct pdec_engine pdec_engine;
+
+/* Message describing the last failure on this thread ("" if none). */
+const char* last_error(void);
+
+/* Bytes of KV state one token occupies across all layers:
+ * n_layers * 2 * n_kv_heads * head_dim * sizeof(dtype).  This is the
+ * per-token footprint the paper uses to convert its decode reserve, given in
+ * tokens, into KV-cache space (Implementation, scheduling parameters).
+ * Returns a negative status for an invalid cfg. */
+int64_t kv_bytes_per_token(const pdec_model_cfg* cfg);
+
+/* Bytes of workspace engine_create needs for these limits; negative status on
+ * invalid arguments.  max_batch bounds decode_step's batch; max_chunk bounds
+ * kv_append_prefix's chunk_tokens; kv_pool_bytes is the pool that will be
+ * passed to engine_create (it bounds the attention work list). */
+int64_t engine_workspace_bytes(const pdec_model_cfg* cfg, int32_t max_seqs, int32_t max_seq_len,
+                               int32_t max_batch, int32_t max_chunk, int64_t kv_pool_bytes);
+
+/* Create an engine (one rollout worker's decode backend).
+ *
+ * kv_pool: device buffer of kv_pool_bytes, carved into
+ *   n_pages = kv_pool_bytes / (PDEC_PAGE_TOKENS * kv_bytes_per_token(cfg))
+ * pages.  Layout, for layer l, page p, KV head g:
+ *   K block at [l][0][p][g] : [16 slots][head_dim]   (row per token)
+ *   V block at [l][1][p][g] : [head_dim][16 slots]   (transposed per page)
+ * i.e. the pool is [n_layers][2][n_pages][n_kv_heads][16 * head_dim].
+ * workspace: device buffer of at least engine_workspace_bytes(...) bytes.
+ * stream: a hipStream_t (NULL = the null stream).
+ * The engine starts with an empty resident set and every page free.
+ * Errors: PDEC_INVALID_ARG (bad sizes, null pointers), PDEC_UNSUPPORTED
+ * (shapes the kernels do not handle: head_dim other than 64/128, GQA group
+ * size not dividing 16, BF16 dims not multiples of 64), PDEC_HIP_ERROR. */
+int engine_create(const pdec_model_cfg* cfg, const pdec_weights* weights, void* kv_pool,
+                  int64_t kv_pool_bytes, int32_t max_seqs, int32_t max_seq_len, int32_t max_batch,
+                  int32_t max_chunk, void* workspace, int64_t workspace_bytes, void* stream,
+                  pdec_engine** out);
+
+/* Release host resources.  Waits for the engine's stream first. */
+void engine_destroy(pdec_engine* engine);
+
+/* Change the stream later calls enqueue on (hipStream_t). */
+int engine_set_stream(pdec_engine* engine, void* stream);
+
+/* Launch timing for measurement.  While enabled, every launch of the timed
+ * classes below is bracketed by a pair of HIP events on the engine's stream;
+ * engine_profile_read synchronises on them and returns the summed elapsed
+ * time (ms) and the launch count of one class, clearing those records. */
+#define PDEC_TIMER_ATTENTION 0 /* paged split-K attention pass, one per layer */
+#define PDEC_TIMER_GEMM 1      /* the four weight projections of each layer */
+#define PDEC_TIMER_LM_HEAD 2   /* the LM-head projection */
+int engine_profile(pdec_engine* engine, int32_t enable);
+int engine_profile_read(pdec_engine* engine, int32_t kind, double* total_ms, int64_t* launches);
+
+/* Admit an empty trajectory and reserve ceil(reserve_tokens / 16) pages for
+ * its growth.  Placement is feasible only if the footprint fits in the
+ * headroom (Design, "Separating Departure from Placement": KV headroom), and
+ * the per-resident decode reserve is a token count (Design, "Sustaining
+ * Specialization": pacing thresholds).  Reserved pages are held by the
+ * sequence and consumed first as it grows.
+ * Errors: PDEC_OUT_OF_PAGES (not enough free pages, nothing changes),
+ * PDEC_INVALID_ARG (reserve_tokens < 0 or > max_seq_len, or no free sequence
+ * slot). */
+int kv_alloc(pdec_engine* engine, int32_t reserve_tokens, int32_t* seq_out);
+
+/* Departure: free every page of the sequence, raising the headroom at once
+ * (Design, "Separating Departure from Placement").  The id becomes stale.
+ * Work already enqueued that reads these pages still runs before any later
+ * reuse, since every call uses the engine's one stream. */
+int kv_free(pdec_engine* engine, int32_t seq);
+
+/* Number of cached tokens of a sequence. */
+int kv_len(pdec_engine* engine, int32_t seq, int32_t* len_out);
+
+/* KV headroom H_w in tokens: free pages x 16 (reserved pages excluded). */
+int kv_headroom(pdec_engine* engine, int64_t* free_tokens_out);
+
+/* Copy the sequence's page ids (logical order, reserved pages included) into
+ * pages_out (host, capacity entries); *n_out receives the count.
+ * PDEC_INVALID_ARG if capacity is too small. */
+int kv_block_table(pdec_engine* engine, int32_t seq, int32_t* pages_out, int32_t capacity,
+                   int32_t* n_out);
+
+/* Extend a sequence by n_tokens positions WITHOUT computing their KV: the
+ * caller owns the content of those slots (benchmarks stage synthetic
+ * contexts this way instead of running a long prefill).  Pages are grown
+ * atomically.  Errors: PDEC_OUT_OF_PAGES, PDEC_SEQ_TOO_LONG, PDEC_BAD_SEQ. */
+int kv_extend_uninit(pdec_engine* engine, int32_t seq, int32_t n_tokens);
+
+/* Chunked prefill of n tokens onto the sequence's existing KV: the
+ * destination-side re-prefill the paper falls back to when prepared KV cannot
+ * be used (Design, "KV Preparation for Late-Bound Placement"), and the
+ * backend's chunked prefill ordering.  Token i is placed at position
+ * kv_len + i.  tokens_host: host array of n token ids.  The work is done in
+ * chunks of at most chunk_tokens rows (1 <= chunk_tokens <= max_chunk); the
+ * result does not depend on the chunking beyond rounding.  last_logits_dev
+ * (nullable): device fp32 [vocab] receiving the logits at the last new
+ * position.  Pages for all n tokens are taken up front.
+ * Errors: PDEC_OUT_OF_PAGES, PDEC_SEQ_TOO_LONG, PDEC_BAD_SEQ, PDEC_INVALID_ARG
+ * (n < 1, token id outside [0, vocab)). */
+int kv_append_prefix(pdec_engine* engine, int32_t seq, const int32_t* tokens_host, int32_t n,
+                     int32_t chunk_tokens, float* last_logits_dev);
+
+/* One decode step for `batch` distinct resident sequences (iteration-level
+ * token batching; Design, "Separating Departure from Placement").
+ * seq_ids_host: host [batch] ids, any order; tokens_dev: device int32 [batch],
+ * token i is the input of seq_ids_host[i] at position kv_len(seq);
+ * logits_dev: device fp32 [batch][vocab] receives the next-token logits.
+ * Each sequence's result does not depend on the order or on the other
+ * members of the batch.  Page growth is atomic across the whole batch.
+ * Errors: PDEC_INVALID_ARG (batch outside [1, max_batch], repeated ids),
+ * PDEC_BAD_SEQ, PDEC_SEQ_TOO_LONG, PDEC_OUT_OF_PAGES. */
+int decode_step(pdec_engine* engine, int32_t batch, const int32_t* seq_ids_host,
+                const int32_t* tokens_dev, float* logits_dev);
+
+/* Next tokens from logits: mode 0 = greedy argmax, ties to the lowest id
+ * (the paper does not state its sampler).  logits_dev: device fp32
+ * [batch][vocab]; tokens_dev_out: device int32 [batch].
+ * Errors: PDEC_UNSUPPORTED for any other mode, PDEC_INVALID_ARG. */
+int sample(pdec_engine* engine, int32_t batch, const float* logits_dev, int32_t* tokens_dev_out,
+           int32_t mode);
+
+/* ---------------------------------------------------------------------------
+ * Isolated paged decode attention (one layer, no engine).
+ *
+ * For each sequence b and query head h (KV head g = h / (n_q_heads /
+ * n_kv_heads)): out[b][h] = softmax(q[b][h] . K_g^T / sqrt(head_dim)) V_g over
+ * the lens[b] cached positions of b.  Long-context decode attention is the
+ * memory-bandwidth-bound part of the step (Design Principles,
+ * "Specialization in Heterogeneous Pools").
+ *   q: device [batch][n_q_heads][head_dim] in dtype;
+ *   k_pages: device [n_pages][n_kv_heads][16][head_dim];
+ *   v_pages: device [n_pages][n_kv_heads][head_dim][16];
+ *   block_table_dev: device int32 [batch][bt_stride], logical page order;
+ *   lens_host: host int32 [batch], each in [1, bt_stride * 16];
+ *   out: device fp32 [batch][n_q_heads][head_dim];
+ *   workspace: device, at least paged_attention_workspace_bytes(...).
+ * Slots past lens[b] in the last page are never read.
+ * ------------------------------------------------------------------------- */
+int64_t paged_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                        int32_t head_dim, int64_t max_total_tokens);
+
+int paged_decode_attention(int32_t dtype, int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                           int32_t head_dim, const void* q, const void* k_pages,
+                           const void* v_pages, const int32_t* block_table_dev, int32_t bt_stride,
+                           const int32_t* lens_host, float* out, void* workspace,
+                           int64_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PDEC_H */

@@ -1,0 +1,344 @@
+// Paged split-K decode/prefill attention for gfx950.
+//
+// Long-context decode attention is bound by HBM bandwidth (paper: Design
+// Principles, "Specialization in Heterogeneous Pools"): every cached K/V byte
+// of a trajectory is read once per step.  The key axis of each query block
+// is cut into work items of whole pages; each (item, KV head) work group
+// streams its pages once, applies them to every query head of the GQA group,
+// and leaves an online-softmax partial (max, sum, unnormalised output) that
+// the combine pass merges.  Query rows of a block = (query, head-in-group)
+// pairs, at most 16: one in-group head set per decode row, 16/G queries in
+// prefill.
+//
+// bf16 path: both products run on MFMA (v_mfma_f32_16x16x32_bf16).  Scores are
+// computed transposed, S^T = K Q^T, so that each lane's output column is one
+// query row; that keeps every softmax statistic lane-private and lets the
+// score registers feed the P operand of O^T = V^T P^T without any shuffle.
+// V pages are stored transposed ([Dh][16]) so each lane's V^T operand is one
+// contiguous 16-byte load.
+#include "hip_common.h"
+#include "kernels.h"
+
+namespace pdec {
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// ---------------------------------------------------------------------------
+// bf16, MFMA.  One wave per work group.  Lane l: c16 = l % 16, q4 = l / 16.
+//
+// Per iteration two pages (32 keys).  S tile u (u = 0, 1) has A-row i (lanes
+// with c16 = i) holding the key of page i/8, in-page token
+// 8*((i/4)%2) + 4u + i%4.  The MFMA result puts rows 4*q4 + rr in lane
+// (q4, c16), so a lane ends up with the 8 consecutive tokens
+// 8*(q4%2) + (4u + rr) of page q4/2 for its query row c16: exactly the k-group
+// the PV MFMA expects from that lane, matching a single 16-byte V^T load.
+// ---------------------------------------------------------------------------
+template <int DH>
+__global__ __launch_bounds__(64) void attn_split_bf16(
+    const AttnItem* __restrict__ items, const AttnQBlock* __restrict__ qblocks,
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
+    const uint16_t* __restrict__ vpool, int64_t page_stride, const int32_t* __restrict__ bt,
+    int32_t bt_stride, int32_t n_q_heads, int32_t n_kv_heads, float scale_log2,
+    float* __restrict__ part_ml, float* __restrict__ part_acc) {
+  constexpr int KC = DH / 32;  // k-steps of QK^T
+  constexpr int DT = DH / 16;  // 16-wide dim tiles of PV
+  const int lane = threadIdx.x;
+  const int c16 = lane & 15, q4 = lane >> 4;
+  const int item_id = blockIdx.x, g = blockIdx.y;
+  const AttnItem it = items[item_id];
+  const AttnQBlock qb = qblocks[it.qblock];
+  const int G = n_q_heads / n_kv_heads;
+
+  // This lane's query row (the B column of S^T and O^T).
+  const int jq = c16 / G;
+  const int head = g * G + (c16 % G);
+  const bool row_valid = jq < qb.n_q;
+
+  bf16x8 qf[KC];
+  if (row_valid) {
+    const uint16_t* qrow = q + ((int64_t)(qb.q_row0 + jq) * n_q_heads + head) * DH;
+#pragma unroll
+    for (int c = 0; c < KC; ++c) qf[c] = *(const bf16x8*)(qrow + c * 32 + q4 * 8);
+  } else {
+#pragma unroll
+    for (int c = 0; c < KC; ++c) qf[c] = bf16x8{};
+  }
+
+  const int key0 = it.page_begin * kPage;
+  const int key_end = (it.page_begin + it.n_pages) * kPage;
+  // Keys at or past kv_lim hold no data for any row of this block: their V is
+  // zeroed so that stale or poisoned slots cannot reach the output.
+  const int kv_lim = min(qb.pos0 + qb.n_q, key_end);
+  // Causal limit of this lane's row (exclusive).
+  const int row_lim = row_valid ? min(qb.pos0 + jq + 1, key_end) : key0;
+
+  const int32_t* btrow = bt + (int64_t)qb.slot * bt_stride + it.page_begin;
+  const int64_t head_off = (int64_t)g * (kPage * DH);
+
+  // Lane-constant offsets.
+  const int k_tok = 8 * ((c16 >> 2) & 1) + (c16 & 3);  // + 4u
+  const int k_page_sel = c16 >> 3;                     // 0: first page, 1: second
+  const int v_page_sel = q4 >> 1;
+  const int v_tok0 = 8 * (q4 & 1);
+
+  float m = -INFINITY;  // running max of scaled scores (log2 units), row-uniform
+  float l = 0.f;        // lane-partial sum of probabilities
+  f32x4 acc[DT];
+#pragma unroll
+  for (int t = 0; t < DT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int n_iter = (it.n_pages + 1) >> 1;
+  for (int iter = 0; iter < n_iter; ++iter) {
+    const int pi = 2 * iter;
+    const int page0 = btrow[pi];
+    const int page1 = (pi + 1 < it.n_pages) ? btrow[pi + 1] : page0;
+    const int64_t base0 = (int64_t)page0 * page_stride + head_off;
+    const int64_t base1 = (int64_t)page1 * page_stride + head_off;
+
+    // K: 2 tiles x KC loads of 16 B; V: DT loads of 16 B.
+    const uint16_t* kb = kpool + (k_page_sel ? base1 : base0);
+    bf16x8 kf[2][KC];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int c = 0; c < KC; ++c)
+        kf[u][c] = *(const bf16x8*)(kb + (k_tok + 4 * u) * DH + c * 32 + q4 * 8);
+    const uint16_t* vb = vpool + (v_page_sel ? base1 : base0) + v_tok0;
+    u16x8 vf[DT];
+#pragma unroll
+    for (int t = 0; t < DT; ++t) vf[t] = *(const u16x8*)(vb + (t * 16 + c16) * kPage);
+
+    f32x4 s[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      s[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < KC; ++c)
+        s[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[u][c], qf[c], s[u], 0, 0, 0);
+    }
+
+    // Keys of this lane: e = 4u + rr  ->  position kbase + e.
+    const int kbase = key0 + (pi + v_page_sel) * kPage + v_tok0;
+    float sv[8];
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int e = 4 * u + rr;
+        const float x = (kbase + e < row_lim) ? s[u][rr] * scale_log2 : -INFINITY;
+        sv[e] = x;
+        mloc = fmaxf(mloc, x);
+      }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+    const float m_new = fmaxf(m, mloc);
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = exp2f(m - m_use);
+    m = m_new;
+    l *= alpha;
+#pragma unroll
+    for (int t = 0; t < DT; ++t) acc[t] *= alpha;
+
+    u16x8 pbits;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint16_t b = f32_to_bf16(exp2f(sv[e] - m_use));
+      pbits[e] = b;
+      l += bf16_to_f32(b);  // normalise by exactly the weights the MFMA uses
+    }
+
+    if (key0 + (pi + 2) * kPage > kv_lim) {  // wave-uniform: the block's last keys
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (kbase + e >= kv_lim)
+#pragma unroll
+          for (int t = 0; t < DT; ++t) vf[t][e] = 0;
+    }
+
+    const bf16x8 pf = __builtin_bit_cast(bf16x8, pbits);
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[t]), pf,
+                                                       acc[t], 0, 0, 0);
+  }
+
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  if (row_valid) {
+    const int64_t prow = ((int64_t)item_id * n_kv_heads + g) * 16 + c16;
+    if (q4 == 0) {
+      part_ml[prow * 2] = m;
+      part_ml[prow * 2 + 1] = l;
+    }
+    float* pa = part_acc + prow * DH;
+#pragma unroll
+    for (int t = 0; t < DT; ++t) *(f32x4*)(pa + t * 16 + 4 * q4) = acc[t];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp32, VALU.  One wave per work group; lane = head dimension (DH/64 per
+// lane).  Rows and keys are walked one at a time: this path serves the small
+// fp32 decoder, where launches, not bytes, set the step time.
+// ---------------------------------------------------------------------------
+template <int DH>
+__global__ __launch_bounds__(64) void attn_split_f32(
+    const AttnItem* __restrict__ items, const AttnQBlock* __restrict__ qblocks,
+    const float* __restrict__ q, const float* __restrict__ kpool, const float* __restrict__ vpool,
+    int64_t page_stride, const int32_t* __restrict__ bt, int32_t bt_stride, int32_t n_q_heads,
+    int32_t n_kv_heads, float scale_log2, float* __restrict__ part_ml,
+    float* __restrict__ part_acc) {
+  constexpr int E = DH / 64;
+  const int lane = threadIdx.x;
+  const int item_id = blockIdx.x, g = blockIdx.y;
+  const AttnItem it = items[item_id];
+  const AttnQBlock qb = qblocks[it.qblock];
+  const int G = n_q_heads / n_kv_heads;
+  const int key0 = it.page_begin * kPage;
+  const int key_end = (it.page_begin + it.n_pages) * kPage;
+  const int32_t* btrow = bt + (int64_t)qb.slot * bt_stride;
+  const int64_t head_off = (int64_t)g * (kPage * DH);
+
+  for (int r = 0; r < qb.n_q * G; ++r) {
+    const int jq = r / G, head = g * G + r % G;
+    const float* qrow = q + ((int64_t)(qb.q_row0 + jq) * n_q_heads + head) * DH;
+    float qv[E], acc[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      qv[e] = qrow[lane + 64 * e] * scale_log2;
+      acc[e] = 0.f;
+    }
+    float m = -INFINITY, l = 0.f;
+    const int lim = min(qb.pos0 + jq + 1, key_end);
+    for (int kp = key0; kp < lim; ++kp) {
+      const int64_t base = (int64_t)btrow[kp / kPage] * page_stride + head_off;
+      const int t = kp % kPage;
+      float part = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) part += qv[e] * kpool[base + t * DH + lane + 64 * e];
+      const float s = wave_sum(part);
+      const float m_new = fmaxf(m, s);
+      const float alpha = exp2f(m - m_new);
+      const float p = exp2f(s - m_new);
+      l = l * alpha + p;
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        acc[e] = acc[e] * alpha + p * vpool[base + (lane + 64 * e) * kPage + t];
+      m = m_new;
+    }
+    const int64_t prow = ((int64_t)item_id * n_kv_heads + g) * 16 + r;
+    if (lane == 0) {
+      part_ml[prow * 2] = m;
+      part_ml[prow * 2 + 1] = l;
+    }
+#pragma unroll
+    for (int e = 0; e < E; ++e) part_acc[prow * DH + lane + 64 * e] = acc[e];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Merge the partials of each (query row, head): M = max m_i,
+// o = sum_i exp2(m_i - M) acc_i / sum_i exp2(m_i - M) l_i, in item order.
+// ---------------------------------------------------------------------------
+template <int DH, typename OutT>
+__global__ __launch_bounds__(64) void attn_combine(const AttnQBlock* __restrict__ qblocks,
+                                                  const float* __restrict__ part_ml,
+                                                  const float* __restrict__ part_acc,
+                                                  int32_t n_q_heads, int32_t n_kv_heads,
+                                                  OutT* __restrict__ out) {
+  constexpr int E = DH / 64;
+  const int lane = threadIdx.x;
+  const AttnQBlock qb = qblocks[blockIdx.x];
+  const int head = blockIdx.y;
+  const int G = n_q_heads / n_kv_heads;
+  const int g = head / G;
+  for (int jq = 0; jq < qb.n_q; ++jq) {
+    const int r = jq * G + head % G;
+    float mmax = -INFINITY;
+    for (int i = qb.item_begin; i < qb.item_end; ++i)
+      mmax = fmaxf(mmax, part_ml[(((int64_t)i * n_kv_heads + g) * 16 + r) * 2]);
+    float lsum = 0.f, o[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) o[e] = 0.f;
+    for (int i = qb.item_begin; i < qb.item_end; ++i) {
+      const int64_t prow = ((int64_t)i * n_kv_heads + g) * 16 + r;
+      const float mi = part_ml[prow * 2];
+      const float w = (mi == -INFINITY) ? 0.f : exp2f(mi - mmax);
+      lsum += w * part_ml[prow * 2 + 1];
+#pragma unroll
+      for (int e = 0; e < E; ++e) o[e] += w * part_acc[prow * DH + lane + 64 * e];
+    }
+    const float inv = 1.f / lsum;
+    OutT* orow = out + ((int64_t)(qb.q_row0 + jq) * n_q_heads + head) * DH;
+#pragma unroll
+    for (int e = 0; e < E; ++e) orow[lane + 64 * e] = Store<OutT>::from(o[e] * inv);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attention_split(int dtype, int head_dim, int n_items, int n_q_heads,
+                                  int n_kv_heads, const AttnItem* items,
+                                  const AttnQBlock* qblocks, const void* q, const void* k_pages,
+                                  const void* v_pages, int64_t page_stride_elems,
+                                  const int32_t* block_table, int32_t bt_stride, float* part_ml,
+                                  float* part_acc, hipStream_t stream) {
+  if (n_items == 0) return hipSuccess;
+  const dim3 grid(n_items, n_kv_heads), block(64);
+  const float scale_log2 = kLog2e / sqrtf((float)head_dim);
+  if (dtype == 1) {
+    if (head_dim == 128)
+      attn_split_bf16<128><<<grid, block, 0, stream>>>(
+          items, qblocks, (const uint16_t*)q, (const uint16_t*)k_pages,
+          (const uint16_t*)v_pages, page_stride_elems, block_table, bt_stride, n_q_heads,
+          n_kv_heads, scale_log2, part_ml, part_acc);
+    else
+      attn_split_bf16<64><<<grid, block, 0, stream>>>(
+          items, qblocks, (const uint16_t*)q, (const uint16_t*)k_pages,
+          (const uint16_t*)v_pages, page_stride_elems, block_table, bt_stride, n_q_heads,
+          n_kv_heads, scale_log2, part_ml, part_acc);
+  } else {
+    if (head_dim == 128)
+      attn_split_f32<128><<<grid, block, 0, stream>>>(
+          items, qblocks, (const float*)q, (const float*)k_pages, (const float*)v_pages,
+          page_stride_elems, block_table, bt_stride, n_q_heads, n_kv_heads, scale_log2, part_ml,
+          part_acc);
+    else
+      attn_split_f32<64><<<grid, block, 0, stream>>>(
+          items, qblocks, (const float*)q, (const float*)k_pages, (const float*)v_pages,
+          page_stride_elems, block_table, bt_stride, n_q_heads, n_kv_heads, scale_log2, part_ml,
+          part_acc);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_combine(int head_dim, int n_qblocks, int n_q_heads, int n_kv_heads,
+                                    const AttnQBlock* qblocks, const float* part_ml,
+                                    const float* part_acc, void* out, int out_bf16,
+                                    hipStream_t stream) {
+  if (n_qblocks == 0) return hipSuccess;
+  const dim3 grid(n_qblocks, n_q_heads), block(64);
+  if (head_dim == 128) {
+    if (out_bf16)
+      attn_combine<128, uint16_t><<<grid, block, 0, stream>>>(qblocks, part_ml, part_acc,
+                                                              n_q_heads, n_kv_heads,
+                                                              (uint16_t*)out);
+    else
+      attn_combine<128, float><<<grid, block, 0, stream>>>(qblocks, part_ml, part_acc, n_q_heads,
+                                                           n_kv_heads, (float*)out);
+  } else {
+    if (out_bf16)
+      attn_combine<64, uint16_t><<<grid, block, 0, stream>>>(qblocks, part_ml, part_acc,
+                                                             n_q_heads, n_kv_heads,
+                                                             (uint16_t*)out);
+    else
+      attn_combine<64, float><<<grid, block, 0, stream>>>(qblocks, part_ml, part_acc, n_q_heads,
+                                                          n_kv_heads, (float*)out);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace pdec

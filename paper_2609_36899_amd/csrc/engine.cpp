@@ -1,0 +1,776 @@
+// C ABI of the decode library: engine state, workspace carving, per-call
+// planning and the launch sequence of one decoder step.
+//
+// The engine is one rollout worker's decode backend (paper: Design,
+// "Separating Departure from Placement"): it holds the resident set, its
+// paged KV cache and the KV headroom, and runs iteration-level token batches
+// over any subset of residents.  Host work per call is bookkeeping only
+// (lengths, page growth, the attention work list); every step of the
+// computation runs in the gfx950 kernels.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/pdec.h"
+#include "kernels.h"
+#include "pagepool.h"
+
+using namespace pdec;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define HIP_OR_FAIL(expr)                                                                \
+  do {                                                                                   \
+    hipError_t e_ = (expr);                                                              \
+    if (e_ != hipSuccess)                                                                \
+      return fail(PDEC_HIP_ERROR, std::string(#expr) + ": " + hipGetErrorString(e_));    \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+int64_t elem_bytes(int32_t dtype) { return dtype == PDEC_BF16 ? 2 : 4; }
+
+// ---------------------------------------------------------------------------
+// Pinned staging ring for host-to-device metadata copies.
+// ---------------------------------------------------------------------------
+class Staging {
+ public:
+  ~Staging() { release(); }
+  hipError_t init(size_t slot_bytes, int n_slots) {
+    slot_bytes_ = slot_bytes;
+    for (int i = 0; i < n_slots; ++i) {
+      void* p = nullptr;
+      hipError_t e = hipHostMalloc(&p, slot_bytes, hipHostMallocDefault);
+      if (e != hipSuccess) return e;
+      slots_.push_back(p);
+      hipEvent_t ev;
+      e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+      if (e != hipSuccess) return e;
+      events_.push_back(ev);
+      used_.push_back(false);
+    }
+    return hipSuccess;
+  }
+  void release() {
+    for (size_t i = 0; i < slots_.size(); ++i) {
+      if (used_[i]) (void)hipEventSynchronize(events_[i]);
+      (void)hipEventDestroy(events_[i]);
+      (void)hipHostFree(slots_[i]);
+    }
+    slots_.clear();
+    events_.clear();
+    used_.clear();
+  }
+  size_t slot_bytes() const { return slot_bytes_; }
+  // Copies in pieces of at most one slot.
+  hipError_t upload(void* dst, const void* src, size_t bytes, hipStream_t s) {
+    size_t off = 0;
+    while (off < bytes) {
+      const size_t n = std::min(slot_bytes_, bytes - off);
+      const int k = next_;
+      next_ = (next_ + 1) % (int)slots_.size();
+      if (used_[k]) {
+        hipError_t e = hipEventSynchronize(events_[k]);
+        if (e != hipSuccess) return e;
+      }
+      std::memcpy(slots_[k], (const char*)src + off, n);
+      hipError_t e = hipMemcpyAsync((char*)dst + off, slots_[k], n, hipMemcpyHostToDevice, s);
+      if (e != hipSuccess) return e;
+      e = hipEventRecord(events_[k], s);
+      if (e != hipSuccess) return e;
+      used_[k] = true;
+      off += n;
+    }
+    return hipSuccess;
+  }
+
+ private:
+  std::vector<void*> slots_;
+  std::vector<hipEvent_t> events_;
+  std::vector<bool> used_;
+  size_t slot_bytes_ = 0;
+  int next_ = 0;
+};
+
+// ---------------------------------------------------------------------------
+// Optional per-launch timing: event pairs around chosen launch classes.
+// ---------------------------------------------------------------------------
+class LaunchTimer {
+ public:
+  ~LaunchTimer() { reset_pool(); }
+  void enable(bool on) { on_ = on; }
+  bool on() const { return on_; }
+  hipError_t begin(int kind, hipStream_t s) {
+    if (!on_) return hipSuccess;
+    hipEvent_t a, b;
+    hipError_t e = take(&a);
+    if (e == hipSuccess) e = take(&b);
+    if (e == hipSuccess) e = hipEventRecord(a, s);
+    if (e != hipSuccess) return e;
+    open_.push_back({kind, a, b});
+    return hipSuccess;
+  }
+  hipError_t end(hipStream_t s) {
+    if (!on_ || open_.empty()) return hipSuccess;
+    Rec r = open_.back();
+    open_.pop_back();
+    done_.push_back(r);
+    return hipEventRecord(r.b, s);
+  }
+  // Sum of elapsed times (ms) and launch count of one kind; clears records.
+  hipError_t read(int kind, double* ms, int64_t* count) {
+    *ms = 0.0;
+    *count = 0;
+    std::vector<Rec> keep;
+    for (const Rec& r : done_) {
+      if (r.kind != kind) {
+        keep.push_back(r);
+        continue;
+      }
+      hipError_t e = hipEventSynchronize(r.b);
+      if (e != hipSuccess) return e;
+      float t = 0.f;
+      e = hipEventElapsedTime(&t, r.a, r.b);
+      if (e != hipSuccess) return e;
+      *ms += t;
+      *count += 1;
+      free_.push_back(r.a);
+      free_.push_back(r.b);
+    }
+    done_.swap(keep);
+    return hipSuccess;
+  }
+
+ private:
+  struct Rec {
+    int kind;
+    hipEvent_t a, b;
+  };
+  hipError_t take(hipEvent_t* ev) {
+    if (!free_.empty()) {
+      *ev = free_.back();
+      free_.pop_back();
+      return hipSuccess;
+    }
+    hipError_t e = hipEventCreate(ev);
+    if (e == hipSuccess) all_.push_back(*ev);
+    return e;
+  }
+  void reset_pool() {
+    for (hipEvent_t e : all_) (void)hipEventDestroy(e);
+    all_.clear();
+    free_.clear();
+    done_.clear();
+    open_.clear();
+  }
+  bool on_ = false;
+  std::vector<Rec> open_, done_;
+  std::vector<hipEvent_t> free_, all_;
+};
+
+// ---------------------------------------------------------------------------
+// Workspace layout.
+// ---------------------------------------------------------------------------
+struct WsLayout {
+  size_t rope, bt, meta, delta, x, h, o, u, q, part, att_ml, att_acc, total;
+  size_t meta_bytes, part_elems, delta_cap;
+  int64_t items_cap, qblocks_cap, rows_cap;
+  int32_t bt_stride;
+};
+
+constexpr size_t kDeltaCap = 65536;
+
+int check_cfg(const pdec_model_cfg* c) {
+  if (!c) return fail(PDEC_INVALID_ARG, "null cfg");
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1 ||
+      c->head_dim < 1 || c->ffn_dim < 1 || c->vocab < 1)
+    return fail(PDEC_INVALID_ARG, "model dimensions must be positive");
+  if (c->dtype != PDEC_F32 && c->dtype != PDEC_BF16)
+    return fail(PDEC_INVALID_ARG, "dtype must be PDEC_F32 or PDEC_BF16");
+  if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f))
+    return fail(PDEC_INVALID_ARG, "rms_eps must be >= 0 and rope_base > 0");
+  if (c->n_q_heads % c->n_kv_heads != 0)
+    return fail(PDEC_INVALID_ARG, "n_q_heads must be a multiple of n_kv_heads");
+  const int G = c->n_q_heads / c->n_kv_heads;
+  if (16 % G != 0) return fail(PDEC_UNSUPPORTED, "GQA group size must divide 16");
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(PDEC_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (c->dtype == PDEC_BF16 && (c->d_model % 64 || c->ffn_dim % 64))
+    return fail(PDEC_UNSUPPORTED, "bf16 path needs d_model and ffn_dim multiples of 64");
+  return PDEC_OK;
+}
+
+int64_t kv_token_bytes(const pdec_model_cfg* c) {
+  return (int64_t)c->n_layers * 2 * c->n_kv_heads * c->head_dim * elem_bytes(c->dtype);
+}
+
+size_t part_elems_for(const pdec_model_cfg* c, int64_t rows_cap) {
+  const int qd = c->n_q_heads * c->head_dim, kvd = c->n_kv_heads * c->head_dim;
+  const int shapes[4][2] = {{qd + 2 * kvd, c->d_model},
+                            {c->d_model, qd},
+                            {2 * c->ffn_dim, c->d_model},
+                            {c->d_model, c->ffn_dim}};
+  size_t best = 0;
+  for (int64_t m = 1; m <= rows_cap; ++m)
+    for (auto& s : shapes) {
+      int ks;
+      const int S = gemm_plan_splits(c->dtype, (int)m, s[0], s[1], &ks);
+      best = std::max(best, (size_t)S * (size_t)m * (size_t)s[0]);
+    }
+  return best;
+}
+
+int make_layout(const pdec_model_cfg* c, int32_t max_seqs, int32_t max_seq_len,
+                int32_t max_batch, int32_t max_chunk, WsLayout* L) {
+  const int G = c->n_q_heads / c->n_kv_heads;
+  const int64_t ab = elem_bytes(c->dtype);
+  const int64_t qd = (int64_t)c->n_q_heads * c->head_dim;
+  L->rows_cap = std::max(max_batch, max_chunk);
+  L->qblocks_cap = std::max<int64_t>(max_batch, (max_chunk + (16 / G) - 1) / (16 / G));
+  L->items_cap = attn_target_items(c->n_kv_heads) + L->qblocks_cap + 16;
+  L->bt_stride = PagePool::pages_for(max_seq_len);
+  L->meta_bytes = align_up(L->rows_cap * sizeof(RowMeta)) +
+                  align_up(L->qblocks_cap * sizeof(AttnQBlock)) +
+                  align_up(L->items_cap * sizeof(AttnItem)) + align_up(L->rows_cap * 4);
+  L->delta_cap = kDeltaCap;
+  L->part_elems = part_elems_for(c, L->rows_cap);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  L->rope = take((size_t)max_seq_len * (c->head_dim / 2) * sizeof(float2));
+  L->bt = take((size_t)max_seqs * L->bt_stride * 4);
+  L->meta = take(L->meta_bytes);
+  L->delta = take(L->delta_cap * sizeof(BtDelta));
+  L->x = take((size_t)L->rows_cap * c->d_model * 4);
+  L->h = take((size_t)L->rows_cap * c->d_model * ab);
+  L->o = take((size_t)L->rows_cap * qd * ab);
+  L->u = take((size_t)L->rows_cap * c->ffn_dim * ab);
+  L->q = take((size_t)L->rows_cap * qd * ab);
+  L->part = take(L->part_elems * 4);
+  L->att_ml = take((size_t)L->items_cap * c->n_kv_heads * 16 * 2 * 4);
+  L->att_acc = take((size_t)L->items_cap * c->n_kv_heads * 16 * c->head_dim * 4);
+  L->total = off;
+  return PDEC_OK;
+}
+
+}  // namespace
+
+struct pdec_engine {
+  pdec_model_cfg cfg;
+  const void* embed = nullptr;
+  const void* lm_head = nullptr;
+  const float* final_norm = nullptr;
+  std::vector<const float*> attn_norm, ffn_norm;
+  std::vector<WSegs> w_qkv, w_o, w_gu, w_down;
+
+  char* kv_pool = nullptr;
+  int64_t n_pages = 0;
+  int64_t page_stride = 0;  // elements of one page in one layer-kind block
+  PagePool* pool = nullptr;
+  int32_t max_batch = 0, max_chunk = 0;
+
+  WsLayout ws{};
+  char* base = nullptr;
+  float2* rope_cs = nullptr;
+  int32_t* bt = nullptr;
+  char* meta = nullptr;
+  BtDelta* delta = nullptr;
+  float* x = nullptr;
+  char *h = nullptr, *o = nullptr, *u = nullptr, *q = nullptr;
+  float* part = nullptr;
+  float* att_ml = nullptr;
+  float* att_acc = nullptr;
+
+  hipStream_t stream = nullptr;
+  Staging staging;
+  LaunchTimer timer;
+  std::vector<char> host_meta;
+  std::vector<int32_t> mark;
+  int32_t epoch = 0;
+
+  int64_t ab() const { return elem_bytes(cfg.dtype); }
+  char* k_layer(int l) const { return kv_pool + (int64_t)(2 * l) * n_pages * page_stride * ab(); }
+  char* v_layer(int l) const {
+    return kv_pool + (int64_t)(2 * l + 1) * n_pages * page_stride * ab();
+  }
+};
+
+namespace {
+
+int flush_deltas(pdec_engine* E) {
+  const auto& pend = E->pool->pending();
+  size_t off = 0;
+  while (off < pend.size()) {
+    const size_t n = std::min(E->ws.delta_cap, pend.size() - off);
+    HIP_OR_FAIL(E->staging.upload(E->delta, pend.data() + off, n * sizeof(BtDelta), E->stream));
+    HIP_OR_FAIL(launch_bt_deltas((int)n, E->delta, E->bt, E->ws.bt_stride, E->stream));
+    off += n;
+  }
+  E->pool->clear_pending();
+  return PDEC_OK;
+}
+
+// Runs the decoder over M rows whose metadata is given; writes the LM-head
+// logits of every row (lm_last_only = false) or of the last row only.
+int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
+                    const std::vector<AttnQBlock>& qblocks, const std::vector<AttnItem>& items,
+                    const int32_t* tokens_dev, const int32_t* tokens_host, float* logits,
+                    bool lm_last_only) {
+  const pdec_model_cfg& c = E->cfg;
+  if ((int64_t)items.size() > E->ws.items_cap || (int64_t)qblocks.size() > E->ws.qblocks_cap ||
+      (int64_t)rows.size() > E->ws.rows_cap)
+    return fail(PDEC_INVALID_ARG, "attention work list exceeds the workspace bound");
+  int rc = flush_deltas(E);
+  if (rc != PDEC_OK) return rc;
+
+  // Pack the metadata into one host buffer and copy it in one go.
+  const size_t o_rows = 0;
+  const size_t o_qb = align_up(rows.size() * sizeof(RowMeta));
+  const size_t o_it = o_qb + align_up(qblocks.size() * sizeof(AttnQBlock));
+  const size_t o_tok = o_it + align_up(items.size() * sizeof(AttnItem));
+  const size_t total = o_tok + (tokens_host ? (size_t)M * 4 : 0);
+  E->host_meta.resize(std::max<size_t>(total, 1));
+  char* hm = E->host_meta.data();
+  std::memcpy(hm + o_rows, rows.data(), rows.size() * sizeof(RowMeta));
+  std::memcpy(hm + o_qb, qblocks.data(), qblocks.size() * sizeof(AttnQBlock));
+  std::memcpy(hm + o_it, items.data(), items.size() * sizeof(AttnItem));
+  if (tokens_host) std::memcpy(hm + o_tok, tokens_host, (size_t)M * 4);
+  HIP_OR_FAIL(E->staging.upload(E->meta, hm, total, E->stream));
+  const RowMeta* d_rows = (const RowMeta*)(E->meta + o_rows);
+  const AttnQBlock* d_qb = (const AttnQBlock*)(E->meta + o_qb);
+  const AttnItem* d_it = (const AttnItem*)(E->meta + o_it);
+  const int32_t* d_tok = tokens_host ? (const int32_t*)(E->meta + o_tok) : tokens_dev;
+
+  const int dt = c.dtype;
+  const int d = c.d_model, F = c.ffn_dim, Dh = c.head_dim;
+  const int qd = c.n_q_heads * Dh, nqkv = qd + 2 * c.n_kv_heads * Dh;
+  hipStream_t s = E->stream;
+  const int n_items = (int)items.size(), n_qb = (int)qblocks.size();
+
+  HIP_OR_FAIL(launch_embed_norm(dt, M, d, c.vocab, d_tok, E->embed, E->attn_norm[0], c.rms_eps, E->x,
+                                E->h, s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    int ks, S;
+    S = gemm_plan_splits(dt, M, nqkv, d, &ks);
+    HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_GEMM, s));
+    HIP_OR_FAIL(launch_gemm(dt, M, nqkv, d, E->h, d, E->w_qkv[l], E->part, S, ks, s));
+    HIP_OR_FAIL(E->timer.end(s));
+    HIP_OR_FAIL(launch_qkv_rope_kv(dt, M, Dh, c.n_q_heads, c.n_kv_heads, E->part, S, d_rows,
+                                   E->rope_cs, E->bt, E->ws.bt_stride, E->q, E->k_layer(l),
+                                   E->v_layer(l), E->page_stride, s));
+    HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_ATTENTION, s));
+    HIP_OR_FAIL(launch_attention_split(dt, Dh, n_items, c.n_q_heads, c.n_kv_heads, d_it, d_qb,
+                                       E->q, E->k_layer(l), E->v_layer(l), E->page_stride, E->bt,
+                                       E->ws.bt_stride, E->att_ml, E->att_acc, s));
+    HIP_OR_FAIL(E->timer.end(s));
+    HIP_OR_FAIL(launch_attention_combine(Dh, n_qb, c.n_q_heads, c.n_kv_heads, d_qb, E->att_ml,
+                                         E->att_acc, E->o, dt == PDEC_BF16, s));
+    S = gemm_plan_splits(dt, M, d, qd, &ks);
+    HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_GEMM, s));
+    HIP_OR_FAIL(launch_gemm(dt, M, d, qd, E->o, qd, E->w_o[l], E->part, S, ks, s));
+    HIP_OR_FAIL(E->timer.end(s));
+    HIP_OR_FAIL(launch_resid_norm(dt, M, d, E->part, S, E->x, E->ffn_norm[l], c.rms_eps, E->h, s));
+    S = gemm_plan_splits(dt, M, 2 * F, d, &ks);
+    HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_GEMM, s));
+    HIP_OR_FAIL(launch_gemm(dt, M, 2 * F, d, E->h, d, E->w_gu[l], E->part, S, ks, s));
+    HIP_OR_FAIL(E->timer.end(s));
+    HIP_OR_FAIL(launch_swiglu(dt, M, F, E->part, S, E->u, s));
+    S = gemm_plan_splits(dt, M, d, F, &ks);
+    HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_GEMM, s));
+    HIP_OR_FAIL(launch_gemm(dt, M, d, F, E->u, F, E->w_down[l], E->part, S, ks, s));
+    HIP_OR_FAIL(E->timer.end(s));
+    const float* next_gain = (l + 1 < c.n_layers) ? E->attn_norm[l + 1] : E->final_norm;
+    HIP_OR_FAIL(launch_resid_norm(dt, M, d, E->part, S, E->x, next_gain, c.rms_eps, E->h, s));
+  }
+  if (logits) {
+    WSegs lm{};
+    lm.ptr[0] = E->lm_head;
+    lm.row_end[0] = c.vocab;
+    lm.n_seg = 1;
+    const char* a = E->h + (lm_last_only ? (int64_t)(M - 1) * d * E->ab() : 0);
+    HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_LM_HEAD, s));
+    HIP_OR_FAIL(launch_gemm(dt, lm_last_only ? 1 : M, c.vocab, d, a, d, lm, logits, 1, d, s));
+    HIP_OR_FAIL(E->timer.end(s));
+  }
+  return PDEC_OK;
+}
+
+std::mutex g_attn_mu;
+Staging* g_attn_staging = nullptr;
+
+}  // namespace
+
+extern "C" {
+
+const char* last_error(void) { return g_err.c_str(); }
+
+int64_t kv_bytes_per_token(const pdec_model_cfg* cfg) {
+  int rc = check_cfg(cfg);
+  if (rc != PDEC_OK) return rc;
+  return kv_token_bytes(cfg);
+}
+
+int64_t engine_workspace_bytes(const pdec_model_cfg* cfg, int32_t max_seqs, int32_t max_seq_len,
+                               int32_t max_batch, int32_t max_chunk, int64_t kv_pool_bytes) {
+  int rc = check_cfg(cfg);
+  if (rc != PDEC_OK) return rc;
+  if (max_seqs < 1 || max_seqs > 65535 || max_seq_len < 1 || max_batch < 1 || max_chunk < 1 ||
+      kv_pool_bytes < 0)
+    return fail(PDEC_INVALID_ARG, "limits must be positive (max_seqs <= 65535)");
+  WsLayout L;
+  make_layout(cfg, max_seqs, max_seq_len, max_batch, max_chunk, &L);
+  return (int64_t)L.total;
+}
+
+int engine_create(const pdec_model_cfg* cfg, const pdec_weights* w, void* kv_pool,
+                  int64_t kv_pool_bytes, int32_t max_seqs, int32_t max_seq_len, int32_t max_batch,
+                  int32_t max_chunk, void* workspace, int64_t workspace_bytes, void* stream,
+                  pdec_engine** out) {
+  int rc = check_cfg(cfg);
+  if (rc != PDEC_OK) return rc;
+  if (!w || !kv_pool || !workspace || !out) return fail(PDEC_INVALID_ARG, "null pointer argument");
+  if (max_seqs < 1 || max_seqs > 65535 || max_seq_len < 1 || max_batch < 1 || max_chunk < 1)
+    return fail(PDEC_INVALID_ARG, "limits must be positive (max_seqs <= 65535)");
+  if (!w->embed || !w->lm_head || !w->final_norm || !w->attn_norm || !w->wq || !w->wk ||
+      !w->wv || !w->wo || !w->ffn_norm || !w->w_gate || !w->w_up || !w->w_down)
+    return fail(PDEC_INVALID_ARG, "null weight pointer");
+  for (int l = 0; l < cfg->n_layers; ++l)
+    if (!w->attn_norm[l] || !w->wq[l] || !w->wk[l] || !w->wv[l] || !w->wo[l] ||
+        !w->ffn_norm[l] || !w->w_gate[l] || !w->w_up[l] || !w->w_down[l])
+      return fail(PDEC_INVALID_ARG, "null weight pointer in layer " + std::to_string(l));
+  const int64_t page_bytes = kv_token_bytes(cfg) * kPage;
+  const int64_t n_pages = kv_pool_bytes / page_bytes;
+  if (n_pages < 1 || n_pages > INT32_MAX)
+    return fail(PDEC_INVALID_ARG, "kv_pool_bytes must hold between 1 and 2^31-1 pages");
+  WsLayout L;
+  make_layout(cfg, max_seqs, max_seq_len, max_batch, max_chunk, &L);
+  if (workspace_bytes < (int64_t)L.total)
+    return fail(PDEC_INVALID_ARG, "workspace too small: need " + std::to_string(L.total));
+
+  auto* E = new pdec_engine();
+  E->cfg = *cfg;
+  E->embed = w->embed;
+  E->lm_head = w->lm_head;
+  E->final_norm = w->final_norm;
+  const int qd = cfg->n_q_heads * cfg->head_dim, kvd = cfg->n_kv_heads * cfg->head_dim;
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    E->attn_norm.push_back(w->attn_norm[l]);
+    E->ffn_norm.push_back(w->ffn_norm[l]);
+    WSegs a{};
+    a.ptr[0] = w->wq[l];
+    a.ptr[1] = w->wk[l];
+    a.ptr[2] = w->wv[l];
+    a.row_end[0] = qd;
+    a.row_end[1] = qd + kvd;
+    a.row_end[2] = qd + 2 * kvd;
+    a.n_seg = 3;
+    E->w_qkv.push_back(a);
+    WSegs o{};
+    o.ptr[0] = w->wo[l];
+    o.row_end[0] = cfg->d_model;
+    o.n_seg = 1;
+    E->w_o.push_back(o);
+    WSegs gu{};
+    gu.ptr[0] = w->w_gate[l];
+    gu.ptr[1] = w->w_up[l];
+    gu.row_end[0] = cfg->ffn_dim;
+    gu.row_end[1] = 2 * cfg->ffn_dim;
+    gu.n_seg = 2;
+    E->w_gu.push_back(gu);
+    WSegs dn{};
+    dn.ptr[0] = w->w_down[l];
+    dn.row_end[0] = cfg->d_model;
+    dn.n_seg = 1;
+    E->w_down.push_back(dn);
+  }
+  E->kv_pool = (char*)kv_pool;
+  E->n_pages = n_pages;
+  E->page_stride = (int64_t)cfg->n_kv_heads * kPage * cfg->head_dim;
+  E->pool = new PagePool((int32_t)n_pages, max_seqs, max_seq_len);
+  E->max_batch = max_batch;
+  E->max_chunk = max_chunk;
+  E->ws = L;
+  E->base = (char*)workspace;
+  E->rope_cs = (float2*)(E->base + L.rope);
+  E->bt = (int32_t*)(E->base + L.bt);
+  E->meta = E->base + L.meta;
+  E->delta = (BtDelta*)(E->base + L.delta);
+  E->x = (float*)(E->base + L.x);
+  E->h = E->base + L.h;
+  E->o = E->base + L.o;
+  E->u = E->base + L.u;
+  E->q = E->base + L.q;
+  E->part = (float*)(E->base + L.part);
+  E->att_ml = (float*)(E->base + L.att_ml);
+  E->att_acc = (float*)(E->base + L.att_acc);
+  E->stream = (hipStream_t)stream;
+  E->mark.assign(max_seqs, 0);
+
+  auto cleanup = [&](int code, const std::string& msg) {
+    delete E->pool;
+    delete E;
+    return fail(code, msg);
+  };
+  hipError_t e = E->staging.init(std::max<size_t>(L.meta_bytes, L.delta_cap * sizeof(BtDelta)), 4);
+  if (e != hipSuccess) return cleanup(PDEC_HIP_ERROR, std::string("staging: ") + hipGetErrorString(e));
+  // Unwritten block-table entries read as page 0 rather than as garbage.
+  e = hipMemsetAsync(E->bt, 0, (size_t)max_seqs * L.bt_stride * 4, E->stream);
+  if (e == hipSuccess)
+    e = launch_rope_table(max_seq_len, cfg->head_dim, (double)cfg->rope_base, E->rope_cs,
+                          E->stream);
+  if (e != hipSuccess) return cleanup(PDEC_HIP_ERROR, std::string("init: ") + hipGetErrorString(e));
+  *out = E;
+  return PDEC_OK;
+}
+
+void engine_destroy(pdec_engine* E) {
+  if (!E) return;
+  (void)hipStreamSynchronize(E->stream);
+  E->staging.release();
+  delete E->pool;
+  delete E;
+}
+
+int engine_profile(pdec_engine* E, int32_t enable) {
+  if (!E) return fail(PDEC_INVALID_ARG, "null engine");
+  E->timer.enable(enable != 0);
+  return PDEC_OK;
+}
+
+int engine_profile_read(pdec_engine* E, int32_t kind, double* total_ms, int64_t* launches) {
+  if (!E || !total_ms || !launches) return fail(PDEC_INVALID_ARG, "null argument");
+  if (kind < PDEC_TIMER_ATTENTION || kind > PDEC_TIMER_LM_HEAD)
+    return fail(PDEC_INVALID_ARG, "unknown timer kind");
+  HIP_OR_FAIL(E->timer.read(kind, total_ms, launches));
+  return PDEC_OK;
+}
+
+int engine_set_stream(pdec_engine* E, void* stream) {
+  if (!E) return fail(PDEC_INVALID_ARG, "null engine");
+  E->stream = (hipStream_t)stream;
+  return PDEC_OK;
+}
+
+int kv_alloc(pdec_engine* E, int32_t reserve_tokens, int32_t* seq_out) {
+  if (!E || !seq_out) return fail(PDEC_INVALID_ARG, "null argument");
+  Status st = E->pool->alloc_seq(reserve_tokens, seq_out);
+  return st.good() ? PDEC_OK : fail(st.code, st.msg);
+}
+
+int kv_free(pdec_engine* E, int32_t seq) {
+  if (!E) return fail(PDEC_INVALID_ARG, "null engine");
+  Status st = E->pool->free_seq(seq);
+  return st.good() ? PDEC_OK : fail(st.code, st.msg);
+}
+
+int kv_len(pdec_engine* E, int32_t seq, int32_t* len_out) {
+  if (!E || !len_out) return fail(PDEC_INVALID_ARG, "null argument");
+  int32_t slot;
+  Status st = E->pool->resolve(seq, &slot);
+  if (!st.good()) return fail(st.code, st.msg);
+  *len_out = E->pool->len(slot);
+  return PDEC_OK;
+}
+
+int kv_headroom(pdec_engine* E, int64_t* free_tokens_out) {
+  if (!E || !free_tokens_out) return fail(PDEC_INVALID_ARG, "null argument");
+  *free_tokens_out = E->pool->headroom_tokens();
+  return PDEC_OK;
+}
+
+int kv_block_table(pdec_engine* E, int32_t seq, int32_t* pages_out, int32_t capacity,
+                   int32_t* n_out) {
+  if (!E || !n_out) return fail(PDEC_INVALID_ARG, "null argument");
+  int32_t slot;
+  Status st = E->pool->resolve(seq, &slot);
+  if (!st.good()) return fail(st.code, st.msg);
+  const auto& pg = E->pool->pages(slot);
+  *n_out = (int32_t)pg.size();
+  if ((int64_t)pg.size() > capacity || (!pages_out && !pg.empty()))
+    return fail(PDEC_INVALID_ARG, "capacity too small for the block table");
+  if (!pg.empty()) std::memcpy(pages_out, pg.data(), pg.size() * 4);
+  return PDEC_OK;
+}
+
+int kv_extend_uninit(pdec_engine* E, int32_t seq, int32_t n_tokens) {
+  if (!E) return fail(PDEC_INVALID_ARG, "null engine");
+  if (n_tokens < 0) return fail(PDEC_INVALID_ARG, "n_tokens must be >= 0");
+  int32_t slot;
+  Status st = E->pool->resolve(seq, &slot);
+  if (!st.good()) return fail(st.code, st.msg);
+  st = E->pool->grow(&slot, 1, n_tokens);
+  return st.good() ? PDEC_OK : fail(st.code, st.msg);
+}
+
+int decode_step(pdec_engine* E, int32_t B, const int32_t* ids, const int32_t* tokens_dev,
+                float* logits) {
+  if (!E || !ids || !tokens_dev || !logits) return fail(PDEC_INVALID_ARG, "null argument");
+  if (B < 1 || B > E->max_batch)
+    return fail(PDEC_INVALID_ARG, "batch " + std::to_string(B) + " outside [1, max_batch]");
+  std::vector<int32_t> slots(B);
+  if (++E->epoch == INT32_MAX) {
+    std::fill(E->mark.begin(), E->mark.end(), 0);
+    E->epoch = 1;
+  }
+  for (int b = 0; b < B; ++b) {
+    Status st = E->pool->resolve(ids[b], &slots[b]);
+    if (!st.good()) return fail(st.code, st.msg);
+    if (E->mark[slots[b]] == E->epoch)
+      return fail(PDEC_INVALID_ARG, "sequence id repeated in the batch");
+    E->mark[slots[b]] = E->epoch;
+  }
+  PagePool::GrowUndo undo;
+  Status st = E->pool->grow(slots.data(), B, 1, &undo);
+  if (!st.good()) return fail(st.code, st.msg);
+
+  std::vector<RowMeta> rows(B);
+  std::vector<QBlockSpec> specs(B);
+  for (int b = 0; b < B; ++b) {
+    const int32_t pos = E->pool->len(slots[b]) - 1;
+    rows[b] = {slots[b], pos};
+    specs[b] = {b, 1, slots[b], pos};
+  }
+  std::vector<AttnQBlock> qblocks;
+  std::vector<AttnItem> items;
+  plan_attention(specs, choose_split_pages(total_key_pages(specs), E->cfg.n_kv_heads), &qblocks, &items);
+  int rc = enqueue_forward(E, B, rows, qblocks, items, tokens_dev, nullptr, logits, false);
+  if (rc != PDEC_OK) E->pool->undo(undo);
+  return rc;
+}
+
+int kv_append_prefix(pdec_engine* E, int32_t seq, const int32_t* tokens_host, int32_t n,
+                     int32_t chunk_tokens, float* last_logits_dev) {
+  if (!E || !tokens_host) return fail(PDEC_INVALID_ARG, "null argument");
+  if (n < 1) return fail(PDEC_INVALID_ARG, "n must be >= 1");
+  if (chunk_tokens < 1 || chunk_tokens > E->max_chunk)
+    return fail(PDEC_INVALID_ARG, "chunk_tokens outside [1, max_chunk]");
+  for (int i = 0; i < n; ++i)
+    if (tokens_host[i] < 0 || tokens_host[i] >= E->cfg.vocab)
+      return fail(PDEC_INVALID_ARG, "token id outside [0, vocab)");
+  int32_t slot;
+  Status st = E->pool->resolve(seq, &slot);
+  if (!st.good()) return fail(st.code, st.msg);
+  const int32_t len0 = E->pool->len(slot);
+  PagePool::GrowUndo undo;
+  st = E->pool->grow(&slot, 1, n, &undo);
+  if (!st.good()) return fail(st.code, st.msg);
+
+  const int QB = 16 / (E->cfg.n_q_heads / E->cfg.n_kv_heads);
+  std::vector<RowMeta> rows;
+  std::vector<QBlockSpec> specs;
+  std::vector<AttnQBlock> qblocks;
+  std::vector<AttnItem> items;
+  for (int32_t c0 = 0; c0 < n; c0 += chunk_tokens) {
+    const int C = std::min(chunk_tokens, n - c0);
+    rows.resize(C);
+    for (int i = 0; i < C; ++i) rows[i] = {slot, len0 + c0 + i};
+    specs.clear();
+    for (int k = 0; k * QB < C; ++k)
+      specs.push_back({k * QB, std::min(QB, C - k * QB), slot, len0 + c0 + k * QB});
+    plan_attention(specs, choose_split_pages(total_key_pages(specs), E->cfg.n_kv_heads), &qblocks, &items);
+    const bool last = c0 + C >= n;
+    int rc = enqueue_forward(E, C, rows, qblocks, items, nullptr, tokens_host + c0,
+                             last ? last_logits_dev : nullptr, true);
+    if (rc != PDEC_OK) {
+      E->pool->undo(undo);
+      return rc;
+    }
+  }
+  return PDEC_OK;
+}
+
+int sample(pdec_engine* E, int32_t B, const float* logits_dev, int32_t* tokens_dev_out,
+           int32_t mode) {
+  if (!E || !logits_dev || !tokens_dev_out) return fail(PDEC_INVALID_ARG, "null argument");
+  if (mode != 0) return fail(PDEC_UNSUPPORTED, "only greedy sampling (mode 0) is implemented");
+  if (B < 1) return fail(PDEC_INVALID_ARG, "batch must be >= 1");
+  HIP_OR_FAIL(launch_argmax(B, E->cfg.vocab, logits_dev, tokens_dev_out, E->stream));
+  return PDEC_OK;
+}
+
+int64_t paged_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                        int32_t head_dim, int64_t max_total_tokens) {
+  (void)max_total_tokens;
+  if (batch < 1 || n_q_heads < 1 || n_kv_heads < 1 || head_dim < 1)
+    return fail(PDEC_INVALID_ARG, "sizes must be positive");
+  const int64_t items_cap = attn_target_items(n_kv_heads) + batch + 16;
+  return (int64_t)(align_up(batch * sizeof(AttnQBlock)) + align_up(items_cap * sizeof(AttnItem)) +
+                   align_up(items_cap * n_kv_heads * 16 * 2 * 4) +
+                   align_up(items_cap * n_kv_heads * 16 * (int64_t)head_dim * 4));
+}
+
+int paged_decode_attention(int32_t dtype, int32_t B, int32_t Hq, int32_t Hkv, int32_t Dh,
+                           const void* q, const void* k_pages, const void* v_pages,
+                           const int32_t* bt, int32_t bt_stride, const int32_t* lens,
+                           float* out, void* workspace, int64_t ws_bytes, void* stream) {
+  if (!q || !k_pages || !v_pages || !bt || !lens || !out || !workspace)
+    return fail(PDEC_INVALID_ARG, "null argument");
+  if (dtype != PDEC_F32 && dtype != PDEC_BF16) return fail(PDEC_INVALID_ARG, "bad dtype");
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || bt_stride < 1)
+    return fail(PDEC_INVALID_ARG, "bad sizes");
+  if (16 % (Hq / Hkv)) return fail(PDEC_UNSUPPORTED, "GQA group size must divide 16");
+  if (Dh != 64 && Dh != 128) return fail(PDEC_UNSUPPORTED, "head_dim must be 64 or 128");
+  const int64_t need = paged_attention_workspace_bytes(B, Hq, Hkv, Dh, 0);
+  if (ws_bytes < need) return fail(PDEC_INVALID_ARG, "workspace too small: need " + std::to_string(need));
+  std::vector<QBlockSpec> specs(B);
+  for (int b = 0; b < B; ++b) {
+    if (lens[b] < 1 || (int64_t)lens[b] > (int64_t)bt_stride * kPage)
+      return fail(PDEC_INVALID_ARG, "lens[b] outside [1, bt_stride*16]");
+    specs[b] = {b, 1, b, lens[b] - 1};
+  }
+  std::vector<AttnQBlock> qblocks;
+  std::vector<AttnItem> items;
+  plan_attention(specs, choose_split_pages(total_key_pages(specs), Hkv), &qblocks, &items);
+
+  const int64_t items_cap = attn_target_items(Hkv) + B + 16;
+  if ((int64_t)items.size() > items_cap) return fail(PDEC_INVALID_ARG, "work list too large");
+  char* base = (char*)workspace;
+  const size_t o_qb = 0;
+  const size_t o_it = align_up(B * sizeof(AttnQBlock));
+  const size_t o_ml = o_it + align_up(items_cap * sizeof(AttnItem));
+  const size_t o_acc = o_ml + align_up(items_cap * Hkv * 16 * 2 * 4);
+  std::vector<char> hm(o_ml);
+  std::memcpy(hm.data() + o_qb, qblocks.data(), qblocks.size() * sizeof(AttnQBlock));
+  std::memcpy(hm.data() + o_it, items.data(), items.size() * sizeof(AttnItem));
+  hipStream_t s = (hipStream_t)stream;
+  {
+    std::lock_guard<std::mutex> lk(g_attn_mu);
+    if (!g_attn_staging) {
+      auto* st = new Staging();
+      hipError_t e = st->init(1 << 20, 4);
+      if (e != hipSuccess) {
+        delete st;
+        return fail(PDEC_HIP_ERROR, std::string("staging: ") + hipGetErrorString(e));
+      }
+      g_attn_staging = st;
+    }
+    HIP_OR_FAIL(g_attn_staging->upload(base, hm.data(), o_ml, s));
+  }
+  const int64_t page_stride = (int64_t)Hkv * kPage * Dh;
+  HIP_OR_FAIL(launch_attention_split(dtype, Dh, (int)items.size(), Hq, Hkv,
+                                     (const AttnItem*)(base + o_it),
+                                     (const AttnQBlock*)(base + o_qb), q, k_pages, v_pages,
+                                     page_stride, bt, bt_stride, (float*)(base + o_ml),
+                                     (float*)(base + o_acc), s));
+  HIP_OR_FAIL(launch_attention_combine(Dh, B, Hq, Hkv, (const AttnQBlock*)(base + o_qb),
+                                       (float*)(base + o_ml), (float*)(base + o_acc), out, 0, s));
+  return PDEC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,75 @@
+// Host-callable launchers of the gfx950 kernels.  Every launcher only
+// enqueues on the given stream; argument checks are the caller's job (the
+// engine validates shapes before any launch).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "meta.h"
+
+namespace pdec {
+
+// Weight matrix made of up to 3 row segments stacked along N (e.g. q|k|v or
+// gate|up).  Segment s covers output columns [row_end[s-1], row_end[s]).
+struct WSegs {
+  const void* ptr[3];
+  int32_t row_end[3];
+  int32_t n_seg;
+};
+
+// ---- attention --------------------------------------------------------------
+// Split pass: one work group per (item, KV head).  Writes per-row partial
+// softmax statistics part_ml [items][Hkv][16][2] = (max in log2 units, sum)
+// and unnormalised outputs part_acc [items][Hkv][16][head_dim].
+hipError_t launch_attention_split(int dtype, int head_dim, int n_items, int n_q_heads,
+                                  int n_kv_heads, const AttnItem* items,
+                                  const AttnQBlock* qblocks, const void* q, const void* k_pages,
+                                  const void* v_pages, int64_t page_stride_elems,
+                                  const int32_t* block_table, int32_t bt_stride, float* part_ml,
+                                  float* part_acc, hipStream_t stream);
+
+// Merge pass: one work group per (query block, query head); writes
+// out [rows][n_q_heads][head_dim] as fp32 (out_bf16 = 0) or bf16.
+hipError_t launch_attention_combine(int head_dim, int n_qblocks, int n_q_heads, int n_kv_heads,
+                                    const AttnQBlock* qblocks, const float* part_ml,
+                                    const float* part_acc, void* out, int out_bf16,
+                                    hipStream_t stream);
+
+// ---- projections ------------------------------------------------------------
+// out[s][m][n] = sum_{k in split s} A[m][k] * W[n][k]  (fp32 partial sums).
+// bf16: A and W bf16, K % 64 == 0, k_split % 64 == 0.  f32: any sizes.
+hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t lda,
+                       const WSegs& w, float* out, int splits, int k_split, hipStream_t stream);
+// Number of K splits the launcher plans for this shape (and the split size).
+int gemm_plan_splits(int dtype, int M, int N, int K, int* k_split);
+
+// ---- per-row and elementwise steps -------------------------------------------
+// x[m] = E[tok[m]];  h[m] = rmsnorm(x[m]) * gain.  Ids are clamped to [0, vocab).
+hipError_t launch_embed_norm(int dtype, int M, int d, int vocab, const int32_t* tokens,
+                             const void* embed,
+                             const float* gain, float eps, float* x, void* h, hipStream_t stream);
+// x[m] += sum_s part[s][m];  h[m] = rmsnorm(x[m]) * gain.
+hipError_t launch_resid_norm(int dtype, int M, int d, const float* part, int splits, float* x,
+                             const float* gain, float eps, void* h, hipStream_t stream);
+// Sum the q|k|v partials, rotate q and k at each row's position (cos/sin
+// table [pos][head_dim/2] of float2), write q to q_out [M][Hq][Dh] and k, v
+// into the row's page slot of this layer's pool.
+hipError_t launch_qkv_rope_kv(int dtype, int M, int head_dim, int n_q_heads, int n_kv_heads,
+                              const float* part, int splits, const RowMeta* rows,
+                              const float2* rope_cs, const int32_t* block_table, int32_t bt_stride,
+                              void* q_out, void* k_pages, void* v_pages, int64_t page_stride_elems,
+                              hipStream_t stream);
+// u[m][n] = silu(g) * up with g, up the summed partials of columns n and F+n.
+hipError_t launch_swiglu(int dtype, int M, int F, const float* part, int splits, void* u,
+                         hipStream_t stream);
+// tokens[b] = argmax_v logits[b][v] (lowest index on ties).
+hipError_t launch_argmax(int B, int V, const float* logits, int32_t* tokens, hipStream_t stream);
+// bt[d.slot * stride + d.idx] = d.page for each delta.
+hipError_t launch_bt_deltas(int n, const BtDelta* deltas, int32_t* bt, int32_t stride,
+                            hipStream_t stream);
+// cs[p][i] = (cos, sin)(p * base^(-2i/Dh)) evaluated in double precision.
+hipError_t launch_rope_table(int max_pos, int head_dim, double base, float2* cs,
+                             hipStream_t stream);
+
+}  // namespace pdec

@@ -1,0 +1,108 @@
+// Host-side page pool, resident-set table and attention work planner.
+//
+// Pure C++ (no HIP): it compiles with g++ into a host-only test library as
+// well as into the device library.  It owns the bookkeeping of the paged KV
+// cache: which physical page holds which 16-token block of which sequence,
+// the free list, reservations, and sequence ids with generation counters.
+#pragma once
+
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "meta.h"
+
+namespace pdec {
+
+struct Status {
+  int code = 0;
+  std::string msg;
+  static Status ok() { return {}; }
+  static Status err(int c, std::string m) { return {c, std::move(m)}; }
+  bool good() const { return code == 0; }
+};
+
+class PagePool {
+ public:
+  PagePool(int32_t n_pages, int32_t max_seqs, int32_t max_seq_len);
+
+  int32_t n_pages() const { return n_pages_; }
+  int32_t max_seqs() const { return max_seqs_; }
+  int32_t max_seq_len() const { return max_seq_len_; }
+  int32_t max_pages_per_seq() const { return max_pages_per_seq_; }
+  int64_t free_pages() const { return (int64_t)free_.size(); }
+  int64_t headroom_tokens() const { return free_pages() * kPage; }
+
+  // Admit an empty sequence with ceil(reserve_tokens/16) reserved pages.
+  Status alloc_seq(int32_t reserve_tokens, int32_t* id_out);
+  // Departure: return every page of the sequence to the free list.
+  Status free_seq(int32_t id);
+  // Resolve an id to its slot; BAD_SEQ if unknown or stale.
+  Status resolve(int32_t id, int32_t* slot) const;
+
+  int32_t len(int32_t slot) const { return seqs_[slot].len; }
+  const std::vector<int32_t>& pages(int32_t slot) const { return seqs_[slot].pages; }
+
+  // Record of one grow() call, enough to take it back.
+  struct GrowUndo {
+    std::vector<int32_t> slots, old_len, old_npages;
+    size_t old_pending = 0;
+  };
+
+  // Make room for `extra` more tokens on each listed slot and advance the
+  // lengths.  All-or-nothing: on failure nothing changes.  The block-table
+  // entries of newly attached pages are appended to the pending list.
+  Status grow(const int32_t* slots, int32_t n, int32_t extra, GrowUndo* undo = nullptr);
+  // Take back a successful grow() (used when enqueueing device work fails).
+  void undo(const GrowUndo& u);
+
+  // Block-table entries written on the host but not yet on the device, in
+  // the order they were made.
+  const std::vector<BtDelta>& pending() const { return pending_; }
+  void clear_pending() { pending_.clear(); }
+
+  // Pages needed to hold `tokens` tokens.
+  static int32_t pages_for(int64_t tokens) { return (int32_t)((tokens + kPage - 1) / kPage); }
+
+ private:
+  struct Seq {
+    bool live = false;
+    int32_t gen = 0;
+    int32_t len = 0;
+    std::vector<int32_t> pages;  // logical order; may exceed pages_for(len) (reserve)
+  };
+  int32_t make_id(int32_t slot) const { return (seqs_[slot].gen << 16) | slot; }
+
+  int32_t n_pages_, max_seqs_, max_seq_len_, max_pages_per_seq_;
+  std::vector<int32_t> free_;        // stack of free page ids
+  std::vector<int32_t> free_slots_;  // stack of free sequence slots
+  std::vector<Seq> seqs_;
+  std::vector<BtDelta> pending_;
+};
+
+// Query block description given to the planner.
+struct QBlockSpec {
+  int32_t q_row0, n_q, slot, pos0;
+};
+
+// Work groups the attention split pass aims for.
+constexpr int64_t kAttnTargetGroups = 16384;
+
+// Items per KV head the planner aims for.
+int64_t attn_target_items(int32_t n_kv_heads);
+
+// Split size (in pages, even, at least 8) for a key-axis workload of
+// `total_pages` (summed over query blocks): the item count stays within
+// attn_target_items(n_kv_heads) plus one per query block.
+int32_t choose_split_pages(int64_t total_pages, int32_t n_kv_heads);
+
+// Cut every query block's key range [0, pos0 + n_q) into items of
+// `split_pages` pages.  Fills qblocks (with item ranges) and items.
+void plan_attention(const std::vector<QBlockSpec>& specs, int32_t split_pages,
+                    std::vector<AttnQBlock>* qblocks, std::vector<AttnItem>* items);
+
+// Total pages touched by the query blocks (the key-axis workload).
+int64_t total_key_pages(const std::vector<QBlockSpec>& specs);
+
+}  // namespace pdec

@@ -1,0 +1,253 @@
+"""Thin torch-facing binding of the C ABI (argument marshalling only).
+
+Torch supplies device memory and the current stream; every step of the
+decoder runs in the library's HIP kernels.  Function and method names follow
+the C ABI: kv_alloc, kv_append_prefix, decode_step, sample, kv_free,
+kv_len, kv_headroom, paged_decode_attention.
+"""
+
+from __future__ import annotations
+
+import ctypes
+from ctypes import POINTER, byref, c_int32, c_int64, c_void_p
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import _native as N
+from ._native import PAGE_TOKENS, PdecError
+
+_TORCH_DTYPE = {N.F32: torch.float32, N.BF16: torch.bfloat16}
+
+
+def _stream_handle(stream: Optional[torch.cuda.Stream]) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def model_cfg(shape, dtype: int) -> N.ModelCfg:
+    """C struct for a shape object exposing the ModelCfg field names."""
+    return N.ModelCfg(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads,
+                      shape.head_dim, shape.ffn_dim, shape.vocab, float(shape.rms_eps),
+                      float(shape.rope_base), dtype)
+
+
+def kv_bytes_per_token(shape, dtype: int) -> int:
+    cfg = model_cfg(shape, dtype)
+    return N.check(N.load().kv_bytes_per_token(byref(cfg)))
+
+
+def weights_to_device(arrays: Dict, dtype: int, device="cuda") -> Dict:
+    """Copy a weight dict (numpy, nn.Linear layout) to device tensors.
+
+    Matrices go to the storage dtype (bf16 inputs must already be
+    bf16-representable, so the cast is exact); norm gains stay fp32.
+    """
+    td = _TORCH_DTYPE[dtype]
+    mat = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(
+        device=device).to(td).contiguous()
+    vec = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device)
+    out = {"embed": mat(arrays["embed"]), "lm_head": mat(arrays["lm_head"]),
+           "final_norm": vec(arrays["final_norm"]), "layers": []}
+    for lay in arrays["layers"]:
+        d = {k: mat(lay[k]) for k in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")}
+        d["attn_norm"] = vec(lay["attn_norm"])
+        d["ffn_norm"] = vec(lay["ffn_norm"])
+        out["layers"].append(d)
+    return out
+
+
+class Engine:
+    """One rollout worker's decode backend over caller-owned device memory."""
+
+    def __init__(self, shape, weights: Dict, dtype: int, kv_pool_bytes: int, max_seqs: int,
+                 max_seq_len: int, max_batch: int, max_chunk: int, device="cuda",
+                 stream: Optional[torch.cuda.Stream] = None):
+        self.lib = N.load()
+        self.shape = shape
+        self.dtype = dtype
+        self.cfg = model_cfg(shape, dtype)
+        self.weights = weights  # keep the tensors alive
+        self.kv_token_bytes = N.check(self.lib.kv_bytes_per_token(byref(self.cfg)))
+        page_bytes = self.kv_token_bytes * PAGE_TOKENS
+        self.n_pages = int(kv_pool_bytes // page_bytes)
+        self.kv_pool = torch.empty(self.n_pages * page_bytes, dtype=torch.uint8, device=device)
+        ws = N.check(self.lib.engine_workspace_bytes(byref(self.cfg), max_seqs, max_seq_len,
+                                                     max_batch, max_chunk,
+                                                     self.kv_pool.numel()))
+        self.workspace = torch.empty(ws, dtype=torch.uint8, device=device)
+        L = shape.n_layers
+
+        def arr(key):
+            a = (c_void_p * L)(*[weights["layers"][i][key].data_ptr() for i in range(L)])
+            return ctypes.cast(a, POINTER(c_void_p)), a
+
+        self._keep = []
+        fields = {}
+        for key in ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down"):
+            p, a = arr(key)
+            self._keep.append(a)
+            fields[key] = p
+        self.cw = N.Weights(embed=weights["embed"].data_ptr(),
+                            lm_head=weights["lm_head"].data_ptr(),
+                            final_norm=weights["final_norm"].data_ptr(), **fields)
+        h = c_void_p()
+        N.check(self.lib.engine_create(byref(self.cfg), byref(self.cw), self.kv_pool.data_ptr(),
+                                       self.kv_pool.numel(), max_seqs, max_seq_len, max_batch,
+                                       max_chunk, self.workspace.data_ptr(),
+                                       self.workspace.numel(), _stream_handle(stream), byref(h)))
+        self.handle = h
+        self.max_batch, self.max_chunk = max_batch, max_chunk
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self.lib.engine_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ---- pool views (layout [layer][K|V][page][Hkv][16 * Dh]) -------------
+    def _pool_view(self):
+        s = self.shape
+        t = self.kv_pool.view(_TORCH_DTYPE[self.dtype])
+        return t.view(s.n_layers, 2, self.n_pages, s.n_kv_heads, PAGE_TOKENS * s.head_dim)
+
+    def k_pages(self, layer: int) -> torch.Tensor:
+        """[pages][Hkv][16][Dh] view of one layer's K pages."""
+        s = self.shape
+        return self._pool_view()[layer, 0].view(self.n_pages, s.n_kv_heads, PAGE_TOKENS,
+                                                s.head_dim)
+
+    def v_pages(self, layer: int) -> torch.Tensor:
+        """[pages][Hkv][Dh][16] view of one layer's V pages (transposed per page)."""
+        s = self.shape
+        return self._pool_view()[layer, 1].view(self.n_pages, s.n_kv_heads, s.head_dim,
+                                                PAGE_TOKENS)
+
+    def profile(self, enable: bool) -> None:
+        """Bracket timed launch classes with HIP events (see engine_profile)."""
+        N.check(self.lib.engine_profile(self.handle, int(bool(enable))))
+
+    def profile_read(self, kind: int):
+        """(total ms, launch count) of one timed class since the last read."""
+        ms, n = ctypes.c_double(), c_int64()
+        N.check(self.lib.engine_profile_read(self.handle, int(kind), byref(ms), byref(n)))
+        return ms.value, n.value
+
+    def set_stream(self, stream: Optional[torch.cuda.Stream] = None):
+        N.check(self.lib.engine_set_stream(self.handle, _stream_handle(stream)))
+
+    # ---- resident set --------------------------------------------------------
+    def kv_alloc(self, reserve_tokens: int = 0) -> int:
+        out = c_int32()
+        N.check(self.lib.kv_alloc(self.handle, int(reserve_tokens), byref(out)))
+        return out.value
+
+    def kv_free(self, seq: int) -> None:
+        N.check(self.lib.kv_free(self.handle, int(seq)))
+
+    def kv_len(self, seq: int) -> int:
+        out = c_int32()
+        N.check(self.lib.kv_len(self.handle, int(seq), byref(out)))
+        return out.value
+
+    def kv_headroom(self) -> int:
+        out = c_int64()
+        N.check(self.lib.kv_headroom(self.handle, byref(out)))
+        return out.value
+
+    def kv_block_table(self, seq: int) -> np.ndarray:
+        n = c_int32()
+        cap = self.n_pages
+        buf = (c_int32 * max(cap, 1))()
+        N.check(self.lib.kv_block_table(self.handle, int(seq), buf, cap, byref(n)))
+        return np.frombuffer(buf, dtype=np.int32, count=n.value).copy()
+
+    def kv_extend_uninit(self, seq: int, n_tokens: int) -> None:
+        N.check(self.lib.kv_extend_uninit(self.handle, int(seq), int(n_tokens)))
+
+    # ---- compute -------------------------------------------------------------
+    def kv_append_prefix(self, seq: int, tokens: Sequence[int], chunk_tokens: int,
+                         last_logits: Optional[torch.Tensor] = None) -> None:
+        tok = np.ascontiguousarray(np.asarray(tokens, dtype=np.int32))
+        if last_logits is not None:
+            assert last_logits.is_cuda and last_logits.dtype == torch.float32
+            assert last_logits.numel() >= self.shape.vocab and last_logits.is_contiguous()
+        N.check(self.lib.kv_append_prefix(self.handle, int(seq),
+                                          tok.ctypes.data_as(POINTER(c_int32)), len(tok),
+                                          int(chunk_tokens), _ptr(last_logits)))
+
+    def decode_step(self, seq_ids: Sequence[int], tokens: torch.Tensor,
+                    logits: torch.Tensor) -> None:
+        ids = np.ascontiguousarray(np.asarray(seq_ids, dtype=np.int32))
+        B = len(ids)
+        assert tokens.is_cuda and tokens.dtype == torch.int32 and tokens.numel() >= B
+        assert logits.is_cuda and logits.dtype == torch.float32 and logits.is_contiguous()
+        assert logits.numel() >= B * self.shape.vocab and tokens.is_contiguous()
+        N.check(self.lib.decode_step(self.handle, B, ids.ctypes.data_as(POINTER(c_int32)),
+                                     tokens.data_ptr(), logits.data_ptr()))
+
+    def sample(self, logits: torch.Tensor, tokens_out: torch.Tensor, mode: int = 0,
+               batch: Optional[int] = None) -> None:
+        B = batch if batch is not None else logits.shape[0]
+        assert logits.is_cuda and logits.dtype == torch.float32 and logits.is_contiguous()
+        assert tokens_out.is_cuda and tokens_out.dtype == torch.int32
+        assert tokens_out.numel() >= B and logits.numel() >= B * self.shape.vocab
+        N.check(self.lib.sample(self.handle, int(B), logits.data_ptr(), tokens_out.data_ptr(),
+                                int(mode)))
+
+
+def paged_attention_workspace_bytes(batch: int, n_q_heads: int, n_kv_heads: int,
+                                    head_dim: int) -> int:
+    return N.check(N.load().paged_attention_workspace_bytes(batch, n_q_heads, n_kv_heads,
+                                                            head_dim, 0))
+
+
+def paged_decode_attention(q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tensor,
+                           block_table: torch.Tensor, lens: Sequence[int], out: torch.Tensor,
+                           workspace: Optional[torch.Tensor] = None,
+                           stream: Optional[torch.cuda.Stream] = None,
+                           check_pages: bool = True) -> torch.Tensor:
+    """Isolated paged decode attention; see include/pdec.h.
+
+    q [B][Hq][Dh] (bf16 or fp32), k_pages [P][Hkv][16][Dh], v_pages
+    [P][Hkv][Dh][16], block_table int32 [B][stride] on the device, lens on
+    the host, out fp32 [B][Hq][Dh].  With ``check_pages`` the page ids the
+    kernel will read are checked against the pool size first (one copy of the
+    block table to the host).
+    """
+    B, Hq, Dh = q.shape
+    P, Hkv, page, Dh2 = k_pages.shape
+    assert page == PAGE_TOKENS and Dh2 == Dh and tuple(v_pages.shape) == (P, Hkv, Dh, PAGE_TOKENS)
+    assert q.dtype == k_pages.dtype == v_pages.dtype
+    assert q.is_contiguous() and k_pages.is_contiguous() and v_pages.is_contiguous()
+    assert block_table.dtype == torch.int32 and block_table.dim() == 2
+    assert block_table.shape[0] == B and block_table.is_contiguous()
+    assert out.dtype == torch.float32 and tuple(out.shape) == (B, Hq, Dh) and out.is_contiguous()
+    dtype = N.BF16 if q.dtype == torch.bfloat16 else N.F32
+    assert dtype == N.BF16 or q.dtype == torch.float32
+    ln = np.ascontiguousarray(np.asarray(lens, dtype=np.int32))
+    assert ln.shape == (B,) and (ln >= 1).all() and (ln <= block_table.shape[1] * PAGE_TOKENS).all()
+    if check_pages:
+        bt = block_table.cpu().numpy()
+        for b in range(B):
+            used = bt[b, :(int(ln[b]) + PAGE_TOKENS - 1) // PAGE_TOKENS]
+            if used.size and (used.min() < 0 or used.max() >= P):
+                raise PdecError(N.INVALID_ARG, f"block table row {b} names a page outside the pool")
+    need = paged_attention_workspace_bytes(B, Hq, Hkv, Dh)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    N.check(N.load().paged_decode_attention(
+        dtype, B, Hq, Hkv, Dh, q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(),
+        block_table.data_ptr(), block_table.shape[1], ln.ctypes.data_as(POINTER(c_int32)),
+        out.data_ptr(), workspace.data_ptr(), workspace.numel(), _stream_handle(stream)))
+    return out

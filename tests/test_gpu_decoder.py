@@ -1,0 +1,237 @@
+"""The whole decode step and the chunked prefix path on the GPU, against the
+float64 oracle, through the C ABI.
+
+* tiny fp32 decoder (2 layers, d 256, 4/2 heads, Dh 64): prefixes of 17, 40,
+  96, 128 tokens, then 32 greedy steps, teacher-forced with the oracle's
+  tokens; 33 logit rows per trajectory within 1e-4 absolute;
+* bf16 decoders (small, and the 8B layer geometry with 2 layers): per-row
+  normwise 2e-2;
+* chunking, re-prefill after departure, batch-order invariance and atomic
+  failure of page growth.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import decoder as od
+from workload import (EIGHT_B, SMALL_BF16, TINY, ModelShape, make_weights, random_tokens)
+
+pytestmark = pytest.mark.gpu
+
+F32_TOL = 1e-4
+BF16_TOL = 2e-2
+
+
+def _P():
+    import paper_2609_36899_amd as P
+    return P
+
+
+def _engine(shape, arrays, bf16, pool_tokens=4096, max_seqs=8, max_seq_len=1024, max_batch=8,
+            max_chunk=64):
+    P = _P()
+    dt = P.BF16 if bf16 else P.F32
+    w = P.weights_to_device(arrays, dt)
+    per_tok = P.kv_bytes_per_token(shape, dt)
+    return P.Engine(shape, w, dt, pool_tokens * per_tok, max_seqs, max_seq_len, max_batch,
+                    max_chunk)
+
+
+def _logits_buf(rows, vocab):
+    return torch.empty((rows, vocab), dtype=torch.float32, device="cuda")
+
+
+def test_tiny_fp32_prefix_then_greedy_steps():
+    arrays = make_weights(TINY, seed=0)
+    dec = od.Decoder(od.ModelWeights.from_arrays(TINY, arrays))
+    E = _engine(TINY, arrays, bf16=False)
+    prefixes = [random_tokens(n, TINY.vocab, seed=100 + i) for i, n in enumerate([17, 40, 96, 128])]
+    seqs = [E.kv_alloc(16) for _ in prefixes]
+    states = [dec.new_state() for _ in prefixes]
+    ref_rows = [[] for _ in prefixes]
+    gpu_rows = [[] for _ in prefixes]
+    buf = _logits_buf(1, TINY.vocab)
+    for i, (s, toks) in enumerate(zip(seqs, prefixes)):
+        E.kv_append_prefix(s, toks, chunk_tokens=32, last_logits=buf)
+        gpu_rows[i].append(buf[0].cpu().numpy().copy())
+        ref_rows[i].append(dec.prefill(states[i], toks))
+    logits = _logits_buf(4, TINY.vocab)
+    gpu_tok = torch.empty(4, dtype=torch.int32, device="cuda")
+    for step in range(32):
+        nxt = [int(od.greedy(r[-1])) for r in ref_rows]  # teacher forcing
+        # greedy agreement on the GPU side where the oracle's top-2 gap is clear
+        E.sample(torch.from_numpy(np.stack([g[-1] for g in gpu_rows])).cuda(), gpu_tok)
+        gt = gpu_tok.cpu().numpy()
+        for i, r in enumerate(ref_rows):
+            top2 = np.sort(r[-1])[-2:]
+            if top2[1] - top2[0] > 4 * F32_TOL:
+                assert gt[i] == nxt[i], (step, i)
+        E.decode_step(seqs, torch.tensor(nxt, dtype=torch.int32, device="cuda"), logits)
+        got = logits.cpu().numpy()
+        for i in range(4):
+            gpu_rows[i].append(got[i].copy())
+            ref_rows[i].append(dec.step(states[i], nxt[i]))
+    for i in range(4):
+        g, r = np.stack(gpu_rows[i]), np.stack(ref_rows[i])
+        assert g.shape == (33, TINY.vocab)
+        err = np.max(np.abs(g - r))
+        assert err <= F32_TOL, (i, err)
+        assert E.kv_len(seqs[i]) == len(prefixes[i]) + 32
+
+
+def test_tiny_fp32_chunking_and_step_equivalence():
+    """kv_append_prefix with any chunk size equals feeding the tokens one at
+    a time through decode_step."""
+    arrays = make_weights(TINY, seed=1)
+    E = _engine(TINY, arrays, bf16=False)
+    toks = random_tokens(77, TINY.vocab, seed=7)
+    outs = []
+    for chunk in (1, 5, 16, 64):
+        s = E.kv_alloc(0)
+        buf = _logits_buf(1, TINY.vocab)
+        E.kv_append_prefix(s, toks, chunk_tokens=chunk, last_logits=buf)
+        outs.append(buf[0].cpu().numpy())
+        E.kv_free(s)
+    s = E.kv_alloc(0)
+    buf = _logits_buf(1, TINY.vocab)
+    for t in toks:
+        E.decode_step([s], torch.tensor([int(t)], dtype=torch.int32, device="cuda"), buf)
+    outs.append(buf[0].cpu().numpy())
+    ref = od.recompute_logits(od.ModelWeights.from_arrays(TINY, arrays), toks)[-1]
+    for o in outs:
+        assert np.max(np.abs(o - ref)) <= F32_TOL
+
+
+def test_reprefill_after_departure_matches_uninterrupted_run():
+    """The destination-side re-prefill fallback: a trajectory that departs and
+    is rebuilt from its tokens continues exactly as if it had stayed."""
+    arrays = make_weights(TINY, seed=2)
+    E = _engine(TINY, arrays, bf16=False)
+    toks = random_tokens(60, TINY.vocab, seed=8)
+    a = E.kv_alloc(0)
+    buf = _logits_buf(1, TINY.vocab)
+    E.kv_append_prefix(a, toks[:50], chunk_tokens=16)
+    for t in toks[50:]:
+        E.decode_step([a], torch.tensor([int(t)], dtype=torch.int32, device="cuda"), buf)
+    stay = buf[0].cpu().numpy().copy()
+    h0 = E.kv_headroom()
+    E.kv_free(a)
+    assert E.kv_headroom() > h0
+    b = E.kv_alloc(0)
+    E.kv_append_prefix(b, toks, chunk_tokens=64, last_logits=buf)
+    moved = buf[0].cpu().numpy()
+    assert np.max(np.abs(stay - moved)) <= F32_TOL
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_batch_order_is_bitwise_invariant(bf16):
+    shape = SMALL_BF16 if bf16 else TINY
+    arrays = make_weights(shape, seed=3, bf16=bf16)
+    E = _engine(shape, arrays, bf16=bf16)
+    lens = [3, 18, 33, 50, 1]
+    seqs = []
+    for i, n in enumerate(lens):
+        s = E.kv_alloc(0)
+        E.kv_append_prefix(s, random_tokens(n, shape.vocab, seed=30 + i), chunk_tokens=16)
+        seqs.append(s)
+    # snapshot the KV pool, run both orders from the same state
+    pool0 = E.kv_pool.clone()
+    lens0 = [E.kv_len(s) for s in seqs]
+    tok = random_tokens(len(seqs), shape.vocab, seed=40)
+    la = _logits_buf(len(seqs), shape.vocab)
+    E.decode_step(seqs, torch.from_numpy(tok).cuda(), la)
+    a = la.cpu().numpy()
+    # roll back: free and rebuild identical sequences is not needed; restore
+    # the pool bytes and replay the prefixes' lengths through fresh ids.
+    for s in seqs:
+        E.kv_free(s)
+    E.kv_pool.copy_(pool0)
+    seqs2 = []
+    for i, n in enumerate(lens0):
+        s = E.kv_alloc(0)
+        E.kv_append_prefix(s, random_tokens(n, shape.vocab, seed=30 + i), chunk_tokens=16)
+        seqs2.append(s)
+    order = [3, 0, 4, 2, 1]
+    lb = _logits_buf(len(seqs), shape.vocab)
+    E.decode_step([seqs2[i] for i in order], torch.from_numpy(tok[order]).cuda(), lb)
+    b = lb.cpu().numpy()
+    np.testing.assert_array_equal(a[order], b)
+
+
+def _bf16_parity(shape, seed, prefix_lens, n_steps, chunk):
+    arrays = make_weights(shape, seed=seed, bf16=True)
+    w64 = od.ModelWeights.from_arrays(shape, arrays)
+    E = _engine(shape, arrays, bf16=True, max_chunk=max(chunk, 16))
+    seqs, toks = [], []
+    gpu = [[] for _ in prefix_lens]
+    buf = _logits_buf(1, shape.vocab)
+    for i, n in enumerate(prefix_lens):
+        t = random_tokens(n + n_steps, shape.vocab, seed=seed * 100 + i)
+        toks.append(t)
+        s = E.kv_alloc(0)
+        E.kv_append_prefix(s, t[:n], chunk_tokens=chunk, last_logits=buf)
+        gpu[i].append(buf[0].cpu().numpy().copy())
+        seqs.append(s)
+    logits = _logits_buf(len(seqs), shape.vocab)
+    for k in range(n_steps):
+        step_tok = np.array([t[n + k] for t, n in zip(toks, prefix_lens)], dtype=np.int32)
+        E.decode_step(seqs, torch.from_numpy(step_tok).cuda(), logits)
+        got = logits.cpu().numpy()
+        for i in range(len(seqs)):
+            gpu[i].append(got[i].copy())
+    for i, n in enumerate(prefix_lens):
+        ref = od.recompute_logits(w64, toks[i])[n - 1:]
+        g = np.stack(gpu[i])
+        assert np.isfinite(g).all()
+        for r in range(ref.shape[0]):
+            err = np.max(np.abs(g[r] - ref[r]))
+            assert err <= BF16_TOL * np.max(np.abs(ref[r])), (i, r, err)
+
+
+def test_bf16_small_decoder_parity():
+    _bf16_parity(SMALL_BF16, seed=5, prefix_lens=[5, 40, 70], n_steps=8, chunk=16)
+
+
+def test_bf16_8b_geometry_two_layers_parity():
+    """Full 8B layer width (d 4096, 32/8 heads, Dh 128, FFN 14336) with two
+    layers and a 4096-entry vocabulary, real prefill plus decode steps."""
+    shape = ModelShape(n_layers=2, d_model=EIGHT_B.d_model, n_q_heads=EIGHT_B.n_q_heads,
+                       n_kv_heads=EIGHT_B.n_kv_heads, head_dim=EIGHT_B.head_dim,
+                       ffn_dim=EIGHT_B.ffn_dim, vocab=4096)
+    _bf16_parity(shape, seed=6, prefix_lens=[9, 33, 48, 20], n_steps=4, chunk=32)
+
+
+def test_page_growth_failure_is_atomic():
+    arrays = make_weights(TINY, seed=4)
+    P = _P()
+    E = _engine(TINY, arrays, bf16=False, pool_tokens=64, max_seq_len=200)  # 4 pages
+    a, b = E.kv_alloc(0), E.kv_alloc(0)
+    E.kv_append_prefix(a, random_tokens(32, TINY.vocab, 1), chunk_tokens=16)  # 2 pages
+    E.kv_append_prefix(b, random_tokens(32, TINY.vocab, 2), chunk_tokens=16)  # 2 pages
+    assert E.kv_headroom() == 0
+    logits = _logits_buf(2, TINY.vocab)
+    tok = torch.zeros(2, dtype=torch.int32, device="cuda")
+    with pytest.raises(P.PdecError) as ei:
+        E.decode_step([a, b], tok, logits)  # both need a new page
+    assert ei.value.code == -2
+    assert E.kv_len(a) == 32 and E.kv_len(b) == 32 and E.kv_headroom() == 0
+    with pytest.raises(P.PdecError) as ei:
+        E.kv_alloc(1)
+    assert ei.value.code == -2
+    with pytest.raises(P.PdecError) as ei:
+        E.decode_step([a, a], tok, logits)
+    assert ei.value.code == -1
+    E.kv_free(b)
+    with pytest.raises(P.PdecError) as ei:
+        E.decode_step([b], tok, logits)
+    assert ei.value.code == -3
+    E.decode_step([a], tok, logits)  # now a page is free
+    assert E.kv_len(a) == 33
+    with pytest.raises(P.PdecError) as ei:
+        E.kv_append_prefix(a, random_tokens(200, TINY.vocab, 3), chunk_tokens=16)
+    assert ei.value.code == -4 and E.kv_len(a) == 33
+    with pytest.raises(P.PdecError) as ei:
+        E.sample(logits, tok, mode=1)
+    assert ei.value.code == -6

@@ -200,3 +200,53 @@ def paged_attention_case(batch: int, n_q_heads: int, n_kv_heads: int, head_dim: 
                 k_pool[last, :, tail:, :] = np.nan
                 v_pool[last, :, tail:, :] = np.nan
     return PagedAttentionCase(q=q, k_pool=k_pool, v_pool=v_pool, block_table=bt, lens=lens)
+
+
+@dataclasses.dataclass
+class LazyPagedAttentionCase:
+    """Isolated decode-attention operands for a big pool, drawn per sequence.
+
+    The block table comes from one random permutation of the pool; the
+    K/V of sequence b (``[n_pages_b, Hkv, 16, Dh]``, float32,
+    bf16-representable, tail slots NaN) and its query are drawn from a
+    generator seeded by (seed, b), so any subset of sequences can be
+    regenerated on its own.
+    """
+
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    lens: np.ndarray
+    block_table: np.ndarray
+    n_pool_pages: int
+    seed: int
+
+    def sequence(self, b: int):
+        rng = np.random.default_rng([self.seed, int(b)])
+        n = int(self.lens[b])
+        npg = (n + PAGE_TOKENS - 1) // PAGE_TOKENS
+        shp = (npg, self.n_kv_heads, PAGE_TOKENS, self.head_dim)
+        k = round_to_bf16(rng.standard_normal(shp, dtype=np.float32))
+        v = round_to_bf16(rng.standard_normal(shp, dtype=np.float32))
+        q = round_to_bf16(rng.standard_normal((self.n_q_heads, self.head_dim), dtype=np.float32))
+        tail = n % PAGE_TOKENS
+        if tail:
+            k[-1, :, tail:, :] = np.nan
+            v[-1, :, tail:, :] = np.nan
+        return q, k, v
+
+
+def lazy_paged_attention_case(batch: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                              lens: np.ndarray, n_pool_pages: int,
+                              seed: int) -> LazyPagedAttentionCase:
+    lens = np.asarray(lens, dtype=np.int64)
+    npages = (lens + PAGE_TOKENS - 1) // PAGE_TOKENS
+    if int(npages.sum()) > n_pool_pages:
+        raise ValueError("pool too small for the requested lengths")
+    perm = np.random.default_rng(seed).permutation(n_pool_pages).astype(np.int32)
+    bt = np.zeros((batch, int(npages.max())), dtype=np.int32)
+    cursor = 0
+    for b in range(batch):
+        bt[b, :npages[b]] = perm[cursor:cursor + npages[b]]
+        cursor += int(npages[b])
+    return LazyPagedAttentionCase(n_q_heads, n_kv_heads, head_dim, lens, bt, n_pool_pages, seed)
