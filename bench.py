@@ -1,0 +1,319 @@
+#!/usr/bin/env python3
+"""Batched paged decode throughput on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+One step = decode_step + sample over the whole active batch: embedding, per
+layer RMSNorm + QKV projection, RoPE + KV page write, paged split-K attention,
+O projection + residual, RMSNorm + gate/up + SwiGLU, down projection +
+residual, then final norm, LM head and greedy argmax.  Greedy tokens feed the
+next step on the device.
+
+Inputs are synthetic and seeded: random-init weights of the named shape,
+context lengths drawn from the named distribution, and KV pages filled with
+N(0,1) bf16 values (the contexts are staged with kv_extend_uninit rather than
+prefilled: decode cost does not depend on KV values).  Prints one JSON line.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode tokens/sec at batch B + achieved HBM GB/s (% of peak), 1 MI355X"
+HBM_PEAK_GBS = 8000.0
+
+# name -> (batch, length distribution)
+WORKLOADS = {
+    # 8B-shaped decoder, throughput regime: lognormal contexts, median 4096.
+    "decode-8b-b256-lognormal": (256, ("lognormal", 4096, 0.8, 256, 32768)),
+    # 8B-shaped decoder, long-context tail: B=8, contexts U[65536, 131072].
+    "decode-8b-b8-long": (8, ("uniform", 65536, 131072)),
+    # multi-turn batch sweep points (capped Pareto contexts), decode only.
+    "decode-8b-b16-pareto": (16, ("pareto", 1.5, 1024, 65536)),
+    "decode-8b-b64-pareto": (64, ("pareto", 1.5, 1024, 65536)),
+    "decode-8b-b256-pareto": (256, ("pareto", 1.5, 1024, 65536)),
+    "decode-8b-b512-pareto": (512, ("pareto", 1.5, 1024, 65536)),
+}
+DEFAULT_WORKLOAD = "decode-8b-b256-lognormal"
+
+
+def log(msg):
+    sys.stderr.write(f"[bench] {msg}\n")
+    sys.stderr.flush()
+
+
+def draw_lengths(batch, spec, seed=1):
+    from workload import lengths_lognormal, lengths_pareto, lengths_uniform
+    kind = spec[0]
+    if kind == "lognormal":
+        return lengths_lognormal(batch, spec[1], spec[2], spec[3], spec[4], seed)
+    if kind == "uniform":
+        return lengths_uniform(batch, spec[1], spec[2], seed)
+    if kind == "pareto":
+        return lengths_pareto(batch, spec[1], spec[2], spec[3], seed)
+    raise ValueError(kind)
+
+
+def gpu_weights(shape, seed=0, std=0.02):
+    """Random-init bf16 weights of the given shape, drawn on the GPU."""
+    import torch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+
+    def mat(rows, cols):
+        w = torch.empty((rows, cols), dtype=torch.bfloat16, device="cuda")
+        w.normal_(0.0, std, generator=g)
+        return w
+
+    ones = lambda: torch.ones(shape.d_model, dtype=torch.float32, device="cuda")
+    out = {"embed": mat(shape.vocab, shape.d_model), "layers": []}
+    for _ in range(shape.n_layers):
+        out["layers"].append({
+            "wq": mat(shape.q_dim, shape.d_model), "wk": mat(shape.kv_dim, shape.d_model),
+            "wv": mat(shape.kv_dim, shape.d_model), "wo": mat(shape.d_model, shape.q_dim),
+            "w_gate": mat(shape.ffn_dim, shape.d_model), "w_up": mat(shape.ffn_dim, shape.d_model),
+            "w_down": mat(shape.d_model, shape.ffn_dim), "attn_norm": ones(), "ffn_norm": ones()})
+    out["lm_head"] = mat(shape.vocab, shape.d_model)
+    out["final_norm"] = ones()
+    return out
+
+
+def weight_bytes_per_step(shape, batch, elem=2):
+    """Weights read once per step: every matrix except the embedding table,
+    of which only the batch's rows are gathered."""
+    per_layer = (shape.q_dim + 2 * shape.kv_dim) * shape.d_model + shape.d_model * shape.q_dim \
+        + 3 * shape.ffn_dim * shape.d_model
+    return elem * (shape.n_layers * per_layer + shape.vocab * shape.d_model
+                   + batch * shape.d_model)
+
+
+def file_hash(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(workload, kernel_src):
+    """Counter-based HBM bytes per attention launch, if measured for this
+    exact kernel source and workload (profiles/attention_traffic.json)."""
+    path = os.path.join(ROOT, "profiles", "attention_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(workload)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("kernel_sha256_16") != file_hash(kernel_src):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle as it stands, on a bounded sample.
+# ---------------------------------------------------------------------------
+
+def cpu_baseline(shape, lens, budget_s=15.0, seed=7):
+    """Time the float32 oracle decoder for single trajectories of the batch.
+
+    The sample is a one-layer slice of the model (full layer width) plus the
+    LM head, stepped once for a seeded random subset of the batch's
+    trajectories at their real context lengths.  Per-token time is
+    extrapolated as layers x (step - LM head) + LM head; the oracle handles
+    one trajectory at a time, so its throughput is 1 / per-token time.
+    """
+    import torch
+
+    from oracle import decoder as od
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max((i.get("num_threads", 0) for i in threadpool_info()), default=os.cpu_count())
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count()
+    gen = torch.Generator().manual_seed(seed)
+
+    def mat(r, c):
+        return (torch.randn((r, c), generator=gen, dtype=torch.float32) * 0.02).numpy()
+
+    lm = mat(shape.vocab, shape.d_model)
+    layer = {"wq": mat(shape.q_dim, shape.d_model), "wk": mat(shape.kv_dim, shape.d_model),
+             "wv": mat(shape.kv_dim, shape.d_model), "wo": mat(shape.d_model, shape.q_dim),
+             "w_gate": mat(shape.ffn_dim, shape.d_model), "w_up": mat(shape.ffn_dim, shape.d_model),
+             "w_down": mat(shape.d_model, shape.ffn_dim),
+             "attn_norm": np.ones(shape.d_model, np.float32),
+             "ffn_norm": np.ones(shape.d_model, np.float32)}
+    w = od.ModelWeights(n_layers=1, n_q_heads=shape.n_q_heads, n_kv_heads=shape.n_kv_heads,
+                        head_dim=shape.head_dim, rms_eps=shape.rms_eps, rope_base=shape.rope_base,
+                        embed=lm, lm_head=lm, final_norm=np.ones(shape.d_model, np.float32),
+                        layers=[layer])
+    dec = od.Decoder(w)
+    x = np.ones(shape.d_model, np.float32)
+    t0 = time.perf_counter()
+    for _ in range(3):
+        w.lm_head @ od.rmsnorm(x, w.final_norm, w.rms_eps)
+    t_lm = (time.perf_counter() - t0) / 3
+    order = np.random.default_rng(seed).permutation(len(lens))
+    rng = np.random.default_rng(seed + 1)
+    per_token, used, spent = [], [], 0.0
+    for b in order:
+        n = int(lens[b])
+        st = dec.new_state()
+        st["k"][0] = rng.standard_normal((n, shape.n_kv_heads, shape.head_dim), dtype=np.float32)
+        st["v"][0] = rng.standard_normal((n, shape.n_kv_heads, shape.head_dim), dtype=np.float32)
+        st["len"] = n
+        t0 = time.perf_counter()
+        dec.step(st, int(b) % shape.vocab)
+        t_step = time.perf_counter() - t0
+        spent += t_step
+        per_token.append(shape.n_layers * max(t_step - t_lm, 0.0) + t_lm)
+        used.append(n)
+        if spent >= budget_s:
+            break
+    t_tok = float(np.mean(per_token))
+    return {"value": 1.0 / t_tok, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"float32 oracle, one layer at full width plus the LM head, one decode "
+                       f"step for {len(used)} of the batch's {len(lens)} trajectories at their "
+                       f"context lengths (mean {np.mean(used):.0f}); per-token time = "
+                       f"{shape.n_layers} x (step - LM head {t_lm * 1e3:.1f} ms) + LM head; "
+                       f"{spent:.1f} s of stepping"),
+            "ms_per_token": t_tok * 1e3}
+
+
+# ---------------------------------------------------------------------------
+# GPU decode run.
+# ---------------------------------------------------------------------------
+
+def run_decode(workload, steps, warmup, with_cpu):
+    import torch
+
+    import paper_2609_36899_amd as P
+    from paper_2609_36899_amd import _native as N
+    from workload import EIGHT_B
+
+    shape = EIGHT_B
+    batch, spec = WORKLOADS[workload]
+    lens = draw_lengths(batch, spec)
+    grow = warmup + steps + 1
+    pages = int(np.sum((lens + grow + 15) // 16)) + 64
+    per_tok = P.kv_bytes_per_token(shape, P.BF16)
+    pool_bytes = pages * 16 * per_tok
+    log(f"{workload}: B={batch}, mean context {lens.mean():.0f}, pool {pool_bytes / 2**30:.1f} GiB")
+
+    torch.cuda.set_device(0)
+    weights = gpu_weights(shape)
+    E = P.Engine(shape, weights, P.BF16, pool_bytes, max_seqs=batch,
+                 max_seq_len=int(lens.max()) + grow + 16, max_batch=batch, max_chunk=16)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(3)
+    pool_bf16 = E.kv_pool.view(torch.bfloat16)
+    chunk = 1 << 30
+    for i in range(0, pool_bf16.numel(), chunk):
+        pool_bf16[i:i + chunk].normal_(0.0, 1.0, generator=g)
+    ids = np.array([E.kv_alloc(0) for _ in range(batch)], dtype=np.int32)
+    for sid, n in zip(ids, lens):
+        E.kv_extend_uninit(int(sid), int(n))
+    tok = torch.randint(0, shape.vocab, (batch,), dtype=torch.int32, device="cuda", generator=g)
+    logits = torch.empty((batch, shape.vocab), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+
+    def step():
+        E.decode_step(ids, tok, logits)
+        E.sample(logits, tok)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({warmup} steps); timing {steps} steps")
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    E.profile(True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    start.record()
+    for _ in range(steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    E.profile(False)
+    gpu_ms = start.elapsed_time(end)
+    attn_ms, attn_n = E.profile_read(N.TIMER_ATTENTION)
+    gemm_ms, gemm_n = E.profile_read(N.TIMER_GEMM)
+    lm_ms, lm_n = E.profile_read(N.TIMER_LM_HEAD)
+    assert np.isfinite(logits[:4].cpu().numpy()).all()
+
+    ms_step = gpu_ms / steps
+    tok_s = batch * steps / (gpu_ms / 1e3)
+    # Algorithmic bytes, averaged over the timed steps: context at timed step
+    # t is lens + warmup + t, and each step reads its new token's KV too.
+    mean_keys = float(np.mean([np.sum(lens + warmup + t + 1) for t in range(steps)]))
+    kv_read = mean_keys * per_tok
+    kv_write = batch * per_tok
+    w_bytes = weight_bytes_per_step(shape, batch)
+    logit_bytes = 2 * batch * shape.vocab * 4  # LM-head write + argmax read
+    step_bytes = kv_read + kv_write + w_bytes + logit_bytes
+    hbm = step_bytes / (ms_step / 1e3) / 1e9
+    attn_bytes = mean_keys * shape.n_kv_heads * shape.head_dim * 2 * 2  # per layer launch
+    attn_avg_ms = attn_ms / max(attn_n, 1)
+    attn_gbs = attn_bytes / (attn_avg_ms / 1e3) / 1e9
+    src = os.path.join(ROOT, "paper_2609_36899_amd", "csrc", "attention.hip")
+    traffic = load_traffic(workload, src)
+    out = {
+        "metric": METRIC, "value": round(tok_s, 2), "unit": "tokens/s", "n_gpus": 1,
+        "steps": steps, "warmup": warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": workload, "model": "8B-shaped decoder (32x4096, 32/8 heads, "
+                   "Dh 128, FFN 14336, vocab 128256), random init",
+                   "batch": int(batch), "context_mean": round(float(lens.mean()), 1),
+                   "context_min": int(lens.min()), "context_max": int(lens.max()),
+                   "length_distribution": list(spec), "page_tokens": 16},
+        "hbm_gbps": round(hbm, 1), "hbm_frac_of_peak": round(hbm / HBM_PEAK_GBS, 4),
+        "step_bytes": int(step_bytes), "wall_s": round(wall, 3),
+        "breakdown_ms_per_step": {"attention": round(attn_ms / steps, 3),
+                                  "projections": round(gemm_ms / steps, 3),
+                                  "lm_head": round(lm_ms / steps, 3)},
+        "roofline": {"kernel": "attn_split_bf16<128>", "bound": "hbm",
+                     "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "bytes_per_launch": int(attn_bytes),
+                     "avg_launch_ms": round(attn_avg_ms, 5), "launches": int(attn_n)},
+    }
+    del E, weights, logits, pool_bf16
+    torch.cuda.empty_cache()
+    if with_cpu:
+        log("timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(shape, lens)
+    else:
+        out["cpu_baseline"] = None
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the decode engine is one worker's backend "
+              "and trajectories shard across GPUs as independent engines (data parallel, no "
+              "exchange).  Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    out = run_decode(args.workload, args.steps, args.warmup, not args.no_cpu_baseline)
+    out["host"] = {"cpu": platform.processor() or platform.machine(), "cpu_count": os.cpu_count()}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
