@@ -46,7 +46,9 @@ __global__ __launch_bounds__(64) void attn_split_bf16(
   constexpr int DT = DH / 16;  // 16-wide dim tiles of PV
   const int lane = threadIdx.x;
   const int c16 = lane & 15, q4 = lane >> 4;
-  const int item_id = blockIdx.x, g = blockIdx.y;
+  // The KV heads of one item are adjacent in the grid, so the work groups in
+  // flight together read whole contiguous page regions ([page][Hkv][...]).
+  const int g = blockIdx.x, item_id = blockIdx.y;
   const AttnItem it = items[item_id];
   const AttnQBlock qb = qblocks[it.qblock];
   const int G = n_q_heads / n_kv_heads;
@@ -104,11 +106,11 @@ __global__ __launch_bounds__(64) void attn_split_bf16(
     for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int c = 0; c < KC; ++c)
-        kf[u][c] = *(const bf16x8*)(kb + (k_tok + 4 * u) * DH + c * 32 + q4 * 8);
+        kf[u][c] = load_stream<bf16x8>(kb + (k_tok + 4 * u) * DH + c * 32 + q4 * 8);
     const uint16_t* vb = vpool + (v_page_sel ? base1 : base0) + v_tok0;
     u16x8 vf[DT];
 #pragma unroll
-    for (int t = 0; t < DT; ++t) vf[t] = *(const u16x8*)(vb + (t * 16 + c16) * kPage);
+    for (int t = 0; t < DT; ++t) vf[t] = load_stream<u16x8>(vb + (t * 16 + c16) * kPage);
 
     f32x4 s[2];
 #pragma unroll
@@ -193,7 +195,7 @@ __global__ __launch_bounds__(64) void attn_split_f32(
     float* __restrict__ part_acc) {
   constexpr int E = DH / 64;
   const int lane = threadIdx.x;
-  const int item_id = blockIdx.x, g = blockIdx.y;
+  const int g = blockIdx.x, item_id = blockIdx.y;
   const AttnItem it = items[item_id];
   const AttnQBlock qb = qblocks[it.qblock];
   const int G = n_q_heads / n_kv_heads;
@@ -240,8 +242,10 @@ __global__ __launch_bounds__(64) void attn_split_f32(
 }
 
 // ---------------------------------------------------------------------------
-// Merge the partials of each (query row, head): M = max m_i,
-// o = sum_i exp2(m_i - M) acc_i / sum_i exp2(m_i - M) l_i, in item order.
+// Merge the partials of each (query row, head) in item order with the
+// online-softmax rule: m = max(m, m_i); l = l e^(m_old-m) + l_i e^(m_i-m);
+// o likewise; output o / l.  One wave per (query block, KV head); a lane owns
+// DH/16 consecutive dims of one of four rows at a time.
 // ---------------------------------------------------------------------------
 template <int DH, typename OutT>
 __global__ __launch_bounds__(64) void attn_combine(const AttnQBlock* __restrict__ qblocks,
@@ -249,32 +253,51 @@ __global__ __launch_bounds__(64) void attn_combine(const AttnQBlock* __restrict_
                                                   const float* __restrict__ part_acc,
                                                   int32_t n_q_heads, int32_t n_kv_heads,
                                                   OutT* __restrict__ out) {
-  constexpr int E = DH / 64;
-  const int lane = threadIdx.x;
+  constexpr int DPL = DH / 16;
+  const int lane = threadIdx.x, rsub = lane >> 4, d0 = (lane & 15) * DPL;
   const AttnQBlock qb = qblocks[blockIdx.x];
-  const int head = blockIdx.y;
+  const int g = blockIdx.y;
   const int G = n_q_heads / n_kv_heads;
-  const int g = head / G;
-  for (int jq = 0; jq < qb.n_q; ++jq) {
-    const int r = jq * G + head % G;
-    float mmax = -INFINITY;
-    for (int i = qb.item_begin; i < qb.item_end; ++i)
-      mmax = fmaxf(mmax, part_ml[(((int64_t)i * n_kv_heads + g) * 16 + r) * 2]);
-    float lsum = 0.f, o[E];
+  const int rows = qb.n_q * G;
+  for (int r = rsub; r < rows; r += 4) {
+    float m = -INFINITY, l = 0.f, o[DPL];
 #pragma unroll
-    for (int e = 0; e < E; ++e) o[e] = 0.f;
-    for (int i = qb.item_begin; i < qb.item_end; ++i) {
-      const int64_t prow = ((int64_t)i * n_kv_heads + g) * 16 + r;
-      const float mi = part_ml[prow * 2];
-      const float w = (mi == -INFINITY) ? 0.f : exp2f(mi - mmax);
-      lsum += w * part_ml[prow * 2 + 1];
+    for (int e = 0; e < DPL; ++e) o[e] = 0.f;
+    // Items in groups of four: every load of a group is issued before use.
+    for (int i0 = qb.item_begin; i0 < qb.item_end; i0 += 4) {
+      float2 ml[4];
+      float4 a[4][DPL / 4];
 #pragma unroll
-      for (int e = 0; e < E; ++e) o[e] += w * part_acc[prow * DH + lane + 64 * e];
+      for (int u = 0; u < 4; ++u) {
+        const int i = min(i0 + u, qb.item_end - 1);
+        const int64_t prow = ((int64_t)i * n_kv_heads + g) * 16 + r;
+        ml[u] = *(const float2*)(part_ml + prow * 2);
+#pragma unroll
+        for (int e = 0; e < DPL / 4; ++e) a[u][e] = *(const float4*)(part_acc + prow * DH + d0 + 4 * e);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (i0 + u >= qb.item_end) break;
+        // An item with no key visible to the row has m = -inf, l = 0, acc = 0.
+        const float mn = fmaxf(m, ml[u].x);
+        const float mu = (mn == -INFINITY) ? 0.f : mn;
+        const float so = exp2f(m - mu), si = exp2f(ml[u].x - mu);
+        l = l * so + ml[u].y * si;
+#pragma unroll
+        for (int e = 0; e < DPL / 4; ++e) {
+          o[4 * e] = o[4 * e] * so + a[u][e].x * si;
+          o[4 * e + 1] = o[4 * e + 1] * so + a[u][e].y * si;
+          o[4 * e + 2] = o[4 * e + 2] * so + a[u][e].z * si;
+          o[4 * e + 3] = o[4 * e + 3] * so + a[u][e].w * si;
+        }
+        m = mn;
+      }
     }
-    const float inv = 1.f / lsum;
-    OutT* orow = out + ((int64_t)(qb.q_row0 + jq) * n_q_heads + head) * DH;
+    const float inv = 1.f / l;
+    const int jq = r / G, head = g * G + r % G;
+    OutT* orow = out + ((int64_t)(qb.q_row0 + jq) * n_q_heads + head) * DH + d0;
 #pragma unroll
-    for (int e = 0; e < E; ++e) orow[lane + 64 * e] = Store<OutT>::from(o[e] * inv);
+    for (int e = 0; e < DPL; ++e) orow[e] = Store<OutT>::from(o[e] * inv);
   }
 }
 
@@ -287,7 +310,7 @@ hipError_t launch_attention_split(int dtype, int head_dim, int n_items, int n_q_
                                   const int32_t* block_table, int32_t bt_stride, float* part_ml,
                                   float* part_acc, hipStream_t stream) {
   if (n_items == 0) return hipSuccess;
-  const dim3 grid(n_items, n_kv_heads), block(64);
+  const dim3 grid(n_kv_heads, n_items), block(64);
   const float scale_log2 = kLog2e / sqrtf((float)head_dim);
   if (dtype == 1) {
     if (head_dim == 128)
@@ -320,7 +343,7 @@ hipError_t launch_attention_combine(int head_dim, int n_qblocks, int n_q_heads, 
                                     const float* part_acc, void* out, int out_bf16,
                                     hipStream_t stream) {
   if (n_qblocks == 0) return hipSuccess;
-  const dim3 grid(n_qblocks, n_q_heads), block(64);
+  const dim3 grid(n_qblocks, n_kv_heads), block(64);
   if (head_dim == 128) {
     if (out_bf16)
       attn_combine<128, uint16_t><<<grid, block, 0, stream>>>(qblocks, part_ml, part_acc,

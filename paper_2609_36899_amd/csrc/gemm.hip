@@ -7,8 +7,9 @@
 // MB) stay in L2.  When the column slices alone cannot fill 256 CUs the K
 // axis is split and the fp32 partial sums are reduced by the next kernel.
 //
-// bf16: v_mfma_f32_16x16x32_bf16 tiles of 16 rows x 16 columns, four waves
-// per work group arranged WM x WN over the (rows, columns) tile.
+// bf16: v_mfma_f32_16x16x32_bf16 tiles of 16 rows x 16 columns.  The
+// weight stream is the bound at small batch, so weight tiles are prefetched
+// several k-steps ahead to keep enough bytes in flight per CU.
 #include "hip_common.h"
 #include "kernels.h"
 
@@ -27,27 +28,131 @@ __device__ __forceinline__ const void* seg_row(const WSegs& w, int n, int64_t ro
   return w.ptr[0];
 }
 
-template <int WM, int WN, int MT, int NT>
-__global__ __launch_bounds__(256) void gemm_bf16_mfma(int M, int N, int K, int k_split,
-                                                      const uint16_t* __restrict__ A,
-                                                      int64_t lda, WSegs w,
-                                                      float* __restrict__ out) {
+// Small batches (M <= 64).  Each wave owns 16 columns of the 64-column
+// block and every row of the batch, so no two waves share weight bytes.  The
+// weight fragments are prefetched NS k-steps ahead through a register ring so
+// that enough HBM bytes are in flight to hide the memory latency; the
+// activations (L2-resident) are prefetched one step ahead.
+template <int MT, int NS>
+__global__ __launch_bounds__(256, 2) void gemm_bf16_small_m(int M, int N, int K, int k_split,
+                                                            const uint16_t* __restrict__ A,
+                                                            int64_t lda, WSegs w,
+                                                            float* __restrict__ out) {
+  static_assert(NS % 2 == 0, "ring depth must be even");
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int c16 = lane & 15, q4 = lane >> 4;
-  const int wm = wave / WN, wn = wave % WN;
-  const int m0 = blockIdx.y * (WM * MT * 16) + wm * MT * 16;
-  const int n0 = blockIdx.x * (WN * NT * 16) + wn * NT * 16;
+  const int n0 = blockIdx.x * 64 + wave * 16;
   const int kbeg = blockIdx.z * k_split;
-  const int kend = min(K, kbeg + k_split);
-  if (m0 >= M || n0 >= N) return;  // no barriers below: idle waves may leave
+  const int n_iter = (min(K, kbeg + k_split) - kbeg) / 64;
+  if (n0 >= N || n_iter <= 0) return;  // no barriers in this kernel
 
+  const uint16_t* wrow = (const uint16_t*)seg_row(w, min(n0 + c16, N - 1), K, 2) + kbeg + q4 * 8;
   const uint16_t* arow[MT];
 #pragma unroll
-  for (int t = 0; t < MT; ++t) arow[t] = A + (int64_t)min(m0 + t * 16 + c16, M - 1) * lda + q4 * 8;
-  const uint16_t* wrow[NT];
+  for (int t = 0; t < MT; ++t)
+    arow[t] = A + (int64_t)min(t * 16 + c16, M - 1) * lda + kbeg + q4 * 8;
+
+  f32x4 acc[MT];
 #pragma unroll
-  for (int t = 0; t < NT; ++t)
-    wrow[t] = (const uint16_t*)seg_row(w, min(n0 + t * 16 + c16, N - 1), K, 2) + q4 * 8;
+  for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 wr[NS][2];
+  bf16x8 ar[2][MT][2];
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    if (s < n_iter) {
+      wr[s][0] = load_stream<bf16x8>(wrow + s * 64);
+      wr[s][1] = load_stream<bf16x8>(wrow + s * 64 + 32);
+    }
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+    ar[0][t][0] = *(const bf16x8*)(arow[t]);
+    ar[0][t][1] = *(const bf16x8*)(arow[t] + 32);
+  }
+  for (int it0 = 0; it0 < n_iter; it0 += NS) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const int it = it0 + s;
+      if (it >= n_iter) break;
+      const bf16x8 b0 = wr[s][0], b1 = wr[s][1];
+      if (it + NS < n_iter) {
+        wr[s][0] = load_stream<bf16x8>(wrow + (it + NS) * 64);
+        wr[s][1] = load_stream<bf16x8>(wrow + (it + NS) * 64 + 32);
+      }
+      if (it + 1 < n_iter) {
+#pragma unroll
+        for (int t = 0; t < MT; ++t) {
+          ar[(s + 1) & 1][t][0] = *(const bf16x8*)(arow[t] + (it + 1) * 64);
+          ar[(s + 1) & 1][t][1] = *(const bf16x8*)(arow[t] + (it + 1) * 64 + 32);
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < MT; ++t) {
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ar[s & 1][t][0], b0, acc[t], 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ar[s & 1][t][1], b1, acc[t], 0, 0, 0);
+      }
+    }
+  }
+
+  float* o = out + (int64_t)blockIdx.z * M * N;
+  const int col = n0 + c16;
+#pragma unroll
+  for (int t = 0; t < MT; ++t)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int row = t * 16 + 4 * q4 + rr;
+      if (row < M && col < N) o[(int64_t)row * N + col] = acc[t][rr];
+    }
+}
+
+// Larger batches (M > 64): 128 x 128 output tiles, four waves in a 2 x 2
+// grid of 64 x 64 sub-tiles.  Per k-step of 64 the A tile (128 rows) and the
+// W tile (128 columns) are staged once through LDS (double-buffered, 16-byte
+// chunks XOR-swizzled by row) and each is shared by the two waves that need
+// it; the tiles of the next NS k-steps are prefetched into a register ring
+// meanwhile (NS even: ring slot s also names the LDS buffer s & 1).
+// Work-group ids are laid out so that the M-blocks of one column tile are
+// dispatched back to back onto the same XCD (ids L and L+8 share an XCD):
+// the first streams the W tile from HBM, the others find it in that XCD's L2
+// (so these loads carry no streaming hint).
+template <int NS>
+__global__ __launch_bounds__(256, 2) void gemm_bf16_tile128(int M, int N, int K, int k_split,
+                                                            int n_mb, int n_nb,
+                                                            const uint16_t* __restrict__ A,
+                                                            int64_t lda, WSegs w,
+                                                            float* __restrict__ out) {
+  constexpr int MT = 4, NT = 4;
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][128 * 64];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int c16 = lane & 15, q4 = lane >> 4;
+  const int L = blockIdx.x;
+  const int grp = L / (8 * n_mb), rem = L % (8 * n_mb);
+  const int mb = rem / 8, nb = grp * 8 + rem % 8;
+  if (nb >= n_nb) return;  // padding of the id layout; uniform over the group
+  const int kbeg = blockIdx.z * k_split;
+  const int n_iter = (min(K, kbeg + k_split) - kbeg) / 64;
+  if (n_iter <= 0) return;
+  const int m_blk = mb * 128, n_blk = nb * 128;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // Staging: 128 rows x 8 chunks per tile, 4 chunks per thread (rows r + 32j).
+  const int r = tid >> 3, c = tid & 7;
+  const int dst = r * 64 + ((c ^ (r & 7)) * 8);  // + 32j*64 for chunk j
+  const uint16_t* asrc[4];
+  const uint16_t* wsrc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    asrc[j] = A + (int64_t)min(m_blk + r + 32 * j, M - 1) * lda + kbeg + c * 8;
+    wsrc[j] = (const uint16_t*)seg_row(w, min(n_blk + r + 32 * j, N - 1), K, 2) + kbeg + c * 8;
+  }
+  int aoff[MT][2], boff[NT][2];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int ra = wm * 64 + t * 16 + c16, rb = wn * 64 + t * 16 + c16, cc = h * 4 + q4;
+      aoff[t][h] = ra * 64 + ((cc ^ (ra & 7)) * 8);
+      boff[t][h] = rb * 64 + ((cc ^ (rb & 7)) * 8);
+    }
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -55,25 +160,51 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(int M, int N, int K, int k
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int k = kbeg; k < kend; k += 64) {
-    bf16x8 a0[MT], a1[MT], b0[NT], b1[NT];
+  // Register ring of NS k-steps (A and W chunks of this thread).
+  u16x8 ra_[NS][4], rw_[NS][4];
 #pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      b0[j] = *(const bf16x8*)(wrow[j] + k);
-      b1[j] = *(const bf16x8*)(wrow[j] + k + 32);
-    }
+  for (int s = 0; s < NS; ++s)
+    if (s < n_iter) {
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      a0[i] = *(const bf16x8*)(arow[i] + k);
-      a1[i] = *(const bf16x8*)(arow[i] + k + 32);
-    }
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-      for (int j = 0; j < NT; ++j) {
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[i], b0[j], acc[i][j], 0, 0, 0);
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[i], b1[j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < 4; ++j) {
+        ra_[s][j] = *(const u16x8*)(asrc[j] + s * 64);
+        rw_[s][j] = *(const u16x8*)(wsrc[j] + s * 64);
       }
+    }
+  for (int it0 = 0; it0 < n_iter; it0 += NS) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const int it = it0 + s;
+      if (it >= n_iter) break;
+      uint16_t* la = lds[s & 1][0];
+      uint16_t* lw = lds[s & 1][1];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        *(u16x8*)(la + dst + j * 32 * 64) = ra_[s][j];
+        *(u16x8*)(lw + dst + j * 32 * 64) = rw_[s][j];
+      }
+      __syncthreads();
+      if (it + NS < n_iter) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          ra_[s][j] = *(const u16x8*)(asrc[j] + (it + NS) * 64);
+          rw_[s][j] = *(const u16x8*)(wsrc[j] + (it + NS) * 64);
+        }
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        bf16x8 af[MT], bf[NT];
+#pragma unroll
+        for (int t = 0; t < MT; ++t) af[t] = *(const bf16x8*)(la + aoff[t][h]);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) bf[t] = *(const bf16x8*)(lw + boff[t][h]);
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+          for (int j = 0; j < NT; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+      }
+    }
   }
 
   float* o = out + (int64_t)blockIdx.z * M * N;
@@ -81,10 +212,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_mfma(int M, int N, int K, int k
   for (int i = 0; i < MT; ++i)
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
-      const int col = n0 + j * 16 + c16;
+      const int col = n_blk + wn * 64 + j * 16 + c16;
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
-        const int row = m0 + i * 16 + 4 * q4 + rr;
+        const int row = m_blk + wm * 64 + i * 16 + 4 * q4 + rr;
         if (row < M && col < N) o[(int64_t)row * N + col] = acc[i][j][rr];
       }
     }
@@ -132,28 +263,20 @@ __global__ __launch_bounds__(256) void gemm_f32_tiled(int M, int N, int K, int k
     }
 }
 
-struct BfCfg {
-  int mblk;
-};
-
-BfCfg bf_cfg(int M) {
-  if (M <= 16) return {16};
-  if (M <= 32) return {32};
-  if (M <= 64) return {64};
-  if (M <= 128) return {128};
-  if (M <= 256) return {256};
-  return {512};
-}
-
 }  // namespace
 
 int gemm_plan_splits(int dtype, int M, int N, int K, int* k_split) {
   const int kq = (dtype == 1) ? 64 : 16;
-  const int mblk = (dtype == 1) ? bf_cfg(M).mblk : 32;
-  const int64_t tiles = (int64_t)((N + 63) / 64) * ((M + mblk - 1) / mblk);
+  const int mblk = (dtype == 1) ? (M <= 64 ? 64 : 128) : 32;
+  const int nblk = (dtype == 1 && M > 64) ? 128 : 64;
+  const int64_t tiles = (int64_t)((N + nblk - 1) / nblk) * ((M + mblk - 1) / mblk);
+  // Small batches: aim for two work groups per CU; the partial sums are
+  // small.  Larger batches: one per CU, since every extra split writes and
+  // re-reads an M x N fp32 slab.
+  const int64_t target = (dtype == 1 && M > 64) ? 256 : 512;
   const int ksteps = (K + kq - 1) / kq;
   int s = 1;
-  if (tiles < 512) s = (int)std::min<int64_t>((512 + tiles - 1) / tiles, 8);
+  if (tiles < target) s = (int)std::min<int64_t>((target + tiles - 1) / tiles, 8);
   s = std::max(1, std::min(s, ksteps));
   const int steps_per = (ksteps + s - 1) / s;
   *k_split = steps_per * kq;
@@ -165,16 +288,20 @@ hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t ld
   if (M <= 0 || N <= 0) return hipSuccess;
   const dim3 block(256);
   if (dtype == 1) {
-    const int mblk = bf_cfg(M).mblk;
-    const dim3 grid((N + 63) / 64, (M + mblk - 1) / mblk, splits);
     const uint16_t* a = (const uint16_t*)A;
-    switch (mblk) {
-      case 16: gemm_bf16_mfma<1, 4, 1, 1><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
-      case 32: gemm_bf16_mfma<1, 4, 2, 1><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
-      case 64: gemm_bf16_mfma<1, 4, 4, 1><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
-      case 128: gemm_bf16_mfma<2, 2, 4, 2><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
-      case 256: gemm_bf16_mfma<4, 1, 4, 4><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
-      default: gemm_bf16_mfma<4, 1, 8, 4><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
+    if (M <= 64) {
+      const dim3 grid((N + 63) / 64, 1, splits);
+      switch ((M + 15) / 16) {
+        case 1: gemm_bf16_small_m<1, 8><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
+        case 2: gemm_bf16_small_m<2, 8><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
+        case 3: gemm_bf16_small_m<3, 8><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
+        default: gemm_bf16_small_m<4, 8><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
+      }
+    } else {
+      const int n_mb = (M + 127) / 128, n_nb = (N + 127) / 128;
+      const dim3 grid(((n_nb + 7) / 8) * 8 * n_mb, 1, splits);
+      gemm_bf16_tile128<2><<<grid, block, 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a, lda, w,
+                                                      out);
     }
   } else {
     const dim3 grid((N + 63) / 64, (M + 31) / 32, splits);

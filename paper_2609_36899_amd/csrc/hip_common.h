@@ -11,6 +11,14 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Streaming loads of data read exactly once per step (KV pages, weight
+// tiles): the non-temporal hint keeps them from displacing reused lines.
+template <typename V>
+__device__ __forceinline__ V load_stream(const void* p) {
+  const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
+  return __builtin_bit_cast(V, v);
+}
+
 // bf16 storage is handled as raw 16-bit patterns.
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __uint_as_float(((uint32_t)b) << 16);

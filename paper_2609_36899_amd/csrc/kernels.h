@@ -29,7 +29,7 @@ hipError_t launch_attention_split(int dtype, int head_dim, int n_items, int n_q_
                                   const int32_t* block_table, int32_t bt_stride, float* part_ml,
                                   float* part_acc, hipStream_t stream);
 
-// Merge pass: one work group per (query block, query head); writes
+// Merge pass: one work group per (query block, KV head); writes
 // out [rows][n_q_heads][head_dim] as fp32 (out_bf16 = 0) or bf16.
 hipError_t launch_attention_combine(int head_dim, int n_qblocks, int n_q_heads, int n_kv_heads,
                                     const AttnQBlock* qblocks, const float* part_ml,

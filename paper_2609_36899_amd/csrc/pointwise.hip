@@ -37,29 +37,57 @@ __global__ __launch_bounds__(kRowThreads) void embed_norm_kernel(
 }
 
 template <typename HT>
-__global__ __launch_bounds__(kRowThreads) void resid_norm_kernel(
+struct Pack4;
+template <>
+struct Pack4<float> {
+  static __device__ __forceinline__ void store(float* p, float4 v) { *(float4*)p = v; }
+};
+template <>
+struct Pack4<uint16_t> {
+  static __device__ __forceinline__ void store(uint16_t* p, float4 v) {
+    const uint32_t lo = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
+    const uint32_t hi = (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16);
+    *(uint2*)p = make_uint2(lo, hi);
+  }
+};
+
+// One work group of up to 1024 threads per row, float4 accesses (d % 4 == 0).
+template <typename HT>
+__global__ __launch_bounds__(1024) void resid_norm_kernel(
     int M, int d, const float* __restrict__ part, int splits, float* __restrict__ x,
     const float* __restrict__ gain, float eps, HT* __restrict__ h) {
-  __shared__ float red[kRowThreads / 64];
+  __shared__ float red[16];
   const int row = blockIdx.x;
   float* xr = x + (int64_t)row * d;
   const int64_t slab = (int64_t)M * d;
+  const float* pr = part + (int64_t)row * d;
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += kRowThreads) {
-    float v = xr[i];
-    for (int s = 0; s < splits; ++s) v += part[s * slab + (int64_t)row * d + i];
-    xr[i] = v;
-    ss += v * v;
+  for (int i = threadIdx.x * 4; i < d; i += blockDim.x * 4) {
+    float4 v = *(const float4*)(xr + i);
+    for (int s = 0; s < splits; ++s) {
+      const float4 p = *(const float4*)(pr + s * slab + i);
+      v.x += p.x;
+      v.y += p.y;
+      v.z += p.z;
+      v.w += p.w;
+    }
+    *(float4*)(xr + i) = v;
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   const float inv = rsqrtf(block_sum(ss, red) / (float)d + eps);
   HT* hr = h + (int64_t)row * d;
-  for (int i = threadIdx.x; i < d; i += kRowThreads)
-    hr[i] = Store<HT>::from(xr[i] * inv * gain[i]);
+  for (int i = threadIdx.x * 4; i < d; i += blockDim.x * 4) {
+    const float4 v = *(const float4*)(xr + i);
+    const float4 g = *(const float4*)(gain + i);
+    Pack4<HT>::store(hr + i, make_float4(v.x * inv * g.x, v.y * inv * g.y, v.z * inv * g.z,
+                                         v.w * inv * g.w));
+  }
 }
 
 // One work group per row.  Pairs (i, i + Dh/2) of every q and k head are
-// rotated by the table angle of the row's position; v is copied.  K goes to
-// [page][g][slot][Dh], V to the transposed block [page][g][Dh][slot].
+// rotated by the table angle of the row's position, four pairs per thread;
+// v is copied.  K goes to [page][g][slot][Dh], V to the transposed block
+// [page][g][Dh][slot].
 template <typename T>
 __global__ __launch_bounds__(kRowThreads) void qkv_rope_kv_kernel(
     int M, int head_dim, int n_q_heads, int n_kv_heads, const float* __restrict__ part,
@@ -77,27 +105,28 @@ __global__ __launch_bounds__(kRowThreads) void qkv_rope_kv_kernel(
   const int64_t page_base = (int64_t)page * page_stride;
   const float2* cs = rope_cs + (int64_t)rm.pos * half;
 
-  const int n_pairs = (n_q_heads + n_kv_heads) * half;
-  for (int p = threadIdx.x; p < n_pairs; p += kRowThreads) {
-    const int hh = p / half, i = p % half;
+  const int quads_per_head = half / 4;
+  const int n_quads = (n_q_heads + n_kv_heads) * quads_per_head;
+  for (int qd = threadIdx.x; qd < n_quads; qd += kRowThreads) {
+    const int hh = qd / quads_per_head, i = (qd % quads_per_head) * 4;
     const int c0 = hh * head_dim + i, c1 = c0 + half;
-    float a = 0.f, b = 0.f;
-    for (int s = 0; s < splits; ++s) {
-      a += pr[s * slab + c0];
-      b += pr[s * slab + c1];
+    float4 a = *(const float4*)(pr + c0), b = *(const float4*)(pr + c1);
+    for (int s = 1; s < splits; ++s) {
+      const float4 a2 = *(const float4*)(pr + s * slab + c0);
+      const float4 b2 = *(const float4*)(pr + s * slab + c1);
+      a.x += a2.x; a.y += a2.y; a.z += a2.z; a.w += a2.w;
+      b.x += b2.x; b.y += b2.y; b.z += b2.z; b.w += b2.w;
     }
-    const float2 t = cs[i];
-    const float ra = a * t.x - b * t.y;
-    const float rb = a * t.y + b * t.x;
-    if (hh < n_q_heads) {
-      T* qr = q_out + ((int64_t)row * n_q_heads + hh) * head_dim;
-      qr[i] = Store<T>::from(ra);
-      qr[i + half] = Store<T>::from(rb);
-    } else {
-      T* kr = kpool + page_base + ((int64_t)(hh - n_q_heads) * kPage + slot) * head_dim;
-      kr[i] = Store<T>::from(ra);
-      kr[i + half] = Store<T>::from(rb);
-    }
+    const float4 t01 = *(const float4*)(cs + i), t23 = *(const float4*)(cs + i + 2);
+    const float4 ra = make_float4(a.x * t01.x - b.x * t01.y, a.y * t01.z - b.y * t01.w,
+                                  a.z * t23.x - b.z * t23.y, a.w * t23.z - b.w * t23.w);
+    const float4 rb = make_float4(a.x * t01.y + b.x * t01.x, a.y * t01.w + b.y * t01.z,
+                                  a.z * t23.y + b.z * t23.x, a.w * t23.w + b.w * t23.z);
+    T* dst = (hh < n_q_heads)
+                 ? q_out + ((int64_t)row * n_q_heads + hh) * head_dim
+                 : kpool + page_base + ((int64_t)(hh - n_q_heads) * kPage + slot) * head_dim;
+    Pack4<T>::store(dst + i, ra);
+    Pack4<T>::store(dst + i + half, rb);
   }
   const int vcol0 = (n_q_heads + n_kv_heads) * head_dim;
   for (int idx = threadIdx.x; idx < n_kv_heads * head_dim; idx += kRowThreads) {
@@ -108,52 +137,68 @@ __global__ __launch_bounds__(kRowThreads) void qkv_rope_kv_kernel(
   }
 }
 
+// Four columns per thread (F % 4 == 0).
 template <typename HT>
 __global__ __launch_bounds__(256) void swiglu_kernel(int M, int F, const float* __restrict__ part,
                                                      int splits, HT* __restrict__ u) {
-  const int64_t n = (int64_t)M * F;
+  const int64_t n4 = (int64_t)M * F / 4;
   const int64_t slab = (int64_t)M * 2 * F;
-  for (int64_t idx = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; idx < n;
-       idx += (int64_t)gridDim.x * blockDim.x) {
+  for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n4;
+       q += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t idx = q * 4;
     const int64_t m = idx / F, c = idx % F;
-    float gt = 0.f, up = 0.f;
-    for (int s = 0; s < splits; ++s) {
-      gt += part[s * slab + m * 2 * F + c];
-      up += part[s * slab + m * 2 * F + F + c];
+    const float* pg = part + m * 2 * F + c;
+    float4 gt = *(const float4*)pg, up = *(const float4*)(pg + F);
+    for (int s = 1; s < splits; ++s) {
+      const float4 g2 = *(const float4*)(pg + s * slab), u2 = *(const float4*)(pg + s * slab + F);
+      gt.x += g2.x; gt.y += g2.y; gt.z += g2.z; gt.w += g2.w;
+      up.x += u2.x; up.y += u2.y; up.z += u2.z; up.w += u2.w;
     }
-    u[idx] = Store<HT>::from(gt / (1.f + expf(-gt)) * up);
+    const float4 r = make_float4(gt.x / (1.f + expf(-gt.x)) * up.x, gt.y / (1.f + expf(-gt.y)) * up.y,
+                                 gt.z / (1.f + expf(-gt.z)) * up.z, gt.w / (1.f + expf(-gt.w)) * up.w);
+    Pack4<HT>::store(u + idx, r);
   }
 }
 
-__global__ __launch_bounds__(256) void argmax_kernel(int V, const float* __restrict__ logits,
-                                                     int32_t* __restrict__ tokens) {
-  __shared__ float sv[256];
-  __shared__ int si[256];
+__device__ __forceinline__ void argmax_merge(float& v, int& i, float v2, int i2) {
+  if (v2 > v || (v2 == v && i2 < i)) {
+    v = v2;
+    i = i2;
+  }
+}
+
+// One work group of 1024 threads per row.  Ties go to the lowest index.
+__global__ __launch_bounds__(1024) void argmax_kernel(int V, const float* __restrict__ logits,
+                                                      int32_t* __restrict__ tokens) {
+  __shared__ float sv[16];
+  __shared__ int si[16];
   const float* lr = logits + (int64_t)blockIdx.x * V;
   float best = -INFINITY;
   int bi = 0x7FFFFFFF;
-  for (int i = threadIdx.x; i < V; i += 256) {
-    const float v = lr[i];
-    if (v > best) {  // strict: the first (lowest) index wins within a thread
-      best = v;
-      bi = i;
-    }
+  const int v4 = (((uintptr_t)lr & 15) == 0) ? V / 4 : 0;
+  for (int q = threadIdx.x; q < v4; q += 1024) {
+    const float4 v = *(const float4*)(lr + q * 4);
+    argmax_merge(best, bi, v.x, q * 4);
+    argmax_merge(best, bi, v.y, q * 4 + 1);
+    argmax_merge(best, bi, v.z, q * 4 + 2);
+    argmax_merge(best, bi, v.w, q * 4 + 3);
   }
-  sv[threadIdx.x] = best;
-  si[threadIdx.x] = bi;
+  for (int i = v4 * 4 + threadIdx.x; i < V; i += 1024) argmax_merge(best, bi, lr[i], i);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float v2 = __shfl_xor(best, o, 64);
+    const int i2 = __shfl_xor(bi, o, 64);
+    argmax_merge(best, bi, v2, i2);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    sv[threadIdx.x >> 6] = best;
+    si[threadIdx.x >> 6] = bi;
+  }
   __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if (threadIdx.x < o) {
-      const float v2 = sv[threadIdx.x + o];
-      const int i2 = si[threadIdx.x + o];
-      if (v2 > sv[threadIdx.x] || (v2 == sv[threadIdx.x] && i2 < si[threadIdx.x])) {
-        sv[threadIdx.x] = v2;
-        si[threadIdx.x] = i2;
-      }
-    }
-    __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 16; ++w) argmax_merge(best, bi, sv[w], si[w]);
+    tokens[blockIdx.x] = (bi == 0x7FFFFFFF) ? 0 : bi;
   }
-  if (threadIdx.x == 0) tokens[blockIdx.x] = (si[0] == 0x7FFFFFFF) ? 0 : si[0];
 }
 
 __global__ void bt_deltas_kernel(int n, const BtDelta* __restrict__ d, int32_t* __restrict__ bt,
@@ -195,12 +240,13 @@ hipError_t launch_embed_norm(int dtype, int M, int d, int vocab, const int32_t* 
 hipError_t launch_resid_norm(int dtype, int M, int d, const float* part, int splits, float* x,
                              const float* gain, float eps, void* h, hipStream_t stream) {
   if (M == 0) return hipSuccess;
+  const int threads = std::max(64, std::min(1024, (d / 4 + 63) / 64 * 64));
   if (dtype == 1)
-    resid_norm_kernel<uint16_t><<<M, kRowThreads, 0, stream>>>(M, d, part, splits, x, gain, eps,
-                                                               (uint16_t*)h);
+    resid_norm_kernel<uint16_t><<<M, threads, 0, stream>>>(M, d, part, splits, x, gain, eps,
+                                                           (uint16_t*)h);
   else
-    resid_norm_kernel<float><<<M, kRowThreads, 0, stream>>>(M, d, part, splits, x, gain, eps,
-                                                            (float*)h);
+    resid_norm_kernel<float><<<M, threads, 0, stream>>>(M, d, part, splits, x, gain, eps,
+                                                        (float*)h);
   return hipGetLastError();
 }
 
@@ -223,7 +269,7 @@ hipError_t launch_qkv_rope_kv(int dtype, int M, int head_dim, int n_q_heads, int
 
 hipError_t launch_swiglu(int dtype, int M, int F, const float* part, int splits, void* u,
                          hipStream_t stream) {
-  const int64_t n = (int64_t)M * F;
+  const int64_t n = (int64_t)M * F / 4;
   if (n == 0) return hipSuccess;
   if (dtype == 1)
     swiglu_kernel<uint16_t><<<grid_for(n, 256), 256, 0, stream>>>(M, F, part, splits,
@@ -235,7 +281,7 @@ hipError_t launch_swiglu(int dtype, int M, int F, const float* part, int splits,
 
 hipError_t launch_argmax(int B, int V, const float* logits, int32_t* tokens, hipStream_t stream) {
   if (B == 0) return hipSuccess;
-  argmax_kernel<<<B, 256, 0, stream>>>(V, logits, tokens);
+  argmax_kernel<<<B, 1024, 0, stream>>>(V, logits, tokens);
   return hipGetLastError();
 }
 
