@@ -46,6 +46,9 @@ WORKLOADS = {
     "decode-8b-b512-pareto": (512, ("pareto", 1.5, 1024, 65536)),
 }
 DEFAULT_WORKLOAD = "decode-8b-b256-lognormal"
+# Multi-turn rollouts: decode segments of 128 steps separated by tool-output
+# appends of U[512, 2048] tokens per trajectory through kv_append_prefix.
+MULTITURN = {f"multiturn-8b-b{b}": b for b in (16, 64, 256, 512)}
 
 
 def log(msg):
@@ -297,12 +300,108 @@ def run_decode(workload, steps, warmup, with_cpu):
     return out
 
 
+def run_multiturn(workload, segments, seg_steps, warmup):
+    """Decode segments with tool-output appends in between.
+
+    Capacity: the pool takes what HBM leaves after weights and workspace.
+    When an append does not fit, trajectories depart longest first until it
+    does (the pacing rule of evicting the longest resident), and the batch
+    continues without them.  Decode tokens/s counts decode_step + sample only;
+    append time is reported separately.
+    """
+    import torch
+
+    import paper_2609_36899_amd as P
+    from workload import EIGHT_B, lengths_uniform
+
+    shape = EIGHT_B
+    batch = MULTITURN[workload]
+    lens = draw_lengths(batch, ("pareto", 1.5, 1024, 65536))
+    adds = [lengths_uniform(batch, 512, 2048, seed=10 + k) for k in range(segments - 1)]
+    per_tok = P.kv_bytes_per_token(shape, P.BF16)
+    torch.cuda.set_device(0)
+    weights = gpu_weights(shape)
+    free_b, _ = torch.cuda.mem_get_info()
+    want = int(np.sum(lens)) + int(sum(a.sum() for a in adds)) + batch * (segments * seg_steps + warmup + 48)
+    pool_tokens = min(want, int((free_b - (24 << 30)) // per_tok))
+    pool_bytes = (pool_tokens // 16) * 16 * per_tok
+    max_len = int(lens.max()) + int(sum(a.max() for a in adds)) + segments * seg_steps + warmup + 32
+    log(f"{workload}: B={batch}, mean context {lens.mean():.0f}, pool {pool_bytes / 2**30:.1f} GiB")
+    E = P.Engine(shape, weights, P.BF16, pool_bytes, max_seqs=batch, max_seq_len=max_len,
+                 max_batch=batch, max_chunk=2048)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(3)
+    pool_bf16 = E.kv_pool.view(torch.bfloat16)
+    for i in range(0, pool_bf16.numel(), 1 << 30):
+        pool_bf16[i:i + (1 << 30)].normal_(0.0, 1.0, generator=g)
+    ids = [E.kv_alloc(0) for _ in range(batch)]
+    for sid, n in zip(ids, lens):
+        E.kv_extend_uninit(int(sid), int(n))
+    live = list(range(batch))
+    tok = torch.randint(0, shape.vocab, (batch,), dtype=torch.int32, device="cuda", generator=g)
+    logits = torch.empty((batch, shape.vocab), dtype=torch.float32, device="cuda")
+    rng = np.random.default_rng(5)
+    dec_ms, dec_tokens, app_ms, app_tokens, departed = 0.0, 0, 0.0, 0, 0
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for seg in range(segments):
+        idarr = np.array([ids[i] for i in live], dtype=np.int32)
+        B = len(idarr)
+        for _ in range(warmup if seg == 0 else 0):
+            E.decode_step(idarr, tok, logits)
+            E.sample(logits, tok, batch=B)
+        torch.cuda.synchronize()
+        ev0.record()
+        for _ in range(seg_steps):
+            E.decode_step(idarr, tok, logits)
+            E.sample(logits, tok, batch=B)
+        ev1.record()
+        torch.cuda.synchronize()
+        dec_ms += ev0.elapsed_time(ev1)
+        dec_tokens += B * seg_steps
+        log(f"segment {seg}: B={B}, {ev0.elapsed_time(ev1) / seg_steps:.2f} ms/step")
+        if seg == segments - 1:
+            break
+        need = int(sum(adds[seg][i] for i in live)) + len(live) * (seg_steps + 32)
+        while E.kv_headroom() < need and live:
+            longest = max(live, key=lambda i: E.kv_len(ids[i]))
+            E.kv_free(ids[longest])
+            live.remove(longest)
+            departed += 1
+            need = int(sum(adds[seg][i] for i in live)) + len(live) * (seg_steps + 32)
+        torch.cuda.synchronize()
+        ev0.record()
+        for i in live:
+            t = rng.integers(0, shape.vocab, size=int(adds[seg][i]), dtype=np.int32)
+            E.kv_append_prefix(ids[i], t, chunk_tokens=2048)
+            app_tokens += len(t)
+        ev1.record()
+        torch.cuda.synchronize()
+        app_ms += ev0.elapsed_time(ev1)
+        log(f"append {seg}: {app_tokens} tokens so far, {ev0.elapsed_time(ev1):.0f} ms")
+    out = {
+        "metric": METRIC, "value": round(dec_tokens / (dec_ms / 1e3), 2), "unit": "tokens/s",
+        "n_gpus": 1, "steps": segments * seg_steps, "warmup": warmup,
+        "ms_per_step": round(dec_ms / (segments * seg_steps), 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": workload, "batch": batch, "segments": segments,
+                   "steps_per_segment": seg_steps, "append_tokens": "U[512, 2048] per trajectory",
+                   "context_mean_initial": round(float(lens.mean()), 1),
+                   "pool_tokens": int(pool_bytes // per_tok)},
+        "departed": departed, "final_batch": len(live),
+        "append": {"tokens": int(app_tokens), "ms": round(app_ms, 1),
+                   "prefill_tokens_per_s": round(app_tokens / (app_ms / 1e3), 1) if app_ms else None},
+        "cpu_baseline": None,
+    }
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
+                    choices=sorted(WORKLOADS) + sorted(MULTITURN))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -310,7 +409,10 @@ def main():
               "and trajectories shard across GPUs as independent engines (data parallel, no "
               "exchange).  Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
-    out = run_decode(args.workload, args.steps, args.warmup, not args.no_cpu_baseline)
+    if args.workload in MULTITURN:
+        out = run_multiturn(args.workload, segments=3, seg_steps=args.steps, warmup=args.warmup)
+    else:
+        out = run_decode(args.workload, args.steps, args.warmup, not args.no_cpu_baseline)
     out["host"] = {"cpu": platform.processor() or platform.machine(), "cpu_count": os.cpu_count()}
     print(json.dumps(out), flush=True)
 

@@ -35,8 +35,8 @@ constexpr float kLog2e = 1.4426950408889634f;
 // 8*(q4%2) + (4u + rr) of page q4/2 for its query row c16: exactly the k-group
 // the PV MFMA expects from that lane, matching a single 16-byte V^T load.
 // ---------------------------------------------------------------------------
-template <int DH>
-__global__ __launch_bounds__(64) void attn_split_bf16(
+template <int DH, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void attn_split_bf16(
     const AttnItem* __restrict__ items, const AttnQBlock* __restrict__ qblocks,
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
     const uint16_t* __restrict__ vpool, int64_t page_stride, const int32_t* __restrict__ bt,
@@ -44,7 +44,8 @@ __global__ __launch_bounds__(64) void attn_split_bf16(
     float* __restrict__ part_ml, float* __restrict__ part_acc) {
   constexpr int KC = DH / 32;  // k-steps of QK^T
   constexpr int DT = DH / 16;  // 16-wide dim tiles of PV
-  const int lane = threadIdx.x;
+  constexpr int R = 16 * WAVES;  // query rows per item
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int c16 = lane & 15, q4 = lane >> 4;
   // The KV heads of one item are adjacent in the grid, so the work groups in
   // flight together read whole contiguous page regions ([page][Hkv][...]).
@@ -53,9 +54,13 @@ __global__ __launch_bounds__(64) void attn_split_bf16(
   const AttnQBlock qb = qblocks[it.qblock];
   const int G = n_q_heads / n_kv_heads;
 
-  // This lane's query row (the B column of S^T and O^T).
-  const int jq = c16 / G;
-  const int head = g * G + (c16 % G);
+  // This lane's query row (the B column of S^T and O^T).  In a multi-wave
+  // group every wave takes 16 rows of the block over the same keys; the
+  // waves' repeated page reads hit in L1/L2, so HBM sees each page once.
+  const int row = wave * 16 + c16;
+  if (wave * 16 >= qb.n_q * G) return;  // no rows for this wave; no barriers below
+  const int jq = row / G;
+  const int head = g * G + (row % G);
   const bool row_valid = jq < qb.n_q;
 
   bf16x8 qf[KC];
@@ -170,7 +175,7 @@ __global__ __launch_bounds__(64) void attn_split_bf16(
   l += __shfl_xor(l, 16, 64);
   l += __shfl_xor(l, 32, 64);
   if (row_valid) {
-    const int64_t prow = ((int64_t)item_id * n_kv_heads + g) * 16 + c16;
+    const int64_t prow = ((int64_t)item_id * n_kv_heads + g) * R + row;
     if (q4 == 0) {
       part_ml[prow * 2] = m;
       part_ml[prow * 2 + 1] = l;
@@ -191,7 +196,7 @@ __global__ __launch_bounds__(64) void attn_split_f32(
     const AttnItem* __restrict__ items, const AttnQBlock* __restrict__ qblocks,
     const float* __restrict__ q, const float* __restrict__ kpool, const float* __restrict__ vpool,
     int64_t page_stride, const int32_t* __restrict__ bt, int32_t bt_stride, int32_t n_q_heads,
-    int32_t n_kv_heads, float scale_log2, float* __restrict__ part_ml,
+    int32_t n_kv_heads, int32_t R, float scale_log2, float* __restrict__ part_ml,
     float* __restrict__ part_acc) {
   constexpr int E = DH / 64;
   const int lane = threadIdx.x;
@@ -231,7 +236,7 @@ __global__ __launch_bounds__(64) void attn_split_f32(
         acc[e] = acc[e] * alpha + p * vpool[base + (lane + 64 * e) * kPage + t];
       m = m_new;
     }
-    const int64_t prow = ((int64_t)item_id * n_kv_heads + g) * 16 + r;
+    const int64_t prow = ((int64_t)item_id * n_kv_heads + g) * R + r;
     if (lane == 0) {
       part_ml[prow * 2] = m;
       part_ml[prow * 2 + 1] = l;
@@ -242,125 +247,140 @@ __global__ __launch_bounds__(64) void attn_split_f32(
 }
 
 // ---------------------------------------------------------------------------
-// Merge the partials of each (query row, head) in item order with the
-// online-softmax rule: m = max(m, m_i); l = l e^(m_old-m) + l_i e^(m_i-m);
-// o likewise; output o / l.  One wave per (query block, KV head); a lane owns
-// DH/16 consecutive dims of one of four rows at a time.
+// Merge the partials of each (query row, head) with the online-softmax rule:
+// m = max(m, m_i); l = l e^(m_old-m) + l_i e^(m_i-m); o likewise; output o/l.
+// One work group of 4 waves per (query block, KV head).  Wave w merges items
+// w, w+4, w+8, ... (in order), then wave 0 merges the four results in wave
+// order, so the result is deterministic.  A lane owns DH/16 consecutive dims
+// of one of four rows at a time.
 // ---------------------------------------------------------------------------
+template <int DPL>
+__device__ __forceinline__ void merge_into(float& m, float& l, float* o, float mi, float li,
+                                           const float* oi) {
+  const float mn = fmaxf(m, mi);
+  const float mu = (mn == -INFINITY) ? 0.f : mn;  // both empty: keep zeros
+  const float so = exp2f(m - mu), si = exp2f(mi - mu);
+  l = l * so + li * si;
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) o[e] = o[e] * so + oi[e] * si;
+  m = mn;
+}
+
 template <int DH, typename OutT>
-__global__ __launch_bounds__(64) void attn_combine(const AttnQBlock* __restrict__ qblocks,
-                                                  const float* __restrict__ part_ml,
-                                                  const float* __restrict__ part_acc,
-                                                  int32_t n_q_heads, int32_t n_kv_heads,
-                                                  OutT* __restrict__ out) {
+__global__ __launch_bounds__(256) void attn_combine(const AttnQBlock* __restrict__ qblocks,
+                                                   const float* __restrict__ part_ml,
+                                                   const float* __restrict__ part_acc,
+                                                   int32_t n_q_heads, int32_t n_kv_heads, int32_t R,
+                                                   OutT* __restrict__ out) {
   constexpr int DPL = DH / 16;
-  const int lane = threadIdx.x, rsub = lane >> 4, d0 = (lane & 15) * DPL;
+  __shared__ float sh[4][64][DPL + 2];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int rsub = lane >> 4, d0 = (lane & 15) * DPL;
   const AttnQBlock qb = qblocks[blockIdx.x];
   const int g = blockIdx.y;
   const int G = n_q_heads / n_kv_heads;
   const int rows = qb.n_q * G;
-  for (int r = rsub; r < rows; r += 4) {
+  for (int r0 = 0; r0 < rows; r0 += 4) {
+    const int r = min(r0 + rsub, rows - 1);
     float m = -INFINITY, l = 0.f, o[DPL];
 #pragma unroll
     for (int e = 0; e < DPL; ++e) o[e] = 0.f;
-    // Items in groups of four: every load of a group is issued before use.
-    for (int i0 = qb.item_begin; i0 < qb.item_end; i0 += 4) {
+    // Items i0 + 4u (u = 0..3) of this wave's stride, loads issued first.
+    for (int i0 = qb.item_begin + wave; i0 < qb.item_end; i0 += 16) {
       float2 ml[4];
-      float4 a[4][DPL / 4];
+      float a[4][DPL];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int i = min(i0 + u, qb.item_end - 1);
-        const int64_t prow = ((int64_t)i * n_kv_heads + g) * 16 + r;
+        const int i = min(i0 + 4 * u, qb.item_end - 1);
+        const int64_t prow = ((int64_t)i * n_kv_heads + g) * R + r;
         ml[u] = *(const float2*)(part_ml + prow * 2);
 #pragma unroll
-        for (int e = 0; e < DPL / 4; ++e) a[u][e] = *(const float4*)(part_acc + prow * DH + d0 + 4 * e);
+        for (int e = 0; e < DPL; e += 4) {
+          const float4 v = *(const float4*)(part_acc + prow * DH + d0 + e);
+          a[u][e] = v.x;
+          a[u][e + 1] = v.y;
+          a[u][e + 2] = v.z;
+          a[u][e + 3] = v.w;
+        }
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        if (i0 + u >= qb.item_end) break;
-        // An item with no key visible to the row has m = -inf, l = 0, acc = 0.
-        const float mn = fmaxf(m, ml[u].x);
-        const float mu = (mn == -INFINITY) ? 0.f : mn;
-        const float so = exp2f(m - mu), si = exp2f(ml[u].x - mu);
-        l = l * so + ml[u].y * si;
-#pragma unroll
-        for (int e = 0; e < DPL / 4; ++e) {
-          o[4 * e] = o[4 * e] * so + a[u][e].x * si;
-          o[4 * e + 1] = o[4 * e + 1] * so + a[u][e].y * si;
-          o[4 * e + 2] = o[4 * e + 2] * so + a[u][e].z * si;
-          o[4 * e + 3] = o[4 * e + 3] * so + a[u][e].w * si;
-        }
-        m = mn;
+        if (i0 + 4 * u >= qb.item_end) break;
+        merge_into<DPL>(m, l, o, ml[u].x, ml[u].y, a[u]);
       }
     }
-    const float inv = 1.f / l;
-    const int jq = r / G, head = g * G + r % G;
-    OutT* orow = out + ((int64_t)(qb.q_row0 + jq) * n_q_heads + head) * DH + d0;
+    sh[wave][lane][0] = m;
+    sh[wave][lane][1] = l;
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) orow[e] = Store<OutT>::from(o[e] * inv);
+    for (int e = 0; e < DPL; ++e) sh[wave][lane][2 + e] = o[e];
+    __syncthreads();
+    if (wave == 0 && r0 + rsub < rows) {
+      for (int w = 1; w < 4; ++w)
+        merge_into<DPL>(m, l, o, sh[w][lane][0], sh[w][lane][1], &sh[w][lane][2]);
+      const float inv = 1.f / l;
+      const int jq = r / G, head = g * G + r % G;
+      OutT* orow = out + ((int64_t)(qb.q_row0 + jq) * n_q_heads + head) * DH + d0;
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) orow[e] = Store<OutT>::from(o[e] * inv);
+    }
+    __syncthreads();
   }
 }
 
 }  // namespace
 
-hipError_t launch_attention_split(int dtype, int head_dim, int n_items, int n_q_heads,
-                                  int n_kv_heads, const AttnItem* items,
+hipError_t launch_attention_split(int dtype, int head_dim, int rows_per_item, int n_items,
+                                  int n_q_heads, int n_kv_heads, const AttnItem* items,
                                   const AttnQBlock* qblocks, const void* q, const void* k_pages,
                                   const void* v_pages, int64_t page_stride_elems,
                                   const int32_t* block_table, int32_t bt_stride, float* part_ml,
                                   float* part_acc, hipStream_t stream) {
   if (n_items == 0) return hipSuccess;
-  const dim3 grid(n_kv_heads, n_items), block(64);
+  const dim3 grid(n_kv_heads, n_items);
   const float scale_log2 = kLog2e / sqrtf((float)head_dim);
   if (dtype == 1) {
-    if (head_dim == 128)
-      attn_split_bf16<128><<<grid, block, 0, stream>>>(
-          items, qblocks, (const uint16_t*)q, (const uint16_t*)k_pages,
-          (const uint16_t*)v_pages, page_stride_elems, block_table, bt_stride, n_q_heads,
-          n_kv_heads, scale_log2, part_ml, part_acc);
-    else
-      attn_split_bf16<64><<<grid, block, 0, stream>>>(
-          items, qblocks, (const uint16_t*)q, (const uint16_t*)k_pages,
-          (const uint16_t*)v_pages, page_stride_elems, block_table, bt_stride, n_q_heads,
-          n_kv_heads, scale_log2, part_ml, part_acc);
+    const uint16_t *qq = (const uint16_t*)q, *kk = (const uint16_t*)k_pages,
+                   *vv = (const uint16_t*)v_pages;
+#define PDEC_ATTN_BF16(DH_, W_)                                                              \
+  attn_split_bf16<DH_, W_><<<grid, dim3(64 * W_), 0, stream>>>(                             \
+      items, qblocks, qq, kk, vv, page_stride_elems, block_table, bt_stride, n_q_heads,     \
+      n_kv_heads, scale_log2, part_ml, part_acc)
+    if (head_dim == 128) {
+      if (rows_per_item == 64) PDEC_ATTN_BF16(128, 4); else PDEC_ATTN_BF16(128, 1);
+    } else {
+      if (rows_per_item == 64) PDEC_ATTN_BF16(64, 4); else PDEC_ATTN_BF16(64, 1);
+    }
+#undef PDEC_ATTN_BF16
   } else {
     if (head_dim == 128)
-      attn_split_f32<128><<<grid, block, 0, stream>>>(
+      attn_split_f32<128><<<grid, dim3(64), 0, stream>>>(
           items, qblocks, (const float*)q, (const float*)k_pages, (const float*)v_pages,
-          page_stride_elems, block_table, bt_stride, n_q_heads, n_kv_heads, scale_log2, part_ml,
-          part_acc);
+          page_stride_elems, block_table, bt_stride, n_q_heads, n_kv_heads, rows_per_item,
+          scale_log2, part_ml, part_acc);
     else
-      attn_split_f32<64><<<grid, block, 0, stream>>>(
+      attn_split_f32<64><<<grid, dim3(64), 0, stream>>>(
           items, qblocks, (const float*)q, (const float*)k_pages, (const float*)v_pages,
-          page_stride_elems, block_table, bt_stride, n_q_heads, n_kv_heads, scale_log2, part_ml,
-          part_acc);
+          page_stride_elems, block_table, bt_stride, n_q_heads, n_kv_heads, rows_per_item,
+          scale_log2, part_ml, part_acc);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_attention_combine(int head_dim, int n_qblocks, int n_q_heads, int n_kv_heads,
-                                    const AttnQBlock* qblocks, const float* part_ml,
-                                    const float* part_acc, void* out, int out_bf16,
-                                    hipStream_t stream) {
+hipError_t launch_attention_combine(int head_dim, int rows_per_item, int n_qblocks,
+                                    int n_q_heads, int n_kv_heads, const AttnQBlock* qblocks,
+                                    const float* part_ml, const float* part_acc, void* out,
+                                    int out_bf16, hipStream_t stream) {
   if (n_qblocks == 0) return hipSuccess;
-  const dim3 grid(n_qblocks, n_kv_heads), block(64);
+  const dim3 grid(n_qblocks, n_kv_heads), block(256);
+#define PDEC_COMBINE(DH_, T_)                                                                \
+  attn_combine<DH_, T_><<<grid, block, 0, stream>>>(qblocks, part_ml, part_acc, n_q_heads, \
+                                                    n_kv_heads, rows_per_item, (T_*)out)
   if (head_dim == 128) {
-    if (out_bf16)
-      attn_combine<128, uint16_t><<<grid, block, 0, stream>>>(qblocks, part_ml, part_acc,
-                                                              n_q_heads, n_kv_heads,
-                                                              (uint16_t*)out);
-    else
-      attn_combine<128, float><<<grid, block, 0, stream>>>(qblocks, part_ml, part_acc, n_q_heads,
-                                                           n_kv_heads, (float*)out);
+    if (out_bf16) PDEC_COMBINE(128, uint16_t); else PDEC_COMBINE(128, float);
   } else {
-    if (out_bf16)
-      attn_combine<64, uint16_t><<<grid, block, 0, stream>>>(qblocks, part_ml, part_acc,
-                                                             n_q_heads, n_kv_heads,
-                                                             (uint16_t*)out);
-    else
-      attn_combine<64, float><<<grid, block, 0, stream>>>(qblocks, part_ml, part_acc, n_q_heads,
-                                                          n_kv_heads, (float*)out);
+    if (out_bf16) PDEC_COMBINE(64, uint16_t); else PDEC_COMBINE(64, float);
   }
+#undef PDEC_COMBINE
   return hipGetLastError();
 }
 

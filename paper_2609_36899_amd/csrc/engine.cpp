@@ -187,11 +187,14 @@ class LaunchTimer {
 struct WsLayout {
   size_t rope, bt, meta, delta, x, h, o, u, q, part, att_ml, att_acc, total;
   size_t meta_bytes, part_elems, delta_cap;
-  int64_t items_cap, qblocks_cap, rows_cap;
+  int64_t items_cap, qblocks_cap, rows_cap, part_row_slots;
   int32_t bt_stride;
 };
 
 constexpr size_t kDeltaCap = 65536;
+// Query rows per attention work item: decode (one wave) and prefill (four).
+constexpr int kDecodeRows = 16;
+constexpr int kPrefillRows = 64;
 
 int check_cfg(const pdec_model_cfg* c) {
   if (!c) return fail(PDEC_INVALID_ARG, "null cfg");
@@ -239,8 +242,14 @@ int make_layout(const pdec_model_cfg* c, int32_t max_seqs, int32_t max_seq_len,
   const int64_t ab = elem_bytes(c->dtype);
   const int64_t qd = (int64_t)c->n_q_heads * c->head_dim;
   L->rows_cap = std::max(max_batch, max_chunk);
-  L->qblocks_cap = std::max<int64_t>(max_batch, (max_chunk + (16 / G) - 1) / (16 / G));
-  L->items_cap = attn_target_items(c->n_kv_heads) + L->qblocks_cap + 16;
+  // Decode: one query per block, 16-row items.  Prefill: kPrefillRows / G
+  // queries per block, 64-row items.
+  const int64_t pre_blocks = (max_chunk + (kPrefillRows / G) - 1) / (kPrefillRows / G);
+  L->qblocks_cap = std::max<int64_t>(max_batch, pre_blocks);
+  const int64_t items_dec = attn_target_items(c->n_kv_heads, kDecodeTargetGroups) + max_batch + 16;
+  const int64_t items_pre = attn_target_items(c->n_kv_heads, kPrefillTargetGroups) + pre_blocks + 16;
+  L->items_cap = std::max(items_dec, items_pre);
+  L->part_row_slots = std::max(items_dec * kDecodeRows, items_pre * kPrefillRows);
   L->bt_stride = PagePool::pages_for(max_seq_len);
   L->meta_bytes = align_up(L->rows_cap * sizeof(RowMeta)) +
                   align_up(L->qblocks_cap * sizeof(AttnQBlock)) +
@@ -263,8 +272,8 @@ int make_layout(const pdec_model_cfg* c, int32_t max_seqs, int32_t max_seq_len,
   L->u = take((size_t)L->rows_cap * c->ffn_dim * ab);
   L->q = take((size_t)L->rows_cap * qd * ab);
   L->part = take(L->part_elems * 4);
-  L->att_ml = take((size_t)L->items_cap * c->n_kv_heads * 16 * 2 * 4);
-  L->att_acc = take((size_t)L->items_cap * c->n_kv_heads * 16 * c->head_dim * 4);
+  L->att_ml = take((size_t)L->part_row_slots * c->n_kv_heads * 2 * 4);
+  L->att_acc = take((size_t)L->part_row_slots * c->n_kv_heads * c->head_dim * 4);
   L->total = off;
   return PDEC_OK;
 }
@@ -330,11 +339,12 @@ int flush_deltas(pdec_engine* E) {
 // logits of every row (lm_last_only = false) or of the last row only.
 int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
                     const std::vector<AttnQBlock>& qblocks, const std::vector<AttnItem>& items,
-                    const int32_t* tokens_dev, const int32_t* tokens_host, float* logits,
-                    bool lm_last_only) {
+                    int rows_per_item, const int32_t* tokens_dev, const int32_t* tokens_host,
+                    float* logits, bool lm_last_only) {
   const pdec_model_cfg& c = E->cfg;
   if ((int64_t)items.size() > E->ws.items_cap || (int64_t)qblocks.size() > E->ws.qblocks_cap ||
-      (int64_t)rows.size() > E->ws.rows_cap)
+      (int64_t)rows.size() > E->ws.rows_cap ||
+      (int64_t)items.size() * rows_per_item > E->ws.part_row_slots)
     return fail(PDEC_INVALID_ARG, "attention work list exceeds the workspace bound");
   int rc = flush_deltas(E);
   if (rc != PDEC_OK) return rc;
@@ -375,12 +385,13 @@ int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
                                    E->rope_cs, E->bt, E->ws.bt_stride, E->q, E->k_layer(l),
                                    E->v_layer(l), E->page_stride, s));
     HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_ATTENTION, s));
-    HIP_OR_FAIL(launch_attention_split(dt, Dh, n_items, c.n_q_heads, c.n_kv_heads, d_it, d_qb,
+    HIP_OR_FAIL(launch_attention_split(dt, Dh, rows_per_item, n_items, c.n_q_heads, c.n_kv_heads,
+                                       d_it, d_qb,
                                        E->q, E->k_layer(l), E->v_layer(l), E->page_stride, E->bt,
                                        E->ws.bt_stride, E->att_ml, E->att_acc, s));
     HIP_OR_FAIL(E->timer.end(s));
-    HIP_OR_FAIL(launch_attention_combine(Dh, n_qb, c.n_q_heads, c.n_kv_heads, d_qb, E->att_ml,
-                                         E->att_acc, E->o, dt == PDEC_BF16, s));
+    HIP_OR_FAIL(launch_attention_combine(Dh, rows_per_item, n_qb, c.n_q_heads, c.n_kv_heads, d_qb,
+                                         E->att_ml, E->att_acc, E->o, dt == PDEC_BF16, s));
     S = gemm_plan_splits(dt, M, d, qd, &ks);
     HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_GEMM, s));
     HIP_OR_FAIL(launch_gemm(dt, M, d, qd, E->o, qd, E->w_o[l], E->part, S, ks, s));
@@ -648,8 +659,10 @@ int decode_step(pdec_engine* E, int32_t B, const int32_t* ids, const int32_t* to
   }
   std::vector<AttnQBlock> qblocks;
   std::vector<AttnItem> items;
-  plan_attention(specs, choose_split_pages(total_key_pages(specs), E->cfg.n_kv_heads), &qblocks, &items);
-  int rc = enqueue_forward(E, B, rows, qblocks, items, tokens_dev, nullptr, logits, false);
+  plan_attention(specs, choose_split_pages(total_key_pages(specs), E->cfg.n_kv_heads), &qblocks,
+                 &items);
+  int rc = enqueue_forward(E, B, rows, qblocks, items, kDecodeRows, tokens_dev, nullptr, logits,
+                           false);
   if (rc != PDEC_OK) E->pool->undo(undo);
   return rc;
 }
@@ -671,7 +684,7 @@ int kv_append_prefix(pdec_engine* E, int32_t seq, const int32_t* tokens_host, in
   st = E->pool->grow(&slot, 1, n, &undo);
   if (!st.good()) return fail(st.code, st.msg);
 
-  const int QB = 16 / (E->cfg.n_q_heads / E->cfg.n_kv_heads);
+  const int QB = kPrefillRows / (E->cfg.n_q_heads / E->cfg.n_kv_heads);
   std::vector<RowMeta> rows;
   std::vector<QBlockSpec> specs;
   std::vector<AttnQBlock> qblocks;
@@ -683,9 +696,12 @@ int kv_append_prefix(pdec_engine* E, int32_t seq, const int32_t* tokens_host, in
     specs.clear();
     for (int k = 0; k * QB < C; ++k)
       specs.push_back({k * QB, std::min(QB, C - k * QB), slot, len0 + c0 + k * QB});
-    plan_attention(specs, choose_split_pages(total_key_pages(specs), E->cfg.n_kv_heads), &qblocks, &items);
+    plan_attention(specs,
+                   choose_split_pages(total_key_pages(specs), E->cfg.n_kv_heads,
+                                      kPrefillTargetGroups),
+                   &qblocks, &items);
     const bool last = c0 + C >= n;
-    int rc = enqueue_forward(E, C, rows, qblocks, items, nullptr, tokens_host + c0,
+    int rc = enqueue_forward(E, C, rows, qblocks, items, kPrefillRows, nullptr, tokens_host + c0,
                              last ? last_logits_dev : nullptr, true);
     if (rc != PDEC_OK) {
       E->pool->undo(undo);
@@ -763,12 +779,13 @@ int paged_decode_attention(int32_t dtype, int32_t B, int32_t Hq, int32_t Hkv, in
     HIP_OR_FAIL(g_attn_staging->upload(base, hm.data(), o_ml, s));
   }
   const int64_t page_stride = (int64_t)Hkv * kPage * Dh;
-  HIP_OR_FAIL(launch_attention_split(dtype, Dh, (int)items.size(), Hq, Hkv,
+  HIP_OR_FAIL(launch_attention_split(dtype, Dh, kDecodeRows, (int)items.size(), Hq, Hkv,
                                      (const AttnItem*)(base + o_it),
                                      (const AttnQBlock*)(base + o_qb), q, k_pages, v_pages,
                                      page_stride, bt, bt_stride, (float*)(base + o_ml),
                                      (float*)(base + o_acc), s));
-  HIP_OR_FAIL(launch_attention_combine(Dh, B, Hq, Hkv, (const AttnQBlock*)(base + o_qb),
+  HIP_OR_FAIL(launch_attention_combine(Dh, kDecodeRows, B, Hq, Hkv,
+                                       (const AttnQBlock*)(base + o_qb),
                                        (float*)(base + o_ml), (float*)(base + o_acc), out, 0, s));
   return PDEC_OK;
 }

@@ -19,10 +19,12 @@ struct WSegs {
 };
 
 // ---- attention --------------------------------------------------------------
-// Split pass: one work group per (item, KV head).  Writes per-row partial
-// softmax statistics part_ml [items][Hkv][16][2] = (max in log2 units, sum)
-// and unnormalised outputs part_acc [items][Hkv][16][head_dim].
-hipError_t launch_attention_split(int dtype, int head_dim, int n_items, int n_q_heads,
+// Split pass: one work group per (item, KV head) of rows_per_item / 16
+// waves (rows_per_item = 16 or 64).  Writes per-row partial softmax
+// statistics part_ml [items][Hkv][rows_per_item][2] = (max in log2 units,
+// sum) and unnormalised outputs part_acc [items][Hkv][rows_per_item][head_dim].
+hipError_t launch_attention_split(int dtype, int head_dim, int rows_per_item, int n_items,
+                                  int n_q_heads,
                                   int n_kv_heads, const AttnItem* items,
                                   const AttnQBlock* qblocks, const void* q, const void* k_pages,
                                   const void* v_pages, int64_t page_stride_elems,
@@ -31,7 +33,8 @@ hipError_t launch_attention_split(int dtype, int head_dim, int n_items, int n_q_
 
 // Merge pass: one work group per (query block, KV head); writes
 // out [rows][n_q_heads][head_dim] as fp32 (out_bf16 = 0) or bf16.
-hipError_t launch_attention_combine(int head_dim, int n_qblocks, int n_q_heads, int n_kv_heads,
+hipError_t launch_attention_combine(int head_dim, int rows_per_item, int n_qblocks,
+                                    int n_q_heads, int n_kv_heads,
                                     const AttnQBlock* qblocks, const float* part_ml,
                                     const float* part_acc, void* out, int out_bf16,
                                     hipStream_t stream);

@@ -115,15 +115,15 @@ void PagePool::undo(const GrowUndo& u) {
   pending_.resize(std::min(pending_.size(), u.old_pending));
 }
 
-int64_t attn_target_items(int32_t n_kv_heads) {
-  return std::max<int64_t>(1, kAttnTargetGroups / std::max(1, n_kv_heads));
+int64_t attn_target_items(int32_t n_kv_heads, int64_t target_groups) {
+  return std::max<int64_t>(1, target_groups / std::max(1, n_kv_heads));
 }
 
-int32_t choose_split_pages(int64_t total_pages, int32_t n_kv_heads) {
+int32_t choose_split_pages(int64_t total_pages, int32_t n_kv_heads, int64_t target_groups) {
   // Enough work groups to keep 256 CUs busy through the tail of the grid,
   // while the per-item fixed cost (query load, partial write) stays small
   // next to the item's KV bytes.
-  const int64_t target = attn_target_items(n_kv_heads);
+  const int64_t target = attn_target_items(n_kv_heads, target_groups);
   int64_t s = (total_pages + target - 1) / target;
   s = std::max<int64_t>(8, s);
   s = (s + 1) & ~int64_t(1);

@@ -86,16 +86,19 @@ struct QBlockSpec {
   int32_t q_row0, n_q, slot, pos0;
 };
 
-// Work groups the attention split pass aims for.
-constexpr int64_t kAttnTargetGroups = 16384;
+// Work groups the attention split pass aims for: decode launches one wave
+// per group, prefill four.
+constexpr int64_t kDecodeTargetGroups = 16384;
+constexpr int64_t kPrefillTargetGroups = 2048;
 
 // Items per KV head the planner aims for.
-int64_t attn_target_items(int32_t n_kv_heads);
+int64_t attn_target_items(int32_t n_kv_heads, int64_t target_groups = kDecodeTargetGroups);
 
 // Split size (in pages, even, at least 8) for a key-axis workload of
 // `total_pages` (summed over query blocks): the item count stays within
-// attn_target_items(n_kv_heads) plus one per query block.
-int32_t choose_split_pages(int64_t total_pages, int32_t n_kv_heads);
+// attn_target_items(n_kv_heads, target_groups) plus one per query block.
+int32_t choose_split_pages(int64_t total_pages, int32_t n_kv_heads,
+                           int64_t target_groups = kDecodeTargetGroups);
 
 // Cut every query block's key range [0, pos0 + n_q) into items of
 // `split_pages` pages.  Fills qblocks (with item ranges) and items.
