@@ -35,8 +35,14 @@ constexpr float kLog2e = 1.4426950408889634f;
 // 8*(q4%2) + (4u + rr) of page q4/2 for its query row c16: exactly the k-group
 // the PV MFMA expects from that lane, matching a single 16-byte V^T load.
 // ---------------------------------------------------------------------------
-template <int DH, int WAVES>
-__global__ __launch_bounds__(64 * WAVES) void attn_split_bf16(
+// RW x PW waves per work group.  RW > 1 (prefill): the waves take different
+// 16-row slices of the query block over the same keys; their repeated page
+// reads hit in L1/L2, so HBM sees each page once.  PW > 1 (decode): the waves
+// take interleaved page pairs of the item for the same 16 rows and are merged
+// through LDS at the end, so one item (and one partial) covers PW times the
+// pages a single wave streams.
+template <int DH, int RW, int PW>
+__global__ __launch_bounds__(64 * RW * PW) __attribute__((amdgpu_waves_per_eu(3))) void attn_split_bf16(
     const AttnItem* __restrict__ items, const AttnQBlock* __restrict__ qblocks,
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
     const uint16_t* __restrict__ vpool, int64_t page_stride, const int32_t* __restrict__ bt,
@@ -44,8 +50,10 @@ __global__ __launch_bounds__(64 * WAVES) void attn_split_bf16(
     float* __restrict__ part_ml, float* __restrict__ part_acc) {
   constexpr int KC = DH / 32;  // k-steps of QK^T
   constexpr int DT = DH / 16;  // 16-wide dim tiles of PV
-  constexpr int R = 16 * WAVES;  // query rows per item
+  constexpr int R = 16 * RW;  // query rows per item
+  static_assert(RW == 1 || PW == 1, "waves split either rows or pages");
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int rw = wave % RW, pw = wave / RW;
   const int c16 = lane & 15, q4 = lane >> 4;
   // The KV heads of one item are adjacent in the grid, so the work groups in
   // flight together read whole contiguous page regions ([page][Hkv][...]).
@@ -54,11 +62,9 @@ __global__ __launch_bounds__(64 * WAVES) void attn_split_bf16(
   const AttnQBlock qb = qblocks[it.qblock];
   const int G = n_q_heads / n_kv_heads;
 
-  // This lane's query row (the B column of S^T and O^T).  In a multi-wave
-  // group every wave takes 16 rows of the block over the same keys; the
-  // waves' repeated page reads hit in L1/L2, so HBM sees each page once.
-  const int row = wave * 16 + c16;
-  if (wave * 16 >= qb.n_q * G) return;  // no rows for this wave; no barriers below
+  // This lane's query row (the B column of S^T and O^T).
+  const int row = rw * 16 + c16;
+  if (PW == 1 && rw * 16 >= qb.n_q * G) return;  // no rows; no barriers when PW == 1
   const int jq = row / G;
   const int head = g * G + (row % G);
   const bool row_valid = jq < qb.n_q;
@@ -97,7 +103,7 @@ __global__ __launch_bounds__(64 * WAVES) void attn_split_bf16(
   for (int t = 0; t < DT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int n_iter = (it.n_pages + 1) >> 1;
-  for (int iter = 0; iter < n_iter; ++iter) {
+  for (int iter = pw; iter < n_iter; iter += PW) {
     const int pi = 2 * iter;
     const int page0 = btrow[pi];
     const int page1 = (pi + 1 < it.n_pages) ? btrow[pi + 1] : page0;
@@ -143,19 +149,27 @@ __global__ __launch_bounds__(64 * WAVES) void attn_split_bf16(
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
     const float m_new = fmaxf(m, mloc);
     const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = exp2f(m - m_use);
-    m = m_new;
-    l *= alpha;
+    // Rescale only when some row's running max moved (wave-uniform test).
+    if (__any(m_new != m)) {
+      const float alpha = __builtin_amdgcn_exp2f(m - m_use);
+      l *= alpha;
 #pragma unroll
-    for (int t = 0; t < DT; ++t) acc[t] *= alpha;
-
-    u16x8 pbits;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint16_t b = f32_to_bf16(exp2f(sv[e] - m_use));
-      pbits[e] = b;
-      l += bf16_to_f32(b);  // normalise by exactly the weights the MFMA uses
+      for (int t = 0; t < DT; ++t) acc[t] *= alpha;
     }
+    m = m_new;
+
+    // P in bf16 (hardware round-to-nearest-even); the normaliser sums exactly
+    // the rounded weights the MFMA consumes.
+    uint32_t pw4[4];
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const f32x2 pv = {__builtin_amdgcn_exp2f(sv[e] - m_use),
+                        __builtin_amdgcn_exp2f(sv[e + 1] - m_use)};
+      const uint32_t bits = __builtin_bit_cast(uint32_t, __builtin_convertvector(pv, bf16x2));
+      pw4[e / 2] = bits;
+      l += __uint_as_float(bits << 16) + __uint_as_float(bits & 0xFFFF0000u);
+    }
+    u16x8 pbits = __builtin_bit_cast(u16x8, u32x4{pw4[0], pw4[1], pw4[2], pw4[3]});
 
     if (key0 + (pi + 2) * kPage > kv_lim) {  // wave-uniform: the block's last keys
 #pragma unroll
@@ -174,6 +188,35 @@ __global__ __launch_bounds__(64 * WAVES) void attn_split_bf16(
 
   l += __shfl_xor(l, 16, 64);
   l += __shfl_xor(l, 32, 64);
+  if constexpr (PW > 1) {
+    // Page-split waves hand (m, l, acc) to wave 0, which merges them in wave
+    // order with the online-softmax rule.
+    __shared__ float sm[PW - 1][64][4 * DT + 2];
+    if (pw > 0) {
+      float* d = sm[pw - 1][lane];
+      d[0] = m;
+      d[1] = l;
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) d[2 + 4 * t + rr] = acc[t][rr];
+    }
+    __syncthreads();
+    if (pw > 0) return;
+#pragma unroll
+    for (int w = 0; w < PW - 1; ++w) {
+      const float* d = sm[w][lane];
+      const float mn = fmaxf(m, d[0]);
+      const float mu = (mn == -INFINITY) ? 0.f : mn;
+      const float so = exp2f(m - mu), sw = exp2f(d[0] - mu);
+      l = l * so + d[1] * sw;
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) acc[t][rr] = acc[t][rr] * so + d[2 + 4 * t + rr] * sw;
+      m = mn;
+    }
+  }
   if (row_valid) {
     const int64_t prow = ((int64_t)item_id * n_kv_heads + g) * R + row;
     if (q4 == 0) {
@@ -341,14 +384,16 @@ hipError_t launch_attention_split(int dtype, int head_dim, int rows_per_item, in
   if (dtype == 1) {
     const uint16_t *qq = (const uint16_t*)q, *kk = (const uint16_t*)k_pages,
                    *vv = (const uint16_t*)v_pages;
-#define PDEC_ATTN_BF16(DH_, W_)                                                              \
-  attn_split_bf16<DH_, W_><<<grid, dim3(64 * W_), 0, stream>>>(                             \
+#define PDEC_ATTN_BF16(DH_, RW_, PW_)                                                        \
+  attn_split_bf16<DH_, RW_, PW_><<<grid, dim3(64 * RW_ * PW_), 0, stream>>>(                \
       items, qblocks, qq, kk, vv, page_stride_elems, block_table, bt_stride, n_q_heads,     \
       n_kv_heads, scale_log2, part_ml, part_acc)
+    // 64-row items (prefill): waves split rows.  16-row items (decode): waves
+    // split pages.
     if (head_dim == 128) {
-      if (rows_per_item == 64) PDEC_ATTN_BF16(128, 4); else PDEC_ATTN_BF16(128, 1);
+      if (rows_per_item == 64) PDEC_ATTN_BF16(128, 4, 1); else PDEC_ATTN_BF16(128, 1, 4);
     } else {
-      if (rows_per_item == 64) PDEC_ATTN_BF16(64, 4); else PDEC_ATTN_BF16(64, 1);
+      if (rows_per_item == 64) PDEC_ATTN_BF16(64, 4, 1); else PDEC_ATTN_BF16(64, 1, 4);
     }
 #undef PDEC_ATTN_BF16
   } else {

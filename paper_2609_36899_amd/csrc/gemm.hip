@@ -28,7 +28,8 @@ __device__ __forceinline__ const void* seg_row(const WSegs& w, int n, int64_t ro
   return w.ptr[0];
 }
 
-// Small batches (M <= 8 in practice, up to 64 supported).  Each wave owns 16 columns of the 64-column
+// Small batches (M <= 4 with long K in practice, up to 64 supported).  Each
+// wave owns 16 columns of the 64-column
 // block and every row of the batch, so no two waves share weight bytes.  The
 // weight fragments are prefetched NS k-steps ahead through a register ring so
 // that enough HBM bytes are in flight to hide the memory latency; the
@@ -104,7 +105,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_small_m(int M, int N, int K,
     }
 }
 
-// Larger batches (M > 8): 128 x 128 output tiles, four waves in a 2 x 2
+// Larger batches (M > 4): 128 x 128 output tiles, four waves in a 2 x 2
 // grid of 64 x 64 sub-tiles.  Per k-step of 64 the A tile (128 rows) and the
 // W tile (128 columns) are staged once through LDS (double-buffered, 16-byte
 // chunks XOR-swizzled by row) and each is shared by the two waves that need
@@ -221,6 +222,69 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_tile128(int M, int N, int K,
     }
 }
 
+// VALU weight-streaming GEMV for tiny batches (M <= 4): out[m][n] =
+// sum_k x[m][k] W[n][k] with v_dot2_f32_bf16.  Each wave streams whole
+// contiguous weight rows (a row of K bf16 is K*2 contiguous bytes, read 1 KiB
+// per instruction), so the weight stream is long sequential runs; the batch's
+// activations sit in LDS.  Every wave covers the full K of its rows: no
+// split-K, results go straight to out (splits = 1).
+// Whole vectors are reinterpreted and split by shuffles (bit-casting a
+// single vector element would read the vector's first element).
+__device__ __forceinline__ float dot8(const u32x4 w, const u32x4 x, float acc) {
+  const bf16x8 wb = __builtin_bit_cast(bf16x8, w), xb = __builtin_bit_cast(bf16x8, x);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(wb, wb, 0, 1),
+                                        __builtin_shufflevector(xb, xb, 0, 1), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(wb, wb, 2, 3),
+                                        __builtin_shufflevector(xb, xb, 2, 3), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(wb, wb, 4, 5),
+                                        __builtin_shufflevector(xb, xb, 4, 5), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(wb, wb, 6, 7),
+                                        __builtin_shufflevector(xb, xb, 6, 7), acc, false);
+  return acc;
+}
+
+template <int M>
+__global__ __launch_bounds__(256) void gemv_bf16(int N, int K, int rows_per_wave,
+                                                 const uint16_t* __restrict__ x, int64_t ldx,
+                                                 WSegs w, float* __restrict__ out) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [M][K]
+  for (int i = threadIdx.x * 8; i < M * K; i += 256 * 8) {
+    const int m = i / K, k = i % K;
+    *(u32x4*)(xs + i) = *(const u32x4*)(x + (int64_t)m * ldx + k);
+  }
+  __syncthreads();
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int n0 = (blockIdx.x * 4 + wave) * rows_per_wave;
+  const int n1 = min(N, n0 + rows_per_wave);
+  for (int n = n0; n < n1; ++n) {
+    const uint16_t* wr = (const uint16_t*)seg_row(w, n, K, 2);
+    float acc[M];
+#pragma unroll
+    for (int m = 0; m < M; ++m) acc[m] = 0.f;
+    int k = lane * 8;
+    for (; k + 3 * 512 < K; k += 4 * 512) {
+      u32x4 wv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) wv[u] = load_stream<u32x4>(wr + k + u * 512);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int m = 0; m < M; ++m)
+          acc[m] = dot8(wv[u], *(const u32x4*)(xs + m * K + k + u * 512), acc[m]);
+    }
+    for (; k < K; k += 512) {
+      const u32x4 wv = load_stream<u32x4>(wr + k);
+#pragma unroll
+      for (int m = 0; m < M; ++m) acc[m] = dot8(wv, *(const u32x4*)(xs + m * K + k), acc[m]);
+    }
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      const float v = wave_sum(acc[m]);
+      if (lane == m) out[(int64_t)m * N + n] = v;
+    }
+  }
+}
+
 // fp32: 32 x 64 tiles through LDS, 2 x 4 outputs per thread.
 __global__ __launch_bounds__(256) void gemm_f32_tiled(int M, int N, int K, int k_split,
                                                       const float* __restrict__ A, int64_t lda,
@@ -265,13 +329,29 @@ __global__ __launch_bounds__(256) void gemm_f32_tiled(int M, int N, int K, int k
 
 }  // namespace
 
-// Batches up to this size use the register-ring kernel without LDS; above it
-// the 128 x 128 tile kernel is faster (measured on the 8B projection shapes).
-constexpr int kSmallM = 8;
+// Kernel choice for bf16, from measurements on the 8B projection shapes:
+//  * GEMV (VALU dot2, whole-row streaming) while the batch's activations fit
+//    in 64 KB of LDS and M <= 4: 6.2-6.6 TB/s at M = 1, ahead of MFMA up to
+//    M = 4;
+//  * the register-ring MFMA kernel for the remaining M <= 4 (long K);
+//  * the 128 x 128 tile MFMA kernel above that.
+enum class GemmPath { kGemv, kSmallM, kTile128 };
+
+GemmPath bf16_path(int M, int K) {
+  if (M <= 4 && (int64_t)M * K * 2 <= 64 * 1024) return GemmPath::kGemv;
+  if (M <= 4) return GemmPath::kSmallM;
+  return GemmPath::kTile128;
+}
+
+constexpr int kGemvWaves = 2048;
 
 int gemm_plan_splits(int dtype, int M, int N, int K, int* k_split) {
   const int kq = (dtype == 1) ? 64 : 16;
-  const bool tile128 = dtype == 1 && M > kSmallM;
+  if (dtype == 1 && bf16_path(M, K) == GemmPath::kGemv) {
+    *k_split = K;
+    return 1;
+  }
+  const bool tile128 = dtype == 1 && bf16_path(M, K) == GemmPath::kTile128;
   const int mblk = (dtype == 1) ? (tile128 ? 128 : 64) : 32;
   const int nblk = tile128 ? 128 : 64;
   const int64_t tiles = (int64_t)((N + nblk - 1) / nblk) * ((M + mblk - 1) / mblk);
@@ -295,7 +375,18 @@ hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t ld
   const dim3 block(256);
   if (dtype == 1) {
     const uint16_t* a = (const uint16_t*)A;
-    if (M <= kSmallM) {
+    const GemmPath path = bf16_path(M, K);
+    if (path == GemmPath::kGemv) {
+      const int rpw = (N + kGemvWaves - 1) / kGemvWaves;
+      const dim3 grid((N + 4 * rpw - 1) / (4 * rpw));
+      const size_t lds = (size_t)M * K * 2;
+      switch (M) {
+        case 1: gemv_bf16<1><<<grid, block, lds, stream>>>(N, K, rpw, a, lda, w, out); break;
+        case 2: gemv_bf16<2><<<grid, block, lds, stream>>>(N, K, rpw, a, lda, w, out); break;
+        case 3: gemv_bf16<3><<<grid, block, lds, stream>>>(N, K, rpw, a, lda, w, out); break;
+        default: gemv_bf16<4><<<grid, block, lds, stream>>>(N, K, rpw, a, lda, w, out); break;
+      }
+    } else if (path == GemmPath::kSmallM) {
       const dim3 grid((N + 63) / 64, 1, splits);
       switch ((M + 15) / 16) {
         case 1: gemm_bf16_small_m<1, 8><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;

@@ -86,9 +86,8 @@ struct QBlockSpec {
   int32_t q_row0, n_q, slot, pos0;
 };
 
-// Work groups the attention split pass aims for: decode launches one wave
-// per group, prefill four.
-constexpr int64_t kDecodeTargetGroups = 16384;
+// Work groups the attention split pass aims for (four waves each).
+constexpr int64_t kDecodeTargetGroups = 4096;
 constexpr int64_t kPrefillTargetGroups = 2048;
 
 // Items per KV head the planner aims for.
