@@ -105,24 +105,28 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_small_m(int M, int N, int K,
     }
 }
 
-// Larger batches (M > 4): 128 x 128 output tiles, four waves in a 2 x 2
-// grid of 64 x 64 sub-tiles.  Per k-step of 64 the A tile (128 rows) and the
-// W tile (128 columns) are staged once through LDS (double-buffered, 16-byte
-// chunks XOR-swizzled by row) and each is shared by the two waves that need
-// it; the tiles of the next NS k-steps are prefetched into a register ring
-// meanwhile (NS even: ring slot s also names the LDS buffer s & 1).
-// Work-group ids are laid out so that the M-blocks of one column tile are
-// dispatched back to back onto the same XCD (ids L and L+8 share an XCD):
-// the first streams the W tile from HBM, the others find it in that XCD's L2
-// (so these loads carry no streaming hint).
-template <int NS>
-__global__ __launch_bounds__(256, 2) void gemm_bf16_tile128(int M, int N, int K, int k_split,
-                                                            int n_mb, int n_nb,
-                                                            const uint16_t* __restrict__ A,
-                                                            int64_t lda, WSegs w,
-                                                            float* __restrict__ out) {
+// Larger batches (M > 4): (64 WM) x 128 output tiles, 2 WM waves in a WM x 2
+// grid of 64 x 64 sub-tiles.  Per k-step of 64 the A tile and the W tile are
+// staged once through LDS (double-buffered, 16-byte chunks XOR-swizzled by
+// row) and each is shared by the waves that need it; the tiles of the next
+// NS k-steps are prefetched into a register ring meanwhile (NS even: ring
+// slot s also names the LDS buffer s & 1).  WM = 4 covers 256 rows, so up to
+// that batch size W is read from HBM exactly once per step.  Larger batches
+// take several M-blocks, laid out so the M-blocks of one column tile are
+// dispatched back to back (ids L and L+8 share an XCD).
+template <int WM, int NS>
+__global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, int k_split,
+                                                          int n_mb, int n_nb,
+                                                          const uint16_t* __restrict__ A,
+                                                          int64_t lda, WSegs w,
+                                                          float* __restrict__ out) {
   constexpr int MT = 4, NT = 4;
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][128 * 64];
+  constexpr int THREADS = 128 * WM, ROWS = 64 * WM;
+  constexpr int RSTEP = THREADS / 8;  // rows covered by one chunk column of the group
+  constexpr int ACH = ROWS / RSTEP;   // A chunks per thread (4)
+  constexpr int WCH = 128 / RSTEP;    // W chunks per thread
+  __shared__ __attribute__((aligned(16))) uint16_t la_s[2][ROWS * 64];
+  __shared__ __attribute__((aligned(16))) uint16_t lw_s[2][128 * 64];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int c16 = lane & 15, q4 = lane >> 4;
   const int L = blockIdx.x;
@@ -132,19 +136,19 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_tile128(int M, int N, int K,
   const int kbeg = blockIdx.z * k_split;
   const int n_iter = (min(K, kbeg + k_split) - kbeg) / 64;
   if (n_iter <= 0) return;
-  const int m_blk = mb * 128, n_blk = nb * 128;
+  const int m_blk = mb * ROWS, n_blk = nb * 128;
   const int wm = wave >> 1, wn = wave & 1;
 
-  // Staging: 128 rows x 8 chunks per tile, 4 chunks per thread (rows r + 32j).
   const int r = tid >> 3, c = tid & 7;
-  const int dst = r * 64 + ((c ^ (r & 7)) * 8);  // + 32j*64 for chunk j
-  const uint16_t* asrc[4];
-  const uint16_t* wsrc[4];
+  const int dst = r * 64 + ((c ^ (r & 7)) * 8);  // + j * RSTEP * 64 for chunk j
+  const uint16_t* asrc[ACH];
+  const uint16_t* wsrc[WCH];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    asrc[j] = A + (int64_t)min(m_blk + r + 32 * j, M - 1) * lda + kbeg + c * 8;
-    wsrc[j] = (const uint16_t*)seg_row(w, min(n_blk + r + 32 * j, N - 1), K, 2) + kbeg + c * 8;
-  }
+  for (int j = 0; j < ACH; ++j)
+    asrc[j] = A + (int64_t)min(m_blk + r + RSTEP * j, M - 1) * lda + kbeg + c * 8;
+#pragma unroll
+  for (int j = 0; j < WCH; ++j)
+    wsrc[j] = (const uint16_t*)seg_row(w, min(n_blk + r + RSTEP * j, N - 1), K, 2) + kbeg + c * 8;
   int aoff[MT][2], boff[NT][2];
 #pragma unroll
   for (int t = 0; t < 4; ++t)
@@ -161,36 +165,32 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_tile128(int M, int N, int K,
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // Register ring of NS k-steps (A and W chunks of this thread).
-  u16x8 ra_[NS][4], rw_[NS][4];
+  u16x8 ra_[NS][ACH], rw_[NS][WCH];
 #pragma unroll
   for (int s = 0; s < NS; ++s)
     if (s < n_iter) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        ra_[s][j] = *(const u16x8*)(asrc[j] + s * 64);
-        rw_[s][j] = *(const u16x8*)(wsrc[j] + s * 64);
-      }
+      for (int j = 0; j < ACH; ++j) ra_[s][j] = *(const u16x8*)(asrc[j] + s * 64);
+#pragma unroll
+      for (int j = 0; j < WCH; ++j) rw_[s][j] = *(const u16x8*)(wsrc[j] + s * 64);
     }
   for (int it0 = 0; it0 < n_iter; it0 += NS) {
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
       const int it = it0 + s;
       if (it >= n_iter) break;
-      uint16_t* la = lds[s & 1][0];
-      uint16_t* lw = lds[s & 1][1];
+      uint16_t* la = la_s[s & 1];
+      uint16_t* lw = lw_s[s & 1];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        *(u16x8*)(la + dst + j * 32 * 64) = ra_[s][j];
-        *(u16x8*)(lw + dst + j * 32 * 64) = rw_[s][j];
-      }
+      for (int j = 0; j < ACH; ++j) *(u16x8*)(la + dst + j * RSTEP * 64) = ra_[s][j];
+#pragma unroll
+      for (int j = 0; j < WCH; ++j) *(u16x8*)(lw + dst + j * RSTEP * 64) = rw_[s][j];
       __syncthreads();
       if (it + NS < n_iter) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          ra_[s][j] = *(const u16x8*)(asrc[j] + (it + NS) * 64);
-          rw_[s][j] = *(const u16x8*)(wsrc[j] + (it + NS) * 64);
-        }
+        for (int j = 0; j < ACH; ++j) ra_[s][j] = *(const u16x8*)(asrc[j] + (it + NS) * 64);
+#pragma unroll
+        for (int j = 0; j < WCH; ++j) rw_[s][j] = *(const u16x8*)(wsrc[j] + (it + NS) * 64);
       }
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
@@ -345,21 +345,24 @@ GemmPath bf16_path(int M, int K) {
 
 constexpr int kGemvWaves = 2048;
 
+// Rows per tile: 128 (4 waves) up to 128-row batches, 256 (8 waves) beyond,
+// so W is read once per step for batches up to 256.
+int tile_rows(int M) { return M <= 128 ? 128 : 256; }
+
 int gemm_plan_splits(int dtype, int M, int N, int K, int* k_split) {
   const int kq = (dtype == 1) ? 64 : 16;
   if (dtype == 1 && bf16_path(M, K) == GemmPath::kGemv) {
     *k_split = K;
     return 1;
   }
-  const bool tile128 = dtype == 1 && bf16_path(M, K) == GemmPath::kTile128;
-  const int mblk = (dtype == 1) ? (tile128 ? 128 : 64) : 32;
-  const int nblk = tile128 ? 128 : 64;
+  const bool tile = dtype == 1 && bf16_path(M, K) == GemmPath::kTile128;
+  const int mblk = (dtype == 1) ? (tile ? tile_rows(M) : 64) : 32;
+  const int nblk = tile ? 128 : 64;
   const int64_t tiles = (int64_t)((N + nblk - 1) / nblk) * ((M + mblk - 1) / mblk);
   // Small batches: aim for two work groups per CU; the partial sums are
-  // small.  Larger batches: one per CU, since every extra split writes and
-  // re-reads an M x N fp32 slab.
-  const int64_t target = (dtype == 1 && M > 64) ? 256 : 512;
-
+  // small.  Larger batches: about one per CU, since every extra split writes
+  // and re-reads an M x N fp32 slab; the 256-row tile holds a whole CU.
+  const int64_t target = !tile || M <= 64 ? 512 : (M <= 128 ? 256 : 224);
   const int ksteps = (K + kq - 1) / kq;
   int s = 1;
   if (tiles < target) s = (int)std::min<int64_t>((target + tiles - 1) / tiles, 8);
@@ -395,10 +398,15 @@ hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t ld
         default: gemm_bf16_small_m<4, 8><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
       }
     } else {
-      const int n_mb = (M + 127) / 128, n_nb = (N + 127) / 128;
+      const int rows = tile_rows(M);
+      const int n_mb = (M + rows - 1) / rows, n_nb = (N + 127) / 128;
       const dim3 grid(((n_nb + 7) / 8) * 8 * n_mb, 1, splits);
-      gemm_bf16_tile128<2><<<grid, block, 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a, lda, w,
-                                                      out);
+      if (rows == 128)
+        gemm_bf16_tile<2, 2><<<grid, dim3(256), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a, lda,
+                                                            w, out);
+      else
+        gemm_bf16_tile<4, 2><<<grid, dim3(512), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a, lda,
+                                                            w, out);
     }
   } else {
     const dim3 grid((N + 63) / 64, (M + 31) / 32, splits);
