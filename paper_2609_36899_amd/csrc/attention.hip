@@ -57,7 +57,7 @@ __global__ __launch_bounds__(64 * RW * PW) __attribute__((amdgpu_waves_per_eu(3)
   const int c16 = lane & 15, q4 = lane >> 4;
   // The KV heads of one item are adjacent in the grid, so the work groups in
   // flight together read whole contiguous page regions ([page][Hkv][...]).
-  const int g = blockIdx.x, item_id = blockIdx.y;
+  const int g = blockIdx.x, item_id = items[blockIdx.y].order;
   const AttnItem it = items[item_id];
   const AttnQBlock qb = qblocks[it.qblock];
   const int G = n_q_heads / n_kv_heads;
@@ -243,7 +243,7 @@ __global__ __launch_bounds__(64) void attn_split_f32(
     float* __restrict__ part_acc) {
   constexpr int E = DH / 64;
   const int lane = threadIdx.x;
-  const int g = blockIdx.x, item_id = blockIdx.y;
+  const int g = blockIdx.x, item_id = items[blockIdx.y].order;
   const AttnItem it = items[item_id];
   const AttnQBlock qb = qblocks[it.qblock];
   const int G = n_q_heads / n_kv_heads;

@@ -96,9 +96,9 @@ int32_t pp_choose_split(int64_t total_pages, int32_t n_kv_heads) {
 int64_t pp_target_items(int32_t n_kv_heads) { return attn_target_items(n_kv_heads); }
 
 // specs: n x (q_row0, n_q, slot, pos0).  Writes qblocks as 6 ints
-// (q_row0, n_q, slot, pos0, item_begin, item_end) and items as 3 ints
-// (qblock, page_begin, n_pages).  Returns the item count (or -1 if the item
-// buffer is too small).
+// (q_row0, n_q, slot, pos0, item_begin, item_end) and items as 4 ints
+// (qblock, page_begin, n_pages, order).  Returns the item count (or -1 if the
+// item buffer is too small).
 int32_t pp_plan(const int32_t* specs, int32_t n, int32_t split, int32_t* qb_out,
                 int32_t* items_out, int32_t items_cap) {
   std::vector<QBlockSpec> sp(n);
@@ -114,9 +114,10 @@ int32_t pp_plan(const int32_t* specs, int32_t n, int32_t split, int32_t* qb_out,
     std::memcpy(qb_out + 6 * i, v, sizeof(v));
   }
   for (size_t i = 0; i < it.size(); ++i) {
-    items_out[3 * i] = it[i].qblock;
-    items_out[3 * i + 1] = it[i].page_begin;
-    items_out[3 * i + 2] = it[i].n_pages;
+    items_out[4 * i] = it[i].qblock;
+    items_out[4 * i + 1] = it[i].page_begin;
+    items_out[4 * i + 2] = it[i].n_pages;
+    items_out[4 * i + 3] = it[i].order;
   }
   return (int32_t)it.size();
 }

@@ -34,7 +34,9 @@ struct AttnItem {
   int32_t qblock;
   int32_t page_begin;
   int32_t n_pages;
-  int32_t pad;
+  // Dispatch order: grid slot d processes item items[d].order.  The planner
+  // orders items longest first so the short ones fill the tail of the grid.
+  int32_t order;
 };
 
 // A block-table entry to write on the device: bt[slot][idx] = page.

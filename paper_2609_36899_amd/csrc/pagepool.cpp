@@ -154,6 +154,12 @@ void plan_attention(const std::vector<QBlockSpec>& specs, int32_t split_pages,
     b.item_end = (int32_t)items->size();
     qblocks->push_back(b);
   }
+  std::vector<int32_t> ord(items->size());
+  for (size_t i = 0; i < ord.size(); ++i) ord[i] = (int32_t)i;
+  std::stable_sort(ord.begin(), ord.end(), [&](int32_t a, int32_t b) {
+    return (*items)[a].n_pages > (*items)[b].n_pages;
+  });
+  for (size_t i = 0; i < ord.size(); ++i) (*items)[i].order = ord[i];
 }
 
 }  // namespace pdec

@@ -100,7 +100,8 @@ int32_t choose_split_pages(int64_t total_pages, int32_t n_kv_heads,
                            int64_t target_groups = kDecodeTargetGroups);
 
 // Cut every query block's key range [0, pos0 + n_q) into items of
-// `split_pages` pages.  Fills qblocks (with item ranges) and items.
+// `split_pages` pages.  Fills qblocks (with item ranges) and items, and sets
+// the dispatch order of the items (longest first, ties in item order).
 void plan_attention(const std::vector<QBlockSpec>& specs, int32_t split_pages,
                     std::vector<AttnQBlock>* qblocks, std::vector<AttnItem>* items);
 

@@ -84,7 +84,7 @@ __global__ __launch_bounds__(1024) void resid_norm_kernel(
   }
 }
 
-// One work group per row.  Pairs (i, i + Dh/2) of every q and k head are
+// A row is handled by gridDim.y work groups.  Pairs (i, i + Dh/2) of every q and k head are
 // rotated by the table angle of the row's position, four pairs per thread;
 // v is copied.  K goes to [page][g][slot][Dh], V to the transposed block
 // [page][g][Dh][slot].
@@ -105,9 +105,11 @@ __global__ __launch_bounds__(kRowThreads) void qkv_rope_kv_kernel(
   const int64_t page_base = (int64_t)page * page_stride;
   const float2* cs = rope_cs + (int64_t)rm.pos * half;
 
+  // blockIdx.y splits the row's work across gridDim.y groups.
+  const int part_id = blockIdx.y, n_parts = gridDim.y;
   const int quads_per_head = half / 4;
   const int n_quads = (n_q_heads + n_kv_heads) * quads_per_head;
-  for (int qd = threadIdx.x; qd < n_quads; qd += kRowThreads) {
+  for (int qd = part_id * kRowThreads + threadIdx.x; qd < n_quads; qd += n_parts * kRowThreads) {
     const int hh = qd / quads_per_head, i = (qd % quads_per_head) * 4;
     const int c0 = hh * head_dim + i, c1 = c0 + half;
     float4 a = *(const float4*)(pr + c0), b = *(const float4*)(pr + c1);
@@ -129,7 +131,8 @@ __global__ __launch_bounds__(kRowThreads) void qkv_rope_kv_kernel(
     Pack4<T>::store(dst + i + half, rb);
   }
   const int vcol0 = (n_q_heads + n_kv_heads) * head_dim;
-  for (int idx = threadIdx.x; idx < n_kv_heads * head_dim; idx += kRowThreads) {
+  for (int idx = part_id * kRowThreads + threadIdx.x; idx < n_kv_heads * head_dim;
+       idx += n_parts * kRowThreads) {
     float v = 0.f;
     for (int s = 0; s < splits; ++s) v += pr[s * slab + vcol0 + idx];
     const int g = idx / head_dim, dd = idx % head_dim;
@@ -256,12 +259,14 @@ hipError_t launch_qkv_rope_kv(int dtype, int M, int head_dim, int n_q_heads, int
                               void* q_out, void* k_pages, void* v_pages, int64_t page_stride_elems,
                               hipStream_t stream) {
   if (M == 0) return hipSuccess;
+  // Enough groups per row that small batches still fill the GPU.
+  const dim3 grid(M, M >= 64 ? 2 : 8);
   if (dtype == 1)
-    qkv_rope_kv_kernel<uint16_t><<<M, kRowThreads, 0, stream>>>(
+    qkv_rope_kv_kernel<uint16_t><<<grid, kRowThreads, 0, stream>>>(
         M, head_dim, n_q_heads, n_kv_heads, part, splits, rows, rope_cs, block_table, bt_stride,
         (uint16_t*)q_out, (uint16_t*)k_pages, (uint16_t*)v_pages, page_stride_elems);
   else
-    qkv_rope_kv_kernel<float><<<M, kRowThreads, 0, stream>>>(
+    qkv_rope_kv_kernel<float><<<grid, kRowThreads, 0, stream>>>(
         M, head_dim, n_q_heads, n_kv_heads, part, splits, rows, rope_cs, block_table, bt_stride,
         (float*)q_out, (float*)k_pages, (float*)v_pages, page_stride_elems);
   return hipGetLastError();

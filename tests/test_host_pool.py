@@ -240,11 +240,16 @@ def _plan(lib, specs, split):
     arr = (c_int32 * (4 * len(specs)))(*[v for s in specs for v in s])
     cap = 200000
     qb = (c_int32 * (6 * len(specs)))()
-    it = (c_int32 * (3 * cap))()
+    it = (c_int32 * (4 * cap))()
     n = lib.pp_plan(arr, len(specs), split, qb, it, cap)
     assert n >= 0
     qbs = [tuple(qb[6 * i:6 * i + 6]) for i in range(len(specs))]
-    items = [tuple(it[3 * i:3 * i + 3]) for i in range(n)]
+    items = [tuple(it[4 * i:4 * i + 3]) for i in range(n)]
+    order = [it[4 * i + 3] for i in range(n)]
+    # The dispatch order is a permutation, longest items first.
+    assert sorted(order) == list(range(n))
+    sizes = [items[o][2] for o in order]
+    assert sizes == sorted(sizes, reverse=True)
     return qbs, items
 
 
