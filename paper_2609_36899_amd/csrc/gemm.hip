@@ -114,7 +114,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_small_m(int M, int N, int K,
 // that batch size W is read from HBM exactly once per step.  Larger batches
 // take several M-blocks, laid out so the M-blocks of one column tile are
 // dispatched back to back (ids L and L+8 share an XCD).
-template <int WM, int NS>
+template <int WM, int NS, int NA>
 __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, int k_split,
                                                           int n_mb, int n_nb,
                                                           const uint16_t* __restrict__ A,
@@ -165,14 +165,18 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  u16x8 ra_[NS][ACH], rw_[NS][WCH];
+  // W (from HBM) is prefetched NS k-steps ahead, A (L2-resident) NA.
+  static_assert(NS % NA == 0 && NA % 2 == 0, "ring depths");
+  u16x8 ra_[NA][ACH], rw_[NS][WCH];
 #pragma unroll
   for (int s = 0; s < NS; ++s)
     if (s < n_iter) {
 #pragma unroll
-      for (int j = 0; j < ACH; ++j) ra_[s][j] = *(const u16x8*)(asrc[j] + s * 64);
-#pragma unroll
       for (int j = 0; j < WCH; ++j) rw_[s][j] = *(const u16x8*)(wsrc[j] + s * 64);
+      if (s < NA) {
+#pragma unroll
+        for (int j = 0; j < ACH; ++j) ra_[s][j] = *(const u16x8*)(asrc[j] + s * 64);
+      }
     }
   for (int it0 = 0; it0 < n_iter; it0 += NS) {
 #pragma unroll
@@ -182,15 +186,17 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
       uint16_t* la = la_s[s & 1];
       uint16_t* lw = lw_s[s & 1];
 #pragma unroll
-      for (int j = 0; j < ACH; ++j) *(u16x8*)(la + dst + j * RSTEP * 64) = ra_[s][j];
+      for (int j = 0; j < ACH; ++j) *(u16x8*)(la + dst + j * RSTEP * 64) = ra_[s % NA][j];
 #pragma unroll
       for (int j = 0; j < WCH; ++j) *(u16x8*)(lw + dst + j * RSTEP * 64) = rw_[s][j];
       __syncthreads();
       if (it + NS < n_iter) {
 #pragma unroll
-        for (int j = 0; j < ACH; ++j) ra_[s][j] = *(const u16x8*)(asrc[j] + (it + NS) * 64);
-#pragma unroll
         for (int j = 0; j < WCH; ++j) rw_[s][j] = *(const u16x8*)(wsrc[j] + (it + NS) * 64);
+      }
+      if (it + NA < n_iter) {
+#pragma unroll
+        for (int j = 0; j < ACH; ++j) ra_[s % NA][j] = *(const u16x8*)(asrc[j] + (it + NA) * 64);
       }
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
@@ -402,11 +408,11 @@ hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t ld
       const int n_mb = (M + rows - 1) / rows, n_nb = (N + 127) / 128;
       const dim3 grid(((n_nb + 7) / 8) * 8 * n_mb, 1, splits);
       if (rows == 128)
-        gemm_bf16_tile<2, 2><<<grid, dim3(256), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a, lda,
-                                                            w, out);
+        gemm_bf16_tile<2, 2, 2><<<grid, dim3(256), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a,
+                                                               lda, w, out);
       else
-        gemm_bf16_tile<4, 2><<<grid, dim3(512), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a, lda,
-                                                            w, out);
+        gemm_bf16_tile<4, 2, 2><<<grid, dim3(512), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a,
+                                                               lda, w, out);
     }
   } else {
     const dim3 grid((N + 63) / 64, (M + 31) / 32, splits);
