@@ -395,13 +395,76 @@ def run_multiturn(workload, segments, seg_steps, warmup):
     return out
 
 
+def run_kv_transfer(lengths=(4096, 16384, 65536)):
+    """Prepared KV versus re-prefill for one departing trajectory.
+
+    For each context length: kv_export of the trajectory's KV into pinned
+    host memory (device to host), kv_import into a fresh sequence (host to
+    device), and kv_append_prefix re-prefilling the same tokens.  This is
+    the prepared-transfer versus re-prefill trade-off of late-bound KV
+    preparation, on one GPU.
+    """
+    import torch
+
+    import paper_2609_36899_amd as P
+    from workload import EIGHT_B, random_tokens
+
+    shape = EIGHT_B
+    per_tok = P.kv_bytes_per_token(shape, P.BF16)
+    torch.cuda.set_device(0)
+    weights = gpu_weights(shape)
+    pool_tokens = 3 * max(lengths) + 4096
+    E = P.Engine(shape, weights, P.BF16, pool_tokens * per_tok, max_seqs=8,
+                 max_seq_len=max(lengths) + 64, max_batch=8, max_chunk=2048)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    rows = []
+    for n in lengths:
+        toks = random_tokens(n, shape.vocab, seed=n)
+        a = E.kv_alloc(0)
+        torch.cuda.synchronize()
+        ev0.record()
+        E.kv_append_prefix(a, toks, chunk_tokens=2048)
+        ev1.record()
+        torch.cuda.synchronize()
+        prefill_ms = ev0.elapsed_time(ev1)
+        snap = torch.empty(E.kv_snapshot_bytes(n), dtype=torch.uint8).pin_memory()
+        ev0.record()
+        E.kv_export(a, snap)
+        ev1.record()
+        torch.cuda.synchronize()
+        export_ms = ev0.elapsed_time(ev1)
+        E.kv_free(a)
+        b = E.kv_alloc(0)
+        ev0.record()
+        E.kv_import(b, snap, n)
+        ev1.record()
+        torch.cuda.synchronize()
+        import_ms = ev0.elapsed_time(ev1)
+        E.kv_free(b)
+        nbytes = snap.numel()
+        rows.append({"tokens": n, "snapshot_bytes": nbytes, "export_ms": round(export_ms, 2),
+                     "export_GBps": round(nbytes / export_ms / 1e6, 1),
+                     "import_ms": round(import_ms, 2),
+                     "import_GBps": round(nbytes / import_ms / 1e6, 1),
+                     "reprefill_ms": round(prefill_ms, 1),
+                     "reprefill_tokens_per_s": round(n / prefill_ms * 1e3, 1)})
+        log(f"kv transfer {n}: export {export_ms:.1f} ms, import {import_ms:.1f} ms, "
+            f"re-prefill {prefill_ms:.0f} ms")
+        del snap
+    return {"metric": "KV snapshot/restore vs re-prefill, 8B-shaped, 1 MI355X",
+            "value": rows[-1]["reprefill_ms"] / rows[-1]["import_ms"], "unit": "x (re-prefill / import)",
+            "n_gpus": 1, "higher_is_better": True, "data": "synthetic", "dtype": "bf16",
+            "config": {"workload": "kv-transfer-8b", "lengths": list(lengths)}, "rows": rows,
+            "cpu_baseline": None}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
-                    choices=sorted(WORKLOADS) + sorted(MULTITURN))
+                    choices=sorted(WORKLOADS) + sorted(MULTITURN) + ["kv-transfer-8b"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -409,7 +472,9 @@ def main():
               "and trajectories shard across GPUs as independent engines (data parallel, no "
               "exchange).  Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
-    if args.workload in MULTITURN:
+    if args.workload == "kv-transfer-8b":
+        out = run_kv_transfer()
+    elif args.workload in MULTITURN:
         out = run_multiturn(args.workload, segments=3, seg_steps=args.steps, warmup=args.warmup)
     else:
         out = run_decode(args.workload, args.steps, args.warmup, not args.no_cpu_baseline)

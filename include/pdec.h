@@ -205,6 +205,32 @@ int kv_append_prefix(pdec_engine* engine, int32_t seq, const int32_t* tokens_hos
 int decode_step(pdec_engine* engine, int32_t batch, const int32_t* seq_ids_host,
                 const int32_t* tokens_dev, float* logits_dev);
 
+/* KV snapshot of a resident trajectory into host memory: phase 1 of the
+ * paper's late-bound KV preparation, where a departing trajectory's KV is
+ * copied from device memory to host DRAM over PCIe so its pages can be freed
+ * while the host copy keeps it available (Design, "KV Preparation for
+ * Late-Bound Placement").  host_dst must be PINNED host memory (hipHostMalloc)
+ * of at least ceil(len/16) * 16 * kv_bytes_per_token bytes.  Layout of the
+ * snapshot, page-major so that a prefix range of pages is one contiguous
+ * range: [page][layer][K|V][n_kv_heads][16 * head_dim] with the V block
+ * transposed as in the pool.  The copy is enqueued on the engine's stream;
+ * synchronise it before reading host_dst.  The sequence stays resident (call
+ * kv_free to depart); later work on the stream cannot overwrite its pages
+ * before the copy has run.  *n_tokens_out receives the sequence length.
+ * Errors: PDEC_BAD_SEQ, PDEC_INVALID_ARG (buffer too small or not pinned). */
+int kv_export(pdec_engine* engine, int32_t seq, void* host_dst, int64_t dst_bytes,
+              int32_t* n_tokens_out);
+
+/* Restore a snapshot written by kv_export into an EMPTY sequence (fresh from
+ * kv_alloc): pages for n_tokens are taken atomically and filled from
+ * host_src (pinned host memory, same layout), and the sequence length
+ * becomes n_tokens.  The alternative to re-prefilling the prefix from its
+ * tokens (kv_append_prefix).
+ * Errors: PDEC_BAD_SEQ, PDEC_OUT_OF_PAGES, PDEC_SEQ_TOO_LONG,
+ * PDEC_INVALID_ARG (non-empty sequence, buffer too small or not pinned). */
+int kv_import(pdec_engine* engine, int32_t seq, const void* host_src, int64_t src_bytes,
+              int32_t n_tokens);
+
 /* Next tokens from logits: mode 0 = greedy argmax, ties to the lowest id
  * (the paper does not state its sampler).  logits_dev: device fp32
  * [batch][vocab]; tokens_dev_out: device int32 [batch].

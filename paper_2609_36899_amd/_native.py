@@ -75,6 +75,8 @@ SIGNATURES = {
                                    c_void_p]),
     "decode_step": (c_int32, [c_void_p, c_int32, POINTER(c_int32), c_void_p, c_void_p]),
     "sample": (c_int32, [c_void_p, c_int32, c_void_p, c_void_p, c_int32]),
+    "kv_export": (c_int32, [c_void_p, c_int32, c_void_p, c_int64, POINTER(c_int32)]),
+    "kv_import": (c_int32, [c_void_p, c_int32, c_void_p, c_int64, c_int32]),
     "paged_attention_workspace_bytes": (c_int64, [c_int32, c_int32, c_int32, c_int32, c_int64]),
     "paged_decode_attention": (c_int32, [c_int32, c_int32, c_int32, c_int32, c_int32, c_void_p,
                                          c_void_p, c_void_p, c_void_p, c_int32, POINTER(c_int32),

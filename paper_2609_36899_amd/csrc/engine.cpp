@@ -711,6 +711,73 @@ int kv_append_prefix(pdec_engine* E, int32_t seq, const int32_t* tokens_host, in
   return PDEC_OK;
 }
 
+namespace {
+
+// Device-visible address of pinned host memory (fails for pageable memory).
+int host_device_ptr(const void* host, void** dev) {
+  hipError_t e = hipHostGetDevicePointer(dev, const_cast<void*>(host), 0);
+  if (e != hipSuccess || !*dev)
+    return fail(PDEC_INVALID_ARG, "host buffer must be pinned (hipHostMalloc) memory");
+  return PDEC_OK;
+}
+
+int enqueue_page_copy(pdec_engine* E, const std::vector<int32_t>& pages, int n_pages,
+                      void* host_dev, int to_host) {
+  if ((size_t)n_pages * sizeof(int32_t) > E->ws.delta_cap * sizeof(BtDelta))
+    return fail(PDEC_INVALID_ARG, "sequence too long for one snapshot call");
+  int rc = flush_deltas(E);
+  if (rc != PDEC_OK) return rc;
+  HIP_OR_FAIL(E->staging.upload(E->delta, pages.data(), (size_t)n_pages * 4, E->stream));
+  const int64_t block_bytes = E->page_stride * E->ab();
+  HIP_OR_FAIL(launch_kv_page_copy(n_pages, (const int32_t*)E->delta, E->cfg.n_layers, E->n_pages,
+                                  block_bytes, E->kv_pool, host_dev, to_host, E->stream));
+  return PDEC_OK;
+}
+
+}  // namespace
+
+int kv_export(pdec_engine* E, int32_t seq, void* host_dst, int64_t dst_bytes,
+              int32_t* n_tokens_out) {
+  if (!E || !host_dst || !n_tokens_out) return fail(PDEC_INVALID_ARG, "null argument");
+  int32_t slot;
+  Status st = E->pool->resolve(seq, &slot);
+  if (!st.good()) return fail(st.code, st.msg);
+  const int32_t len = E->pool->len(slot);
+  const int n_pages = PagePool::pages_for(len);
+  const int64_t need = (int64_t)n_pages * kPage * kv_token_bytes(&E->cfg);
+  if (dst_bytes < need)
+    return fail(PDEC_INVALID_ARG, "host buffer too small: need " + std::to_string(need));
+  void* dev = nullptr;
+  int rc = host_device_ptr(host_dst, &dev);
+  if (rc != PDEC_OK) return rc;
+  rc = enqueue_page_copy(E, E->pool->pages(slot), n_pages, dev, 1);
+  if (rc == PDEC_OK) *n_tokens_out = len;
+  return rc;
+}
+
+int kv_import(pdec_engine* E, int32_t seq, const void* host_src, int64_t src_bytes,
+              int32_t n_tokens) {
+  if (!E || !host_src) return fail(PDEC_INVALID_ARG, "null argument");
+  if (n_tokens < 1) return fail(PDEC_INVALID_ARG, "n_tokens must be >= 1");
+  int32_t slot;
+  Status st = E->pool->resolve(seq, &slot);
+  if (!st.good()) return fail(st.code, st.msg);
+  if (E->pool->len(slot) != 0) return fail(PDEC_INVALID_ARG, "kv_import needs an empty sequence");
+  const int n_pages = PagePool::pages_for(n_tokens);
+  const int64_t need = (int64_t)n_pages * kPage * kv_token_bytes(&E->cfg);
+  if (src_bytes < need)
+    return fail(PDEC_INVALID_ARG, "host buffer too small: need " + std::to_string(need));
+  void* dev = nullptr;
+  int rc = host_device_ptr(host_src, &dev);
+  if (rc != PDEC_OK) return rc;
+  PagePool::GrowUndo undo;
+  st = E->pool->grow(&slot, 1, n_tokens, &undo);
+  if (!st.good()) return fail(st.code, st.msg);
+  rc = enqueue_page_copy(E, E->pool->pages(slot), n_pages, dev, 0);
+  if (rc != PDEC_OK) E->pool->undo(undo);
+  return rc;
+}
+
 int sample(pdec_engine* E, int32_t B, const float* logits_dev, int32_t* tokens_dev_out,
            int32_t mode) {
   if (!E || !logits_dev || !tokens_dev_out) return fail(PDEC_INVALID_ARG, "null argument");

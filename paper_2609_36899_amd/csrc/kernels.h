@@ -75,4 +75,12 @@ hipError_t launch_bt_deltas(int n, const BtDelta* deltas, int32_t* bt, int32_t s
 hipError_t launch_rope_table(int max_pos, int head_dim, double base, float2* cs,
                              hipStream_t stream);
 
+// ---- KV snapshot / restore ---------------------------------------------------
+// Copy whole pages between the pool and a host buffer mapped for the device.
+// Page i of the list moves between pool block [layer][kind][pages[i]] and
+// host bytes [(i * n_layers * 2 + layer * 2 + kind) * block_bytes, + block_bytes).
+hipError_t launch_kv_page_copy(int n_pages, const int32_t* pages_dev, int n_layers,
+                               int64_t n_pool_pages, int64_t block_bytes, void* pool,
+                               void* host_dev_ptr, int to_host, hipStream_t stream);
+
 }  // namespace pdec

@@ -196,6 +196,27 @@ class Engine:
         N.check(self.lib.decode_step(self.handle, B, ids.ctypes.data_as(POINTER(c_int32)),
                                      tokens.data_ptr(), logits.data_ptr()))
 
+    def kv_snapshot_bytes(self, n_tokens: int) -> int:
+        """Host bytes kv_export needs for a sequence of n_tokens tokens."""
+        return -(-int(n_tokens) // PAGE_TOKENS) * PAGE_TOKENS * self.kv_token_bytes
+
+    def kv_export(self, seq: int, host_dst: torch.Tensor) -> int:
+        """Snapshot a sequence's KV into a pinned host tensor; returns its length.
+
+        The copy is asynchronous on the engine's stream: synchronise before
+        reading host_dst."""
+        assert host_dst.device.type == "cpu" and host_dst.is_pinned() and host_dst.is_contiguous()
+        n = c_int32()
+        N.check(self.lib.kv_export(self.handle, int(seq), host_dst.data_ptr(),
+                                   host_dst.numel() * host_dst.element_size(), byref(n)))
+        return n.value
+
+    def kv_import(self, seq: int, host_src: torch.Tensor, n_tokens: int) -> None:
+        """Restore a kv_export snapshot into an empty sequence."""
+        assert host_src.device.type == "cpu" and host_src.is_pinned() and host_src.is_contiguous()
+        N.check(self.lib.kv_import(self.handle, int(seq), host_src.data_ptr(),
+                                   host_src.numel() * host_src.element_size(), int(n_tokens)))
+
     def sample(self, logits: torch.Tensor, tokens_out: torch.Tensor, mode: int = 0,
                batch: Optional[int] = None) -> None:
         B = batch if batch is not None else logits.shape[0]
