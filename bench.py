@@ -395,6 +395,60 @@ def run_multiturn(workload, segments, seg_steps, warmup):
     return out
 
 
+PROJ_SHAPES = [("qkv", 6144, 4096), ("o", 4096, 4096), ("gate_up", 28672, 4096),
+               ("down", 4096, 14336), ("lm_head", 128256, 4096)]
+
+
+def run_projections(batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), iters=20):
+    """The 8B projection shapes through weight_projection, swept over the batch.
+
+    Per shape and batch: time per call (HIP events), weight-stream GB/s,
+    TFLOP/s, and the roofline time max(weights / 8 TB/s, flops / 2.5 PF/s).
+    """
+    import torch
+
+    import paper_2609_36899_amd as P
+
+    torch.cuda.set_device(0)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    rows = []
+    for name, n, k in PROJ_SHAPES:
+        w = torch.empty((n, k), dtype=torch.bfloat16, device="cuda").normal_(0, 0.02, generator=g)
+        for m in batches:
+            x = torch.empty((m, k), dtype=torch.bfloat16, device="cuda").normal_(generator=g)
+            out = torch.empty((m, n), dtype=torch.float32, device="cuda")
+            ws = torch.empty(max(1, P.weight_projection_workspace_bytes(P.BF16, m, n, k)),
+                             dtype=torch.uint8, device="cuda")
+            for _ in range(3):
+                P.weight_projection(x, w, out, ws)
+            torch.cuda.synchronize()
+            ev0.record()
+            for _ in range(iters):
+                P.weight_projection(x, w, out, ws)
+            ev1.record()
+            torch.cuda.synchronize()
+            us = ev0.elapsed_time(ev1) / iters * 1e3
+            wbytes, flops = 2 * n * k, 2 * m * n * k
+            roof_us = max(wbytes / HBM_PEAK_GBS / 1e3, flops / 2.5e15 * 1e6)
+            rows.append({"shape": name, "N": n, "K": k, "M": m, "us": round(us, 2),
+                         "weight_GBps": round(wbytes / us / 1e3, 1),
+                         "TFLOPs": round(flops / us / 1e6, 1),
+                         "roofline_us": round(roof_us, 2), "frac_of_roofline": round(roof_us / us, 3)})
+        log(f"projections {name} done")
+    layer = {}
+    for r in rows:
+        if r["shape"] != "lm_head":
+            layer[r["M"]] = layer.get(r["M"], 0.0) + r["us"]
+    return {"metric": "weight projection time per 8B layer, 1 MI355X", "value": layer.get(256),
+            "unit": "us at batch 256", "n_gpus": 1, "higher_is_better": False,
+            "data": "synthetic", "dtype": "bf16",
+            "config": {"workload": "projections-8b", "batches": list(batches)},
+            "layer_us": {str(m): round(v, 1) for m, v in layer.items()}, "rows": rows,
+            "cpu_baseline": None}
+
+
 def run_kv_transfer(lengths=(4096, 16384, 65536)):
     """Prepared KV versus re-prefill for one departing trajectory.
 
@@ -464,7 +518,8 @@ def main():
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
-                    choices=sorted(WORKLOADS) + sorted(MULTITURN) + ["kv-transfer-8b"])
+                    choices=sorted(WORKLOADS) + sorted(MULTITURN)
+                    + ["kv-transfer-8b", "projections-8b"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -474,6 +529,8 @@ def main():
         sys.exit(2)
     if args.workload == "kv-transfer-8b":
         out = run_kv_transfer()
+    elif args.workload == "projections-8b":
+        out = run_projections()
     elif args.workload in MULTITURN:
         out = run_multiturn(args.workload, segments=3, seg_steps=args.steps, warmup=args.warmup)
     else:

@@ -255,6 +255,23 @@ int sample(pdec_engine* engine, int32_t batch, const float* logits_dev, int32_t*
  *   workspace: device, at least paged_attention_workspace_bytes(...).
  * Slots past lens[b] in the last page are never read.
  * ------------------------------------------------------------------------- */
+/* ---------------------------------------------------------------------------
+ * Isolated weight projection: out = x W^T with the engine's own plan and
+ * kernels (GEMV for tiny batches, MFMA GEMMs otherwise, split-K summed in a
+ * fixed order).  Each decode step reads the weights once for the whole batch
+ * (Introduction; Design Principles, "Specialization in Heterogeneous Pools").
+ *   x: device [M][K] in dtype; w: device [N][K] in dtype (nn.Linear layout);
+ *   out: device fp32 [M][N]; workspace: device, at least
+ *   weight_projection_workspace_bytes(...) bytes (may be 0).
+ * Errors: PDEC_UNSUPPORTED (bf16 with K % 64 != 0, N % 4 != 0),
+ * PDEC_INVALID_ARG.
+ * ------------------------------------------------------------------------- */
+int64_t weight_projection_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K);
+
+int weight_projection(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* x,
+                      const void* w, float* out, void* workspace, int64_t workspace_bytes,
+                      void* stream);
+
 int64_t paged_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
                                         int32_t head_dim, int64_t max_total_tokens);
 

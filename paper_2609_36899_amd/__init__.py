@@ -12,7 +12,8 @@ def __getattr__(name):
     # The torch-facing binding is imported lazily so that host-only tooling
     # (build, ABI checks) does not pay for importing torch.
     if name in ("Engine", "paged_decode_attention", "paged_attention_workspace_bytes",
-                "kv_bytes_per_token", "weights_to_device", "model_cfg"):
+                "kv_bytes_per_token", "weights_to_device", "model_cfg", "weight_projection",
+                "weight_projection_workspace_bytes"):
         from . import engine
         return getattr(engine, name)
     raise AttributeError(name)

@@ -787,6 +787,38 @@ int sample(pdec_engine* E, int32_t B, const float* logits_dev, int32_t* tokens_d
   return PDEC_OK;
 }
 
+int64_t weight_projection_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K) {
+  if ((dtype != PDEC_F32 && dtype != PDEC_BF16) || M < 1 || N < 1 || K < 1)
+    return fail(PDEC_INVALID_ARG, "bad projection arguments");
+  int ks;
+  const int S = gemm_plan_splits(dtype, M, N, K, &ks);
+  return S > 1 ? (int64_t)S * M * N * 4 : 0;
+}
+
+int weight_projection(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* x,
+                      const void* w, float* out, void* workspace, int64_t ws_bytes,
+                      void* stream) {
+  if (!x || !w || !out) return fail(PDEC_INVALID_ARG, "null argument");
+  const int64_t need = weight_projection_workspace_bytes(dtype, M, N, K);
+  if (need < 0) return (int)need;
+  if (dtype == PDEC_BF16 && K % 64)
+    return fail(PDEC_UNSUPPORTED, "bf16 projections need K % 64 == 0");
+  if (N % 4) return fail(PDEC_UNSUPPORTED, "projections need N % 4 == 0");
+  if (ws_bytes < need || (need > 0 && !workspace))
+    return fail(PDEC_INVALID_ARG, "workspace too small: need " + std::to_string(need));
+  WSegs ws{};
+  ws.ptr[0] = w;
+  ws.row_end[0] = N;
+  ws.n_seg = 1;
+  int ks;
+  const int S = gemm_plan_splits(dtype, M, N, K, &ks);
+  hipStream_t s = (hipStream_t)stream;
+  float* dst = S > 1 ? (float*)workspace : out;
+  HIP_OR_FAIL(launch_gemm(dtype, M, N, K, x, K, ws, dst, S, ks, s));
+  if (S > 1) HIP_OR_FAIL(launch_sum_splits((int64_t)M * N, dst, S, out, s));
+  return PDEC_OK;
+}
+
 int64_t paged_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
                                         int32_t head_dim, int64_t max_total_tokens) {
   (void)max_total_tokens;

@@ -66,6 +66,9 @@ hipError_t launch_qkv_rope_kv(int dtype, int M, int head_dim, int n_q_heads, int
 // u[m][n] = silu(g) * up with g, up the summed partials of columns n and F+n.
 hipError_t launch_swiglu(int dtype, int M, int F, const float* part, int splits, void* u,
                          hipStream_t stream);
+// out[i] = sum_s part[s][i] over `splits` slabs of n floats (n % 4 == 0).
+hipError_t launch_sum_splits(int64_t n, const float* part, int splits, float* out,
+                             hipStream_t stream);
 // tokens[b] = argmax_v logits[b][v] (lowest index on ties).
 hipError_t launch_argmax(int B, int V, const float* logits, int32_t* tokens, hipStream_t stream);
 // bt[d.slot * stride + d.idx] = d.page for each delta.

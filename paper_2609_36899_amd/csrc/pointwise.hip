@@ -163,6 +163,20 @@ __global__ __launch_bounds__(256) void swiglu_kernel(int M, int F, const float* 
   }
 }
 
+// out[i] = sum_s part[s][i] in split order (float4; n % 4 == 0).
+__global__ __launch_bounds__(256) void sum_splits_kernel(int64_t n4, const float* __restrict__ part,
+                                                         int splits, float* __restrict__ out) {
+  for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n4;
+       q += (int64_t)gridDim.x * blockDim.x) {
+    float4 v = *(const float4*)(part + q * 4);
+    for (int s = 1; s < splits; ++s) {
+      const float4 p = *(const float4*)(part + (int64_t)s * n4 * 4 + q * 4);
+      v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+    }
+    *(float4*)(out + q * 4) = v;
+  }
+}
+
 __device__ __forceinline__ void argmax_merge(float& v, int& i, float v2, int i2) {
   if (v2 > v || (v2 == v && i2 < i)) {
     v = v2;
@@ -281,6 +295,13 @@ hipError_t launch_swiglu(int dtype, int M, int F, const float* part, int splits,
                                                                    (uint16_t*)u);
   else
     swiglu_kernel<float><<<grid_for(n, 256), 256, 0, stream>>>(M, F, part, splits, (float*)u);
+  return hipGetLastError();
+}
+
+hipError_t launch_sum_splits(int64_t n, const float* part, int splits, float* out,
+                             hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  sum_splits_kernel<<<grid_for(n / 4, 256), 256, 0, stream>>>(n / 4, part, splits, out);
   return hipGetLastError();
 }
 

@@ -227,6 +227,32 @@ class Engine:
                                 int(mode)))
 
 
+def weight_projection_workspace_bytes(dtype: int, rows: int, cols: int, k: int) -> int:
+    """Scratch bytes weight_projection needs for split-K partials (0 if none)."""
+    return N.check(N.load().weight_projection_workspace_bytes(dtype, rows, cols, k))
+
+
+def weight_projection(x: torch.Tensor, w: torch.Tensor, out: torch.Tensor,
+                      workspace: Optional[torch.Tensor] = None,
+                      stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """out = x W^T through the library's projection kernels; see include/pdec.h."""
+    rows, k = x.shape
+    cols, k2 = w.shape
+    assert k == k2 and x.dtype == w.dtype and x.is_contiguous() and w.is_contiguous()
+    assert out.dtype == torch.float32 and tuple(out.shape) == (rows, cols)
+    assert out.is_contiguous()
+    assert x.dtype in (torch.bfloat16, torch.float32)
+    dtype = N.BF16 if x.dtype == torch.bfloat16 else N.F32
+    lib = N.load()
+    need = N.check(lib.weight_projection_workspace_bytes(dtype, rows, cols, k))
+    if need and (workspace is None or workspace.numel() < need):
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    N.check(lib.weight_projection(dtype, rows, cols, k, x.data_ptr(), w.data_ptr(),
+                                  out.data_ptr(), workspace.data_ptr() if need else None,
+                                  workspace.numel() if need else 0, _stream_handle(stream)))
+    return out
+
+
 def paged_attention_workspace_bytes(batch: int, n_q_heads: int, n_kv_heads: int,
                                     head_dim: int) -> int:
     return N.check(N.load().paged_attention_workspace_bytes(batch, n_q_heads, n_kv_heads,
