@@ -74,20 +74,26 @@ def gpu_weights(shape, seed=0, std=0.02):
     g = torch.Generator(device="cuda")
     g.manual_seed(seed)
 
+    import paper_2609_36899_amd as P
+
     def mat(rows, cols):
         w = torch.empty((rows, cols), dtype=torch.bfloat16, device="cuda")
         w.normal_(0.0, std, generator=g)
         return w
 
+    def proj(rows, cols):  # projections are stored packed
+        return P.pack_weight(mat(rows, cols))
+
     ones = lambda: torch.ones(shape.d_model, dtype=torch.float32, device="cuda")
     out = {"embed": mat(shape.vocab, shape.d_model), "layers": []}
     for _ in range(shape.n_layers):
         out["layers"].append({
-            "wq": mat(shape.q_dim, shape.d_model), "wk": mat(shape.kv_dim, shape.d_model),
-            "wv": mat(shape.kv_dim, shape.d_model), "wo": mat(shape.d_model, shape.q_dim),
-            "w_gate": mat(shape.ffn_dim, shape.d_model), "w_up": mat(shape.ffn_dim, shape.d_model),
-            "w_down": mat(shape.d_model, shape.ffn_dim), "attn_norm": ones(), "ffn_norm": ones()})
-    out["lm_head"] = mat(shape.vocab, shape.d_model)
+            "wq": proj(shape.q_dim, shape.d_model), "wk": proj(shape.kv_dim, shape.d_model),
+            "wv": proj(shape.kv_dim, shape.d_model), "wo": proj(shape.d_model, shape.q_dim),
+            "w_gate": proj(shape.ffn_dim, shape.d_model),
+            "w_up": proj(shape.ffn_dim, shape.d_model),
+            "w_down": proj(shape.d_model, shape.ffn_dim), "attn_norm": ones(), "ffn_norm": ones()})
+    out["lm_head"] = proj(shape.vocab, shape.d_model)
     out["final_norm"] = ones()
     return out
 
@@ -415,7 +421,8 @@ def run_projections(batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), iters=20):
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     rows = []
     for name, n, k in PROJ_SHAPES:
-        w = torch.empty((n, k), dtype=torch.bfloat16, device="cuda").normal_(0, 0.02, generator=g)
+        w = P.pack_weight(torch.empty((n, k), dtype=torch.bfloat16,
+                                      device="cuda").normal_(0, 0.02, generator=g))
         for m in batches:
             x = torch.empty((m, k), dtype=torch.bfloat16, device="cuda").normal_(generator=g)
             out = torch.empty((m, n), dtype=torch.float32, device="cuda")

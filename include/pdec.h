@@ -71,8 +71,12 @@ typedef struct pdec_model_cfg {
   int32_t dtype;     /* PDEC_F32 or PDEC_BF16 */
 } pdec_model_cfg;
 
-/* Device pointers to the weights, all row-major in the nn.Linear [out][in]
- * layout and stored in cfg->dtype, except the norm gains (always fp32).
+/* Device pointers to the weights, stored in cfg->dtype except the norm gains
+ * (always fp32).  The embedding table is row-major [vocab][d_model].  The
+ * projection matrices (wq ... w_down, lm_head), listed below in their
+ * nn.Linear [out][in] shape, are passed as produced by pack_weight: for bf16
+ * that is the strip layout the weight-streaming kernels read, for fp32 the
+ * row-major matrix itself.
  * The per-layer members are HOST arrays of n_layers DEVICE pointers; the
  * arrays are copied by engine_create and may be freed afterwards. */
 typedef struct pdec_weights {
@@ -256,12 +260,31 @@ int sample(pdec_engine* engine, int32_t batch, const float* logits_dev, int32_t*
  * Slots past lens[b] in the last page are never read.
  * ------------------------------------------------------------------------- */
 /* ---------------------------------------------------------------------------
+ * Weight packing.  Each decode step streams every projection matrix from HBM
+ * once for the whole batch (Introduction; Design Principles, "Specialization
+ * in Heterogeneous Pools"), so bf16 matrices are stored in a layout whose
+ * stream is long contiguous runs: strip j holds columns 16j .. 16j+15 (the
+ * last strip zero-padded) for all K, as K/32 blocks of 16 x 32 elements, each
+ * block 1 KiB in the lane order of the MFMA B operand; element (n, k) is at
+ *   ((j * K/32 + b) * 64 + q * 16 + c) * 8 + e,  n = 16j + c, k = 32b + 8q + e.
+ * fp32 matrices keep the row-major layout (pack_weight copies them).
+ *   packed_weight_bytes: size of the packed form of an [N][K] matrix
+ *     (bf16: ceil(N/16)*16*K*2 bytes, fp32: N*K*4), or a negative status.
+ *   pack_weight: w is a device row-major [N][K] matrix in dtype; packed is a
+ *     caller-owned device buffer of packed_weight_bytes(...) bytes, not
+ *     overlapping w.  Asynchronous on stream.
+ * Errors: PDEC_UNSUPPORTED (bf16 with K % 64 != 0), PDEC_INVALID_ARG.
+ * ------------------------------------------------------------------------- */
+int64_t packed_weight_bytes(int32_t dtype, int32_t N, int32_t K);
+
+int pack_weight(int32_t dtype, int32_t N, int32_t K, const void* w, void* packed, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Isolated weight projection: out = x W^T with the engine's own plan and
- * kernels (GEMV for tiny batches, MFMA GEMMs otherwise, split-K summed in a
- * fixed order).  Each decode step reads the weights once for the whole batch
- * (Introduction; Design Principles, "Specialization in Heterogeneous Pools").
- *   x: device [M][K] in dtype; w: device [N][K] in dtype (nn.Linear layout);
- *   out: device fp32 [M][N]; workspace: device, at least
+ * kernels (the weight-streaming MFMA kernel up to 32 rows, MFMA tiles beyond,
+ * split-K summed in a fixed order).
+ *   x: device [M][K] in dtype; w: the [N][K] weight as produced by
+ *   pack_weight; out: device fp32 [M][N]; workspace: device, at least
  *   weight_projection_workspace_bytes(...) bytes (may be 0).
  * Errors: PDEC_UNSUPPORTED (bf16 with K % 64 != 0, N % 4 != 0),
  * PDEC_INVALID_ARG.

@@ -787,6 +787,24 @@ int sample(pdec_engine* E, int32_t B, const float* logits_dev, int32_t* tokens_d
   return PDEC_OK;
 }
 
+int64_t packed_weight_bytes(int32_t dtype, int32_t N, int32_t K) {
+  if ((dtype != PDEC_F32 && dtype != PDEC_BF16) || N < 1 || K < 1)
+    return fail(PDEC_INVALID_ARG, "bad weight shape");
+  if (dtype == PDEC_BF16) {
+    if (K % 64) return fail(PDEC_UNSUPPORTED, "bf16 weights need K % 64 == 0");
+    return (int64_t)((N + 15) / 16) * 16 * K * 2;
+  }
+  return (int64_t)N * K * 4;
+}
+
+int pack_weight(int32_t dtype, int32_t N, int32_t K, const void* w, void* packed, void* stream) {
+  const int64_t bytes = packed_weight_bytes(dtype, N, K);
+  if (bytes < 0) return (int)bytes;
+  if (!w || !packed) return fail(PDEC_INVALID_ARG, "null argument");
+  HIP_OR_FAIL(launch_pack_weight(dtype, N, K, w, packed, (hipStream_t)stream));
+  return PDEC_OK;
+}
+
 int64_t weight_projection_workspace_bytes(int32_t dtype, int32_t M, int32_t N, int32_t K) {
   if ((dtype != PDEC_F32 && dtype != PDEC_BF16) || M < 1 || N < 1 || K < 1)
     return fail(PDEC_INVALID_ARG, "bad projection arguments");

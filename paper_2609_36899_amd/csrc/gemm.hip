@@ -1,15 +1,22 @@
 // Weight-streaming projections: out[s][m][n] = sum_{k in split s} A[m][k] W[n][k].
 //
 // Each decode step reads the weights once for the whole active batch (paper:
-// Introduction; Design Principles, "Specialization in Heterogeneous Pools").
-// A work group owns a 64-column slice of W and every row of the batch, so W
-// is streamed from HBM exactly once per step; the activations (at most a few
-// MB) stay in L2.  When the column slices alone cannot fill 256 CUs the K
-// axis is split and the fp32 partial sums are reduced by the next kernel.
+// Introduction; Design Principles, "Specialization in Heterogeneous Pools"),
+// so at decode batch sizes the weight stream from HBM is the bound.  bf16
+// weights are stored packed so that this stream is long contiguous runs:
 //
-// bf16: v_mfma_f32_16x16x32_bf16 tiles of 16 rows x 16 columns.  The
-// weight stream is the bound at small batch, so weight tiles are prefetched
-// several k-steps ahead to keep enough bytes in flight per CU.
+//   strip j = columns 16j .. 16j+15 (the last strip zero-padded), holding
+//   K/32 blocks of 16 columns x 32 k, each block 1 KiB in the lane order of
+//   the v_mfma_f32_16x16x32_bf16 B operand: element (n, k) of W sits at
+//       ((j * K/32 + b) * 64 + q * 16 + c) * 8 + e,
+//   n = 16j + c, k = 32b + 8q + e.
+//
+// One 16-byte load per lane at lane * 8 is then exactly one MFMA fragment,
+// and a strip's K range is a single contiguous run.  Row-wise [N][K] weights
+// give 128-byte runs in many rows at once and stream 10-25% slower.
+//
+// When the column tiles alone cannot fill 256 CUs the K axis is split and the
+// fp32 partial sums are reduced in a fixed order by the next kernel.
 #include "hip_common.h"
 #include "kernels.h"
 
@@ -17,103 +24,131 @@ namespace pdec {
 
 namespace {
 
-__device__ __forceinline__ const void* seg_row(const WSegs& w, int n, int64_t row_elems,
-                                               int elem_bytes) {
+// Base of strip j (16 columns, all K) of a weight given as up to three
+// packed segments; every segment but the last holds a multiple of 16 columns.
+__device__ __forceinline__ const uint16_t* strip_base(const WSegs& w, int j, int K) {
   int start = 0;
   for (int s = 0; s < w.n_seg; ++s) {
-    if (n < w.row_end[s])
-      return (const char*)w.ptr[s] + (int64_t)(n - start) * row_elems * elem_bytes;
+    if (16 * j < w.row_end[s] || s == w.n_seg - 1)
+      return (const uint16_t*)w.ptr[s] + (int64_t)(j - start / 16) * K * 16;
     start = w.row_end[s];
   }
-  return w.ptr[0];
+  return (const uint16_t*)w.ptr[0];
 }
 
-// Small batches (M <= 4 with long K in practice, up to 64 supported).  Each
-// wave owns 16 columns of the 64-column
-// block and every row of the batch, so no two waves share weight bytes.  The
-// weight fragments are prefetched NS k-steps ahead through a register ring so
-// that enough HBM bytes are in flight to hide the memory latency; the
-// activations (L2-resident) are prefetched one step ahead.
-template <int MT, int NS>
-__global__ __launch_bounds__(256, 2) void gemm_bf16_small_m(int M, int N, int K, int k_split,
-                                                            const uint16_t* __restrict__ A,
-                                                            int64_t lda, WSegs w,
-                                                            float* __restrict__ out) {
-  static_assert(NS % 2 == 0, "ring depth must be even");
+__global__ __launch_bounds__(256) void pack_weight_kernel(const uint16_t* __restrict__ W, int N,
+                                                          int K, uint16_t* __restrict__ P) {
+  const int KB = K / 32;
+  const int64_t chunk = (int64_t)blockIdx.x * 256 + threadIdx.x;  // one 8-element chunk
+  if (chunk >= (int64_t)((N + 15) / 16) * KB * 64) return;
+  const int l = (int)(chunk & 63);
+  const int64_t jb = chunk >> 6;
+  const int b = (int)(jb % KB), j = (int)(jb / KB);
+  const int n = 16 * j + (l & 15), k = 32 * b + 8 * (l >> 4);
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (n < N) v = *(const u32x4*)(W + (int64_t)n * K + k);
+  *(u32x4*)(P + chunk * 8) = v;
+}
+
+// Small batches (M <= 32): each wave owns WS strips and every row of the
+// batch (MT tiles of 16 rows), so no two waves share weight bytes and no LDS
+// or barrier is needed.  The weight fragments and the matching activation
+// fragments (L2-resident) of the next NS k-steps are in flight in a register
+// ring.  The steady-state loop is branch-free (the prefetch index is clamped
+// to the last step) and pinned to consume-then-refill order per slot, so the
+// compiler keeps all NS slots in flight instead of draining the ring.
+template <int MT, int WS, int NS>
+__global__ __launch_bounds__(256) void gemm_bf16_stream(int M, int N, int K, int k_split,
+                                                        const uint16_t* __restrict__ A,
+                                                        int64_t lda, WSegs w,
+                                                        float* __restrict__ out) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int c16 = lane & 15, q4 = lane >> 4;
-  const int n0 = blockIdx.x * 64 + wave * 16;
+  const int n_strips = (N + 15) / 16;
+  const int j0 = (blockIdx.x * 4 + wave) * WS;
   const int kbeg = blockIdx.z * k_split;
   const int n_iter = (min(K, kbeg + k_split) - kbeg) / 64;
-  if (n0 >= N || n_iter <= 0) return;  // no barriers in this kernel
+  if (j0 >= n_strips || n_iter <= 0) return;  // no barriers in this kernel
 
-  const uint16_t* wrow = (const uint16_t*)seg_row(w, min(n0 + c16, N - 1), K, 2) + kbeg + q4 * 8;
-  const uint16_t* arow[MT];
+  const uint16_t* wp[WS];
+#pragma unroll
+  for (int s = 0; s < WS; ++s)
+    wp[s] = strip_base(w, min(j0 + s, n_strips - 1), K) + (int64_t)kbeg * 16 + lane * 8;
+  const uint16_t* ap[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t)
-    arow[t] = A + (int64_t)min(t * 16 + c16, M - 1) * lda + kbeg + q4 * 8;
+    ap[t] = A + (int64_t)min(t * 16 + c16, M - 1) * lda + kbeg + q4 * 8;
 
-  f32x4 acc[MT];
+  f32x4 acc[MT][WS];
 #pragma unroll
-  for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  bf16x8 wr[NS][2];
-  bf16x8 ar[2][MT][2];
+  for (int t = 0; t < MT; ++t)
 #pragma unroll
-  for (int s = 0; s < NS; ++s)
-    if (s < n_iter) {
-      wr[s][0] = load_stream<bf16x8>(wrow + s * 64);
-      wr[s][1] = load_stream<bf16x8>(wrow + s * 64 + 32);
+    for (int s = 0; s < WS; ++s) acc[t][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 rw[NS][WS][2], ra[NS][MT][2];
+  auto load = [&](int i, bf16x8(&wr)[WS][2], bf16x8(&ar)[MT][2]) {
+#pragma unroll
+    for (int s = 0; s < WS; ++s) {
+      wr[s][0] = load_stream<bf16x8>(wp[s] + i * 1024);
+      wr[s][1] = load_stream<bf16x8>(wp[s] + i * 1024 + 512);
     }
 #pragma unroll
-  for (int t = 0; t < MT; ++t) {
-    ar[0][t][0] = *(const bf16x8*)(arow[t]);
-    ar[0][t][1] = *(const bf16x8*)(arow[t] + 32);
-  }
-  for (int it0 = 0; it0 < n_iter; it0 += NS) {
+    for (int t = 0; t < MT; ++t) {
+      ar[t][0] = *(const bf16x8*)(ap[t] + i * 64);
+      ar[t][1] = *(const bf16x8*)(ap[t] + i * 64 + 32);
+    }
+  };
+  auto mma = [&](const bf16x8(&wr)[WS][2], const bf16x8(&ar)[MT][2]) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int s = 0; s < WS; ++s)
+          acc[t][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ar[t][h], wr[s][h], acc[t][s], 0, 0, 0);
+  };
+  const int last = n_iter - 1;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) load(min(s, last), rw[s], ra[s]);
+  int it0 = 0;
+  for (; it0 + NS <= n_iter; it0 += NS) {
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      const int it = it0 + s;
-      if (it >= n_iter) break;
-      const bf16x8 b0 = wr[s][0], b1 = wr[s][1];
-      if (it + NS < n_iter) {
-        wr[s][0] = load_stream<bf16x8>(wrow + (it + NS) * 64);
-        wr[s][1] = load_stream<bf16x8>(wrow + (it + NS) * 64 + 32);
-      }
-      if (it + 1 < n_iter) {
-#pragma unroll
-        for (int t = 0; t < MT; ++t) {
-          ar[(s + 1) & 1][t][0] = *(const bf16x8*)(arow[t] + (it + 1) * 64);
-          ar[(s + 1) & 1][t][1] = *(const bf16x8*)(arow[t] + (it + 1) * 64 + 32);
-        }
-      }
-#pragma unroll
-      for (int t = 0; t < MT; ++t) {
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ar[s & 1][t][0], b0, acc[t], 0, 0, 0);
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ar[s & 1][t][1], b1, acc[t], 0, 0, 0);
-      }
+      mma(rw[s], ra[s]);
+      load(min(it0 + s + NS, last), rw[s], ra[s]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
+  const int rem = n_iter - it0;
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    if (s < rem) mma(rw[s], ra[s]);
 
   float* o = out + (int64_t)blockIdx.z * M * N;
-  const int col = n0 + c16;
 #pragma unroll
   for (int t = 0; t < MT; ++t)
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int row = t * 16 + 4 * q4 + rr;
-      if (row < M && col < N) o[(int64_t)row * N + col] = acc[t][rr];
+    for (int s = 0; s < WS; ++s) {
+      const int col = (j0 + s) * 16 + c16;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int row = t * 16 + 4 * q4 + rr;
+        if (row < M && col < N) o[(int64_t)row * N + col] = acc[t][s][rr];
+      }
     }
 }
 
-// Larger batches (M > 4): (64 WM) x 128 output tiles, 2 WM waves in a WM x 2
+// Larger batches (M > 32): (64 WM) x 128 output tiles, 2 WM waves in a WM x 2
 // grid of 64 x 64 sub-tiles.  Per k-step of 64 the A tile and the W tile are
-// staged once through LDS (double-buffered, 16-byte chunks XOR-swizzled by
-// row) and each is shared by the waves that need it; the tiles of the next
-// NS k-steps are prefetched into a register ring meanwhile (NS even: ring
-// slot s also names the LDS buffer s & 1).  WM = 4 covers 256 rows, so up to
-// that batch size W is read from HBM exactly once per step.  Larger batches
-// take several M-blocks, laid out so the M-blocks of one column tile are
-// dispatched back to back (ids L and L+8 share an XCD).
+// staged once through LDS (double-buffered) and each is shared by the waves
+// that need it; the tiles of the next NS k-steps are prefetched into a
+// register ring meanwhile (NS even: ring slot s also names the LDS buffer
+// s & 1).  The W tile is 8 strips x 2 blocks, copied in packed order (eight
+// 2 KiB runs from HBM; fragment reads from LDS are linear, hence free of bank
+// conflicts); the A tile is row-major with 16-byte chunks XOR-swizzled by
+// row.  WM = 4 covers 256 rows, so up to that batch size W is read from HBM
+// exactly once per step.  Larger batches take several M-blocks, laid out so
+// the M-blocks of one column tile are dispatched back to back (ids L and L+8
+// share an XCD).
 template <int WM, int NS, int NA>
 __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, int k_split,
                                                           int n_mb, int n_nb,
@@ -122,9 +157,9 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
                                                           float* __restrict__ out) {
   constexpr int MT = 4, NT = 4;
   constexpr int THREADS = 128 * WM, ROWS = 64 * WM;
-  constexpr int RSTEP = THREADS / 8;  // rows covered by one chunk column of the group
+  constexpr int RSTEP = THREADS / 8;  // A rows covered by one chunk column of the group
   constexpr int ACH = ROWS / RSTEP;   // A chunks per thread (4)
-  constexpr int WCH = 128 / RSTEP;    // W chunks per thread
+  constexpr int WCH = 1024 / THREADS; // W chunks per thread (16 KiB tile)
   __shared__ __attribute__((aligned(16))) uint16_t la_s[2][ROWS * 64];
   __shared__ __attribute__((aligned(16))) uint16_t lw_s[2][128 * 64];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -138,6 +173,7 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
   if (n_iter <= 0) return;
   const int m_blk = mb * ROWS, n_blk = nb * 128;
   const int wm = wave >> 1, wn = wave & 1;
+  const int n_strips = (N + 15) / 16;
 
   const int r = tid >> 3, c = tid & 7;
   const int dst = r * 64 + ((c ^ (r & 7)) * 8);  // + j * RSTEP * 64 for chunk j
@@ -147,16 +183,18 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
   for (int j = 0; j < ACH; ++j)
     asrc[j] = A + (int64_t)min(m_blk + r + RSTEP * j, M - 1) * lda + kbeg + c * 8;
 #pragma unroll
-  for (int j = 0; j < WCH; ++j)
-    wsrc[j] = (const uint16_t*)seg_row(w, min(n_blk + r + RSTEP * j, N - 1), K, 2) + kbeg + c * 8;
-  int aoff[MT][2], boff[NT][2];
+  for (int j = 0; j < WCH; ++j) {
+    const int id = tid + j * THREADS;  // chunk id in the tile: strip id >> 7
+    wsrc[j] = strip_base(w, min(nb * 8 + (id >> 7), n_strips - 1), K) + (int64_t)kbeg * 16 +
+              (id & 127) * 8;
+  }
+  int aoff[MT][2];
 #pragma unroll
   for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const int ra = wm * 64 + t * 16 + c16, rb = wn * 64 + t * 16 + c16, cc = h * 4 + q4;
+      const int ra = wm * 64 + t * 16 + c16, cc = h * 4 + q4;
       aoff[t][h] = ra * 64 + ((cc ^ (ra & 7)) * 8);
-      boff[t][h] = rb * 64 + ((cc ^ (rb & 7)) * 8);
     }
 
   f32x4 acc[MT][NT];
@@ -172,7 +210,7 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
   for (int s = 0; s < NS; ++s)
     if (s < n_iter) {
 #pragma unroll
-      for (int j = 0; j < WCH; ++j) rw_[s][j] = *(const u16x8*)(wsrc[j] + s * 64);
+      for (int j = 0; j < WCH; ++j) rw_[s][j] = *(const u16x8*)(wsrc[j] + s * 1024);
       if (s < NA) {
 #pragma unroll
         for (int j = 0; j < ACH; ++j) ra_[s][j] = *(const u16x8*)(asrc[j] + s * 64);
@@ -188,11 +226,11 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
 #pragma unroll
       for (int j = 0; j < ACH; ++j) *(u16x8*)(la + dst + j * RSTEP * 64) = ra_[s % NA][j];
 #pragma unroll
-      for (int j = 0; j < WCH; ++j) *(u16x8*)(lw + dst + j * RSTEP * 64) = rw_[s][j];
+      for (int j = 0; j < WCH; ++j) *(u16x8*)(lw + (tid + j * THREADS) * 8) = rw_[s][j];
       __syncthreads();
       if (it + NS < n_iter) {
 #pragma unroll
-        for (int j = 0; j < WCH; ++j) rw_[s][j] = *(const u16x8*)(wsrc[j] + (it + NS) * 64);
+        for (int j = 0; j < WCH; ++j) rw_[s][j] = *(const u16x8*)(wsrc[j] + (it + NS) * 1024);
       }
       if (it + NA < n_iter) {
 #pragma unroll
@@ -204,7 +242,8 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
 #pragma unroll
         for (int t = 0; t < MT; ++t) af[t] = *(const bf16x8*)(la + aoff[t][h]);
 #pragma unroll
-        for (int t = 0; t < NT; ++t) bf[t] = *(const bf16x8*)(lw + boff[t][h]);
+        for (int t = 0; t < NT; ++t)
+          bf[t] = *(const bf16x8*)(lw + (((wn * 4 + t) * 2 + h) * 64 + lane) * 8);
 #pragma unroll
         for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -228,67 +267,16 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
     }
 }
 
-// VALU weight-streaming GEMV for tiny batches (M <= 4): out[m][n] =
-// sum_k x[m][k] W[n][k] with v_dot2_f32_bf16.  Each wave streams whole
-// contiguous weight rows (a row of K bf16 is K*2 contiguous bytes, read 1 KiB
-// per instruction), so the weight stream is long sequential runs; the batch's
-// activations sit in LDS.  Every wave covers the full K of its rows: no
-// split-K, results go straight to out (splits = 1).
-// Whole vectors are reinterpreted and split by shuffles (bit-casting a
-// single vector element would read the vector's first element).
-__device__ __forceinline__ float dot8(const u32x4 w, const u32x4 x, float acc) {
-  const bf16x8 wb = __builtin_bit_cast(bf16x8, w), xb = __builtin_bit_cast(bf16x8, x);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(wb, wb, 0, 1),
-                                        __builtin_shufflevector(xb, xb, 0, 1), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(wb, wb, 2, 3),
-                                        __builtin_shufflevector(xb, xb, 2, 3), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(wb, wb, 4, 5),
-                                        __builtin_shufflevector(xb, xb, 4, 5), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(wb, wb, 6, 7),
-                                        __builtin_shufflevector(xb, xb, 6, 7), acc, false);
-  return acc;
-}
-
-template <int M>
-__global__ __launch_bounds__(256) void gemv_bf16(int N, int K, int rows_per_wave,
-                                                 const uint16_t* __restrict__ x, int64_t ldx,
-                                                 WSegs w, float* __restrict__ out) {
-  extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [M][K]
-  for (int i = threadIdx.x * 8; i < M * K; i += 256 * 8) {
-    const int m = i / K, k = i % K;
-    *(u32x4*)(xs + i) = *(const u32x4*)(x + (int64_t)m * ldx + k);
+// fp32 weights are row-major [N][K] (the packed layout is for bf16 only).
+__device__ __forceinline__ const void* seg_row(const WSegs& w, int n, int64_t row_elems,
+                                               int elem_bytes) {
+  int start = 0;
+  for (int s = 0; s < w.n_seg; ++s) {
+    if (n < w.row_end[s])
+      return (const char*)w.ptr[s] + (int64_t)(n - start) * row_elems * elem_bytes;
+    start = w.row_end[s];
   }
-  __syncthreads();
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int n0 = (blockIdx.x * 4 + wave) * rows_per_wave;
-  const int n1 = min(N, n0 + rows_per_wave);
-  for (int n = n0; n < n1; ++n) {
-    const uint16_t* wr = (const uint16_t*)seg_row(w, n, K, 2);
-    float acc[M];
-#pragma unroll
-    for (int m = 0; m < M; ++m) acc[m] = 0.f;
-    int k = lane * 8;
-    for (; k + 3 * 512 < K; k += 4 * 512) {
-      u32x4 wv[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) wv[u] = load_stream<u32x4>(wr + k + u * 512);
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int m = 0; m < M; ++m)
-          acc[m] = dot8(wv[u], *(const u32x4*)(xs + m * K + k + u * 512), acc[m]);
-    }
-    for (; k < K; k += 512) {
-      const u32x4 wv = load_stream<u32x4>(wr + k);
-#pragma unroll
-      for (int m = 0; m < M; ++m) acc[m] = dot8(wv, *(const u32x4*)(xs + m * K + k), acc[m]);
-    }
-#pragma unroll
-    for (int m = 0; m < M; ++m) {
-      const float v = wave_sum(acc[m]);
-      if (lane == m) out[(int64_t)m * N + n] = v;
-    }
-  }
+  return w.ptr[0];
 }
 
 // fp32: 32 x 64 tiles through LDS, 2 x 4 outputs per thread.
@@ -336,20 +324,10 @@ __global__ __launch_bounds__(256) void gemm_f32_tiled(int M, int N, int K, int k
 }  // namespace
 
 // Kernel choice for bf16, from measurements on the 8B projection shapes:
-//  * GEMV (VALU dot2, whole-row streaming) while the batch's activations fit
-//    in 64 KB of LDS and M <= 4: 6.2-6.6 TB/s at M = 1, ahead of MFMA up to
-//    M = 4;
-//  * the register-ring MFMA kernel for the remaining M <= 4 (long K);
-//  * the 128 x 128 tile MFMA kernel above that.
-enum class GemmPath { kGemv, kSmallM, kTile128 };
-
-GemmPath bf16_path(int M, int K) {
-  if (M <= 4 && (int64_t)M * K * 2 <= 64 * 1024) return GemmPath::kGemv;
-  if (M <= 4) return GemmPath::kSmallM;
-  return GemmPath::kTile128;
-}
-
-constexpr int kGemvWaves = 2048;
+//  * M <= 32: the streaming kernel (two strips per wave, ring depth 2);
+//    6.0-6.6 TB/s of weights up to M = 16;
+//  * larger M: the 128 x 128 tile (M <= 128) or 256 x 128 tile.
+constexpr int kStreamMaxRows = 32;
 
 // Rows per tile: 128 (4 waves) up to 128-row batches, 256 (8 waves) beyond,
 // so W is read once per step for batches up to 256.
@@ -357,25 +335,38 @@ int tile_rows(int M) { return M <= 128 ? 128 : 256; }
 
 int gemm_plan_splits(int dtype, int M, int N, int K, int* k_split) {
   const int kq = (dtype == 1) ? 64 : 16;
-  if (dtype == 1 && bf16_path(M, K) == GemmPath::kGemv) {
-    *k_split = K;
-    return 1;
+  const bool stream = dtype == 1 && M <= kStreamMaxRows;
+  const bool tile = dtype == 1 && !stream;
+  int64_t groups;
+  if (stream) {
+    groups = ((N + 15) / 16 + 7) / 8;  // 4 waves x 2 strips
+  } else {
+    const int mblk = tile ? tile_rows(M) : 32, nblk = tile ? 128 : 64;
+    groups = (int64_t)((N + nblk - 1) / nblk) * ((M + mblk - 1) / mblk);
   }
-  const bool tile = dtype == 1 && bf16_path(M, K) == GemmPath::kTile128;
-  const int mblk = (dtype == 1) ? (tile ? tile_rows(M) : 64) : 32;
-  const int nblk = tile ? 128 : 64;
-  const int64_t tiles = (int64_t)((N + nblk - 1) / nblk) * ((M + mblk - 1) / mblk);
-  // Small batches: aim for two work groups per CU; the partial sums are
-  // small.  Larger batches: about one per CU, since every extra split writes
-  // and re-reads an M x N fp32 slab; the 256-row tile holds a whole CU.
-  const int64_t target = !tile || M <= 64 ? 512 : (M <= 128 ? 256 : 224);
+  // Streaming: about one work group per CU (measured best on all five
+  // shapes).  Tiles at small M: two per CU; at larger M about one, since
+  // every extra split writes and re-reads an M x N fp32 slab; the 256-row
+  // tile holds a whole CU.
+  const int64_t target = stream ? 256 : (!tile || M <= 64 ? 512 : (M <= 128 ? 256 : 224));
   const int ksteps = (K + kq - 1) / kq;
   int s = 1;
-  if (tiles < target) s = (int)std::min<int64_t>((target + tiles - 1) / tiles, 8);
+  if (groups < target) s = (int)std::min<int64_t>((target + groups - 1) / groups, 8);
   s = std::max(1, std::min(s, ksteps));
   const int steps_per = (ksteps + s - 1) / s;
   *k_split = steps_per * kq;
   return (K + *k_split - 1) / *k_split;
+}
+
+hipError_t launch_pack_weight(int dtype, int N, int K, const void* w, void* packed,
+                              hipStream_t stream) {
+  if (N <= 0 || K <= 0) return hipSuccess;
+  if (dtype != 1)
+    return hipMemcpyAsync(packed, w, (size_t)N * K * 4, hipMemcpyDeviceToDevice, stream);
+  const int64_t chunks = (int64_t)((N + 15) / 16) * (K / 32) * 64;
+  pack_weight_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, stream>>>(
+      (const uint16_t*)w, N, K, (uint16_t*)packed);
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t lda,
@@ -384,25 +375,12 @@ hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t ld
   const dim3 block(256);
   if (dtype == 1) {
     const uint16_t* a = (const uint16_t*)A;
-    const GemmPath path = bf16_path(M, K);
-    if (path == GemmPath::kGemv) {
-      const int rpw = (N + kGemvWaves - 1) / kGemvWaves;
-      const dim3 grid((N + 4 * rpw - 1) / (4 * rpw));
-      const size_t lds = (size_t)M * K * 2;
-      switch (M) {
-        case 1: gemv_bf16<1><<<grid, block, lds, stream>>>(N, K, rpw, a, lda, w, out); break;
-        case 2: gemv_bf16<2><<<grid, block, lds, stream>>>(N, K, rpw, a, lda, w, out); break;
-        case 3: gemv_bf16<3><<<grid, block, lds, stream>>>(N, K, rpw, a, lda, w, out); break;
-        default: gemv_bf16<4><<<grid, block, lds, stream>>>(N, K, rpw, a, lda, w, out); break;
-      }
-    } else if (path == GemmPath::kSmallM) {
-      const dim3 grid((N + 63) / 64, 1, splits);
-      switch ((M + 15) / 16) {
-        case 1: gemm_bf16_small_m<1, 8><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
-        case 2: gemm_bf16_small_m<2, 8><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
-        case 3: gemm_bf16_small_m<3, 8><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
-        default: gemm_bf16_small_m<4, 8><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out); break;
-      }
+    if (M <= kStreamMaxRows) {
+      const dim3 grid(((N + 15) / 16 + 7) / 8, 1, splits);
+      if (M <= 16)
+        gemm_bf16_stream<1, 2, 2><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out);
+      else
+        gemm_bf16_stream<2, 2, 2><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out);
     } else {
       const int rows = tile_rows(M);
       const int n_mb = (M + rows - 1) / rows, n_nb = (N + 127) / 128;

@@ -42,20 +42,51 @@ def kv_bytes_per_token(shape, dtype: int) -> int:
     return N.check(N.load().kv_bytes_per_token(byref(cfg)))
 
 
+class PackedWeight:
+    """A projection matrix [n][k] in the layout pack_weight produces."""
+
+    def __init__(self, data: torch.Tensor, n: int, k: int, dtype: int):
+        self.data, self.n, self.k, self.dtype = data, n, k, dtype
+
+    @property
+    def shape(self):
+        return (self.n, self.k)
+
+    def data_ptr(self) -> int:
+        return self.data.data_ptr()
+
+
+def pack_weight(w: torch.Tensor, stream: Optional[torch.cuda.Stream] = None) -> PackedWeight:
+    """Pack a device row-major [n][k] matrix (bf16 or fp32) with pack_weight."""
+    assert w.dim() == 2 and w.is_cuda and w.is_contiguous()
+    assert w.dtype in (torch.bfloat16, torch.float32)
+    dtype = N.BF16 if w.dtype == torch.bfloat16 else N.F32
+    n, k = w.shape
+    lib = N.load()
+    nbytes = N.check(lib.packed_weight_bytes(dtype, n, k))
+    data = torch.empty(nbytes // w.element_size(), dtype=w.dtype, device=w.device)
+    N.check(lib.pack_weight(dtype, n, k, w.data_ptr(), data.data_ptr(), _stream_handle(stream)))
+    return PackedWeight(data, n, k, dtype)
+
+
+PROJECTIONS = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
+
+
 def weights_to_device(arrays: Dict, dtype: int, device="cuda") -> Dict:
-    """Copy a weight dict (numpy, nn.Linear layout) to device tensors.
+    """Copy a weight dict (numpy, nn.Linear layout) to the device.
 
     Matrices go to the storage dtype (bf16 inputs must already be
-    bf16-representable, so the cast is exact); norm gains stay fp32.
+    bf16-representable, so the cast is exact) and the projections are packed
+    with pack_weight; norm gains stay fp32.
     """
     td = _TORCH_DTYPE[dtype]
     mat = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(
         device=device).to(td).contiguous()
     vec = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device)
-    out = {"embed": mat(arrays["embed"]), "lm_head": mat(arrays["lm_head"]),
+    out = {"embed": mat(arrays["embed"]), "lm_head": pack_weight(mat(arrays["lm_head"])),
            "final_norm": vec(arrays["final_norm"]), "layers": []}
     for lay in arrays["layers"]:
-        d = {k: mat(lay[k]) for k in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")}
+        d = {k: pack_weight(mat(lay[k])) for k in PROJECTIONS}
         d["attn_norm"] = vec(lay["attn_norm"])
         d["ffn_norm"] = vec(lay["ffn_norm"])
         out["layers"].append(d)
@@ -232,22 +263,21 @@ def weight_projection_workspace_bytes(dtype: int, rows: int, cols: int, k: int) 
     return N.check(N.load().weight_projection_workspace_bytes(dtype, rows, cols, k))
 
 
-def weight_projection(x: torch.Tensor, w: torch.Tensor, out: torch.Tensor,
+def weight_projection(x: torch.Tensor, w: PackedWeight, out: torch.Tensor,
                       workspace: Optional[torch.Tensor] = None,
                       stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """out = x W^T through the library's projection kernels; see include/pdec.h."""
     rows, k = x.shape
-    cols, k2 = w.shape
-    assert k == k2 and x.dtype == w.dtype and x.is_contiguous() and w.is_contiguous()
+    cols = w.n
+    assert isinstance(w, PackedWeight) and k == w.k and x.is_contiguous()
     assert out.dtype == torch.float32 and tuple(out.shape) == (rows, cols)
     assert out.is_contiguous()
-    assert x.dtype in (torch.bfloat16, torch.float32)
-    dtype = N.BF16 if x.dtype == torch.bfloat16 else N.F32
+    assert x.dtype == _TORCH_DTYPE[w.dtype]
     lib = N.load()
-    need = N.check(lib.weight_projection_workspace_bytes(dtype, rows, cols, k))
+    need = N.check(lib.weight_projection_workspace_bytes(w.dtype, rows, cols, k))
     if need and (workspace is None or workspace.numel() < need):
         workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
-    N.check(lib.weight_projection(dtype, rows, cols, k, x.data_ptr(), w.data_ptr(),
+    N.check(lib.weight_projection(w.dtype, rows, cols, k, x.data_ptr(), w.data_ptr(),
                                   out.data_ptr(), workspace.data_ptr() if need else None,
                                   workspace.numel() if need else 0, _stream_handle(stream)))
     return out

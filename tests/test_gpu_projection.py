@@ -1,10 +1,12 @@
 """Weight projections (out = x W^T) through the C ABI against a float64 matmul.
 
-Covers every kernel the planner picks: the VALU GEMV (M <= 4 with small
-activations), the register-ring MFMA kernel (M <= 4 with long K), the 128-row
-and 256-row MFMA tiles, split-K and ragged M, N.  Inputs are bf16-representable
-values, so the only difference from the float64 product is fp32 accumulation:
-per row, max|gpu - ref| <= 1e-4 * max|ref|.
+Covers every kernel the planner picks: the weight-streaming MFMA kernel (one
+and two 16-row tiles), the 128-row and 256-row MFMA tiles, split-K, ragged M
+and N (a zero-padded last strip of the packed weight).  Inputs are
+bf16-representable values, so the only difference from the float64 product
+is fp32 accumulation: per row, max|gpu - ref| <= 1e-4 * max|ref|.
+The packed layout itself is checked element by element against its
+definition.
 """
 
 import numpy as np
@@ -27,7 +29,7 @@ def _run(M, N, K, bf16=True, seed=0, rows=None):
         x, w = round_to_bf16(x), round_to_bf16(w)
     td = torch.bfloat16 if bf16 else torch.float32
     xd = torch.from_numpy(x).cuda().to(td).contiguous()
-    wd = torch.from_numpy(w).cuda().to(td).contiguous()
+    wd = P.pack_weight(torch.from_numpy(w).cuda().to(td).contiguous())
     out = torch.empty((M, N), dtype=torch.float32, device="cuda")
     P.weight_projection(xd, wd, out)
     got = out.cpu().numpy()
@@ -53,3 +55,26 @@ def test_bf16_8b_shapes_sampled_rows(M, N, K):
 @pytest.mark.parametrize("M", [1, 4, 33])
 def test_f32(M):
     _run(M, 688, 256, bf16=False, seed=M)
+
+
+@pytest.mark.parametrize("N,K", [(64, 64), (1412, 576), (40, 128)])
+def test_pack_layout(N, K):
+    """Element (n, k) sits at ((j*K/32 + b)*64 + q*16 + c)*8 + e with n = 16j + c,
+    k = 32b + 8q + e; the columns of the padded last strip are zero."""
+    import paper_2609_36899_amd as P
+    w = np.arange(N * K, dtype=np.int64).reshape(N, K) % 65521
+    wd = torch.from_numpy(w.astype(np.int16)).cuda().view(torch.bfloat16)
+    pw = P.pack_weight(wd.contiguous())
+    torch.cuda.synchronize()
+    got = pw.data.view(torch.int16).cpu().numpy().astype(np.int64) % 65536
+    n_strips = (N + 15) // 16
+    assert got.size == n_strips * 16 * K
+    expect = np.zeros(n_strips * 16 * K, dtype=np.int64)
+    for n in range(N):
+        j, c = divmod(n, 16)
+        for k in range(K):
+            b, r = divmod(k, 32)
+            q, e = divmod(r, 8)
+            expect[((j * (K // 32) + b) * 64 + q * 16 + c) * 8 + e] = w[n, k] % 65536
+    np.testing.assert_array_equal(got, expect)
+
