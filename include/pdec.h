@@ -138,14 +138,17 @@ void engine_destroy(pdec_engine* engine);
 /* Change the stream later calls enqueue on (hipStream_t). */
 int engine_set_stream(pdec_engine* engine, void* stream);
 
-/* Launch timing for measurement.  While enabled, every launch of the timed
- * classes below is bracketed by a pair of HIP events on the engine's stream;
- * engine_profile_read synchronises on them and returns the summed elapsed
- * time (ms) and the launch count of one class, clearing those records. */
+/* Launch timing for measurement.  engine_profile(engine, classes) takes a
+ * bitmask of the classes below ((1 << PDEC_TIMER_ATTENTION) | ...; 0 turns
+ * timing off).  Every launch of a selected class is bracketed by a pair of HIP
+ * events on the engine's stream (each pair adds a few microseconds to the
+ * step, so select only what is being measured); engine_profile_read
+ * synchronises on them and returns the summed elapsed time (ms) and the
+ * launch count of one class, clearing those records. */
 #define PDEC_TIMER_ATTENTION 0 /* paged split-K attention pass, one per layer */
 #define PDEC_TIMER_GEMM 1      /* the four weight projections of each layer */
 #define PDEC_TIMER_LM_HEAD 2   /* the LM-head projection */
-int engine_profile(pdec_engine* engine, int32_t enable);
+int engine_profile(pdec_engine* engine, int32_t classes);
 int engine_profile_read(pdec_engine* engine, int32_t kind, double* total_ms, int64_t* launches);
 
 /* Admit an empty trajectory and reserve ceil(reserve_tokens / 16) pages for

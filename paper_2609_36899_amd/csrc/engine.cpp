@@ -111,10 +111,15 @@ class Staging {
 class LaunchTimer {
  public:
   ~LaunchTimer() { reset_pool(); }
-  void enable(bool on) { on_ = on; }
-  bool on() const { return on_; }
+  void enable(uint32_t mask) { mask_ = mask; }
+  bool on() const { return mask_ != 0; }
+  // Classes not in the mask push an empty record so that end() pairs up.
   hipError_t begin(int kind, hipStream_t s) {
-    if (!on_) return hipSuccess;
+    if (!mask_) return hipSuccess;
+    if (!(mask_ >> kind & 1u)) {
+      open_.push_back({-1, nullptr, nullptr});
+      return hipSuccess;
+    }
     hipEvent_t a, b;
     hipError_t e = take(&a);
     if (e == hipSuccess) e = take(&b);
@@ -124,9 +129,10 @@ class LaunchTimer {
     return hipSuccess;
   }
   hipError_t end(hipStream_t s) {
-    if (!on_ || open_.empty()) return hipSuccess;
+    if (!mask_ || open_.empty()) return hipSuccess;
     Rec r = open_.back();
     open_.pop_back();
+    if (r.kind < 0) return hipSuccess;
     done_.push_back(r);
     return hipEventRecord(r.b, s);
   }
@@ -176,7 +182,7 @@ class LaunchTimer {
     done_.clear();
     open_.clear();
   }
-  bool on_ = false;
+  uint32_t mask_ = 0;
   std::vector<Rec> open_, done_;
   std::vector<hipEvent_t> free_, all_;
 };
@@ -558,9 +564,9 @@ void engine_destroy(pdec_engine* E) {
   delete E;
 }
 
-int engine_profile(pdec_engine* E, int32_t enable) {
+int engine_profile(pdec_engine* E, int32_t classes) {
   if (!E) return fail(PDEC_INVALID_ARG, "null engine");
-  E->timer.enable(enable != 0);
+  E->timer.enable((uint32_t)classes & 7u);
   return PDEC_OK;
 }
 

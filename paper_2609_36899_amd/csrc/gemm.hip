@@ -149,7 +149,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(int M, int N, int K, int
 // exactly once per step.  Larger batches take several M-blocks, laid out so
 // the M-blocks of one column tile are dispatched back to back (ids L and L+8
 // share an XCD).
-template <int WM, int NS, int NA>
+template <int WM, int NS>
 __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, int k_split,
                                                           int n_mb, int n_nb,
                                                           const uint16_t* __restrict__ A,
@@ -203,55 +203,65 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // W (from HBM) is prefetched NS k-steps ahead, A (L2-resident) NA.
-  static_assert(NS % NA == 0 && NA % 2 == 0, "ring depths");
-  u16x8 ra_[NA][ACH], rw_[NS][WCH];
+  // The A and W tiles of the next NS k-steps are in flight in a register
+  // ring.  As in the streaming kernel, the steady-state loop is branch-free
+  // (prefetch index clamped to the last step), so each LDS store waits only
+  // for its own slot's loads and the younger slots stay in flight.
+  static_assert(NS % 2 == 0, "ring depth must be even");
+  u16x8 ra_[NS][ACH], rw_[NS][WCH];
+  auto gload = [&](int i, u16x8(&ra)[ACH], u16x8(&rw)[WCH]) {
 #pragma unroll
-  for (int s = 0; s < NS; ++s)
-    if (s < n_iter) {
+    for (int j = 0; j < WCH; ++j) rw[j] = *(const u16x8*)(wsrc[j] + i * 1024);
 #pragma unroll
-      for (int j = 0; j < WCH; ++j) rw_[s][j] = *(const u16x8*)(wsrc[j] + s * 1024);
-      if (s < NA) {
+    for (int j = 0; j < ACH; ++j) ra[j] = *(const u16x8*)(asrc[j] + i * 64);
+  };
+  auto stage = [&](int buf, const u16x8(&ra)[ACH], const u16x8(&rw)[WCH]) {
 #pragma unroll
-        for (int j = 0; j < ACH; ++j) ra_[s][j] = *(const u16x8*)(asrc[j] + s * 64);
-      }
+    for (int j = 0; j < ACH; ++j) *(u16x8*)(la_s[buf] + dst + j * RSTEP * 64) = ra[j];
+#pragma unroll
+    for (int j = 0; j < WCH; ++j) *(u16x8*)(lw_s[buf] + (tid + j * THREADS) * 8) = rw[j];
+  };
+  auto compute = [&](int buf) {
+    const uint16_t* la = la_s[buf];
+    const uint16_t* lw = lw_s[buf];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      bf16x8 af[MT], bf[NT];
+#pragma unroll
+      for (int t = 0; t < MT; ++t) af[t] = *(const bf16x8*)(la + aoff[t][h]);
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        bf[t] = *(const bf16x8*)(lw + (((wn * 4 + t) * 2 + h) * 64 + lane) * 8);
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
-  for (int it0 = 0; it0 < n_iter; it0 += NS) {
+  };
+  const int last = n_iter - 1;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) gload(min(s, last), ra_[s], rw_[s]);
+  int it0 = 0;
+  for (; it0 + NS <= n_iter; it0 += NS) {
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      const int it = it0 + s;
-      if (it >= n_iter) break;
-      uint16_t* la = la_s[s & 1];
-      uint16_t* lw = lw_s[s & 1];
-#pragma unroll
-      for (int j = 0; j < ACH; ++j) *(u16x8*)(la + dst + j * RSTEP * 64) = ra_[s % NA][j];
-#pragma unroll
-      for (int j = 0; j < WCH; ++j) *(u16x8*)(lw + (tid + j * THREADS) * 8) = rw_[s][j];
+      // step it0 + s uses LDS buffer s & 1 (it0 is a multiple of NS, which is even)
+      stage(s & 1, ra_[s], rw_[s]);
       __syncthreads();
-      if (it + NS < n_iter) {
-#pragma unroll
-        for (int j = 0; j < WCH; ++j) rw_[s][j] = *(const u16x8*)(wsrc[j] + (it + NS) * 1024);
-      }
-      if (it + NA < n_iter) {
-#pragma unroll
-        for (int j = 0; j < ACH; ++j) ra_[s % NA][j] = *(const u16x8*)(asrc[j] + (it + NA) * 64);
-      }
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        bf16x8 af[MT], bf[NT];
-#pragma unroll
-        for (int t = 0; t < MT; ++t) af[t] = *(const bf16x8*)(la + aoff[t][h]);
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-          bf[t] = *(const bf16x8*)(lw + (((wn * 4 + t) * 2 + h) * 64 + lane) * 8);
-#pragma unroll
-        for (int i = 0; i < MT; ++i)
-#pragma unroll
-          for (int j = 0; j < NT; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
-      }
+      gload(min(it0 + s + NS, last), ra_[s], rw_[s]);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(s & 1);
     }
   }
+  const int tail = n_iter - it0;  // uniform over the work group
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    if (s < tail) {
+      stage(s & 1, ra_[s], rw_[s]);
+      __syncthreads();
+      compute(s & 1);
+    }
 
   float* o = out + (int64_t)blockIdx.z * M * N;
 #pragma unroll
@@ -335,23 +345,28 @@ int tile_rows(int M) { return M <= 128 ? 128 : 256; }
 
 int gemm_plan_splits(int dtype, int M, int N, int K, int* k_split) {
   const int kq = (dtype == 1) ? 64 : 16;
-  const bool stream = dtype == 1 && M <= kStreamMaxRows;
-  const bool tile = dtype == 1 && !stream;
-  int64_t groups;
-  if (stream) {
-    groups = ((N + 15) / 16 + 7) / 8;  // 4 waves x 2 strips
-  } else {
-    const int mblk = tile ? tile_rows(M) : 32, nblk = tile ? 128 : 64;
-    groups = (int64_t)((N + nblk - 1) / nblk) * ((M + mblk - 1) / mblk);
-  }
-  // Streaming: about one work group per CU (measured best on all five
-  // shapes).  Tiles at small M: two per CU; at larger M about one, since
-  // every extra split writes and re-reads an M x N fp32 slab; the 256-row
-  // tile holds a whole CU.
-  const int64_t target = stream ? 256 : (!tile || M <= 64 ? 512 : (M <= 128 ? 256 : 224));
   const int ksteps = (K + kq - 1) / kq;
   int s = 1;
-  if (groups < target) s = (int)std::min<int64_t>((target + groups - 1) / groups, 8);
+  if (dtype == 1) {
+    int64_t groups;
+    if (M <= kStreamMaxRows) {
+      groups = ((N + 15) / 16 + 7) / 8;  // 4 waves x 2 strips
+    } else {
+      const int rows = tile_rows(M);
+      groups = (int64_t)((N + 127) / 128) * ((M + rows - 1) / rows);
+    }
+    // Measured on the 8B shapes with weights streamed from HBM: the best
+    // split count fills one round of work groups on the 256 CUs (a partial
+    // second round costs 15-30%), except that the 128-row tile prefers two
+    // short rounds to one long one when the column tiles alone nearly fill
+    // the chip.
+    s = (int)std::max<int64_t>(1, 256 / groups);
+    if (M > kStreamMaxRows && tile_rows(M) == 128 && s == 1 && groups <= 256) s = 2;
+    s = std::min(s, 8);
+  } else {
+    const int64_t groups = (int64_t)((N + 63) / 64) * ((M + 31) / 32);
+    if (groups < 512) s = (int)std::min<int64_t>((512 + groups - 1) / groups, 8);
+  }
   s = std::max(1, std::min(s, ksteps));
   const int steps_per = (ksteps + s - 1) / s;
   *k_split = steps_per * kq;
@@ -386,10 +401,10 @@ hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t ld
       const int n_mb = (M + rows - 1) / rows, n_nb = (N + 127) / 128;
       const dim3 grid(((n_nb + 7) / 8) * 8 * n_mb, 1, splits);
       if (rows == 128)
-        gemm_bf16_tile<2, 2, 2><<<grid, dim3(256), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a,
+        gemm_bf16_tile<2, 2><<<grid, dim3(256), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a,
                                                                lda, w, out);
       else
-        gemm_bf16_tile<4, 2, 2><<<grid, dim3(512), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a,
+        gemm_bf16_tile<4, 2><<<grid, dim3(512), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a,
                                                                lda, w, out);
     }
   } else {

@@ -164,9 +164,13 @@ class Engine:
         return self._pool_view()[layer, 1].view(self.n_pages, s.n_kv_heads, s.head_dim,
                                                 PAGE_TOKENS)
 
-    def profile(self, enable: bool) -> None:
-        """Bracket timed launch classes with HIP events (see engine_profile)."""
-        N.check(self.lib.engine_profile(self.handle, int(bool(enable))))
+    def profile(self, kinds: Sequence[int] = ()) -> None:
+        """Bracket the launches of the given timer classes (N.TIMER_*) with HIP
+        events; an empty sequence turns timing off (see engine_profile)."""
+        mask = 0
+        for k in kinds:
+            mask |= 1 << int(k)
+        N.check(self.lib.engine_profile(self.handle, mask))
 
     def profile_read(self, kind: int):
         """(total ms, launch count) of one timed class since the last read."""
