@@ -411,15 +411,107 @@ def run_multiturn(workload, segments, seg_steps, warmup):
     return out
 
 
+# Decode landscape: batch x mean context x within-batch skew (lognormal sigma).
+LANDSCAPE = {"batches": (1, 4, 16, 64, 256), "means": (1024, 4096, 16384, 65536),
+             "sigmas": (0.0, 1.0)}
+
+
+def run_landscape(steps=8, warmup=2):
+    """Decode throughput over batch x mean context x skew (one engine per cell).
+
+    Per cell: tokens/s, step time, achieved HBM GB/s over the algorithmic
+    bytes (weights once + every cached KV byte once + new KV + logits) and
+    the mean per-trajectory bandwidth share (KV_b + W / B) / step time.
+    Cells whose KV does not fit in free HBM are reported as skipped.
+    """
+    import torch
+
+    import paper_2609_36899_amd as P
+    from workload import EIGHT_B, lengths_skewed
+
+    shape = EIGHT_B
+    torch.cuda.set_device(0)
+    weights = gpu_weights(shape)
+    per_tok = P.kv_bytes_per_token(shape, P.BF16)
+    w_bytes_layerless = weight_bytes_per_step(shape, 0)
+    cells = []
+    for batch in LANDSCAPE["batches"]:
+        for mean in LANDSCAPE["means"]:
+            for sigma in LANDSCAPE["sigmas"]:
+                if batch == 1 and sigma > 0:
+                    continue
+                lens = lengths_skewed(batch, mean, sigma, seed=batch * 7919 + mean)
+                grow = warmup + steps + 1
+                pages = int(np.sum((lens + grow + 15) // 16)) + 64
+                pool_bytes = pages * 16 * per_tok
+                free, _ = torch.cuda.mem_get_info()
+                cell = {"batch": batch, "mean_context": mean, "sigma": sigma,
+                        "max_context": int(lens.max()), "kv_gib": round(pool_bytes / 2**30, 1)}
+                if pool_bytes > free - (8 << 30):
+                    cell["skipped"] = "KV exceeds free HBM"
+                    cells.append(cell)
+                    continue
+                E = P.Engine(shape, weights, P.BF16, pool_bytes, max_seqs=batch,
+                             max_seq_len=int(lens.max()) + grow + 16, max_batch=batch,
+                             max_chunk=16)
+                g = torch.Generator(device="cuda")
+                g.manual_seed(batch + mean)
+                pool = E.kv_pool.view(torch.bfloat16)
+                for i in range(0, pool.numel(), 1 << 30):
+                    pool[i:i + (1 << 30)].normal_(0.0, 1.0, generator=g)
+                ids = np.array([E.kv_alloc(0) for _ in range(batch)], dtype=np.int32)
+                for sid, n in zip(ids, lens):
+                    E.kv_extend_uninit(int(sid), int(n))
+                tok = torch.randint(0, shape.vocab, (batch,), dtype=torch.int32, device="cuda",
+                                    generator=g)
+                logits = torch.empty((batch, shape.vocab), dtype=torch.float32, device="cuda")
+                for _ in range(warmup):
+                    E.decode_step(ids, tok, logits)
+                    E.sample(logits, tok)
+                torch.cuda.synchronize()
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                for _ in range(steps):
+                    E.decode_step(ids, tok, logits)
+                    E.sample(logits, tok)
+                b.record()
+                torch.cuda.synchronize()
+                ms = a.elapsed_time(b) / steps
+                keys = float(np.mean([np.sum(lens + warmup + t + 1) for t in range(steps)]))
+                w_bytes = w_bytes_layerless + 2 * batch * shape.d_model
+                step_bytes = keys * per_tok + batch * per_tok + w_bytes + 2 * batch * shape.vocab * 4
+                share = (float(np.mean(lens)) * per_tok + w_bytes / batch) / (ms / 1e3) / 1e9
+                cell.update({"tokens_per_s": round(batch / (ms / 1e3), 1), "ms_per_step": round(ms, 3),
+                             "hbm_gbps": round(step_bytes / (ms / 1e3) / 1e9, 1),
+                             "hbm_frac": round(step_bytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 3),
+                             "share_gbps_per_traj": round(share, 1)})
+                cells.append(cell)
+                log(f"landscape B={batch} mean={mean} sigma={sigma}: {cell['tokens_per_s']} tok/s, "
+                    f"{cell['hbm_gbps']} GB/s")
+                del E, pool, logits
+                torch.cuda.empty_cache()
+    return {"metric": "decode tokens/s over batch x mean context x skew, 1 MI355X",
+            "value": None, "unit": "tokens/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+            "higher_is_better": True, "data": "synthetic", "dtype": "bf16",
+            "config": {"workload": "landscape-8b", **{k: list(v) for k, v in LANDSCAPE.items()}},
+            "cells": cells, "cpu_baseline": None}
+
+
 PROJ_SHAPES = [("qkv", 6144, 4096), ("o", 4096, 4096), ("gate_up", 28672, 4096),
                ("down", 4096, 14336), ("lm_head", 128256, 4096)]
 
 
-def run_projections(batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), iters=20):
+def run_projections(batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), iters=24):
     """The 8B projection shapes through weight_projection, swept over the batch.
 
     Per shape and batch: time per call (HIP events), weight-stream GB/s,
     TFLOP/s, and the roofline time max(weights / 8 TB/s, flops / 2.5 PF/s).
+    Calls rotate over copies of the weight totalling >= 768 MB, so every call
+    streams its weight from HBM rather than from the 256 MB last-level cache
+    (as in a decode step, where 32 layers' weights pass through).  The time
+    includes the split-K reduction kernel, which inside a decode step is fused
+    into the consumer.  For context, torch.matmul (hipBLASLt) on row-major
+    copies of the same weights, rotated the same way, bf16 output.
     """
     import torch
 
@@ -429,41 +521,54 @@ def run_projections(batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), iters=20):
     g = torch.Generator(device="cuda")
     g.manual_seed(0)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn, n_copies):
+        for i in range(3):
+            fn(i % n_copies)
+        torch.cuda.synchronize()
+        n = max(iters, 2 * n_copies)
+        ev0.record()
+        for i in range(n):
+            fn(i % n_copies)
+        ev1.record()
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / n * 1e3
+
     rows = []
     for name, n, k in PROJ_SHAPES:
-        w = P.pack_weight(torch.empty((n, k), dtype=torch.bfloat16,
-                                      device="cuda").normal_(0, 0.02, generator=g))
+        copies = max(1, -(-(768 << 20) // (2 * n * k)))
+        raw = [torch.empty((n, k), dtype=torch.bfloat16, device="cuda").normal_(
+            0, 0.02, generator=g) for _ in range(copies)]
+        packed = [P.pack_weight(w) for w in raw]
         for m in batches:
             x = torch.empty((m, k), dtype=torch.bfloat16, device="cuda").normal_(generator=g)
             out = torch.empty((m, n), dtype=torch.float32, device="cuda")
             ws = torch.empty(max(1, P.weight_projection_workspace_bytes(P.BF16, m, n, k)),
                              dtype=torch.uint8, device="cuda")
-            for _ in range(3):
-                P.weight_projection(x, w, out, ws)
-            torch.cuda.synchronize()
-            ev0.record()
-            for _ in range(iters):
-                P.weight_projection(x, w, out, ws)
-            ev1.record()
-            torch.cuda.synchronize()
-            us = ev0.elapsed_time(ev1) / iters * 1e3
+            us = timed(lambda i: P.weight_projection(x, packed[i], out, ws), copies)
+            ref_us = timed(lambda i: torch.matmul(x, raw[i].t()), copies)
             wbytes, flops = 2 * n * k, 2 * m * n * k
             roof_us = max(wbytes / HBM_PEAK_GBS / 1e3, flops / 2.5e15 * 1e6)
             rows.append({"shape": name, "N": n, "K": k, "M": m, "us": round(us, 2),
                          "weight_GBps": round(wbytes / us / 1e3, 1),
                          "TFLOPs": round(flops / us / 1e6, 1),
-                         "roofline_us": round(roof_us, 2), "frac_of_roofline": round(roof_us / us, 3)})
+                         "roofline_us": round(roof_us, 2), "frac_of_roofline": round(roof_us / us, 3),
+                         "torch_matmul_us": round(ref_us, 2)})
+        del raw, packed
+        torch.cuda.empty_cache()
         log(f"projections {name} done")
-    layer = {}
+    layer, layer_ref = {}, {}
     for r in rows:
         if r["shape"] != "lm_head":
             layer[r["M"]] = layer.get(r["M"], 0.0) + r["us"]
+            layer_ref[r["M"]] = layer_ref.get(r["M"], 0.0) + r["torch_matmul_us"]
     return {"metric": "weight projection time per 8B layer, 1 MI355X", "value": layer.get(256),
             "unit": "us at batch 256", "n_gpus": 1, "higher_is_better": False,
             "data": "synthetic", "dtype": "bf16",
             "config": {"workload": "projections-8b", "batches": list(batches)},
-            "layer_us": {str(m): round(v, 1) for m, v in layer.items()}, "rows": rows,
-            "cpu_baseline": None}
+            "layer_us": {str(m): round(v, 1) for m, v in layer.items()},
+            "layer_us_torch_matmul": {str(m): round(v, 1) for m, v in layer_ref.items()},
+            "rows": rows, "cpu_baseline": None}
 
 
 def run_kv_transfer(lengths=(4096, 16384, 65536)):
@@ -536,7 +641,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
                     choices=sorted(WORKLOADS) + sorted(MULTITURN)
-                    + ["kv-transfer-8b", "projections-8b"])
+                    + ["kv-transfer-8b", "projections-8b", "landscape-8b"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -548,6 +653,8 @@ def main():
         out = run_kv_transfer()
     elif args.workload == "projections-8b":
         out = run_projections()
+    elif args.workload == "landscape-8b":
+        out = run_landscape()
     elif args.workload in MULTITURN:
         out = run_multiturn(args.workload, segments=3, seg_steps=args.steps, warmup=args.warmup)
     else:

@@ -138,6 +138,18 @@ def lengths_pareto(batch: int, alpha: float, xmin: int, cap: int, seed: int) -> 
     return np.minimum(np.floor(xmin * u ** (-1.0 / alpha)), cap).astype(np.int64)
 
 
+def lengths_skewed(batch: int, mean: int, sigma: float, seed: int) -> np.ndarray:
+    """Within-batch skew at a fixed mean: lengths mean * exp(sigma z - sigma^2 / 2),
+    z ~ N(0, 1), rescaled so the batch mean is `mean`, clamped to [16, 16 mean].
+    sigma = 0 gives every trajectory the same length."""
+    if sigma == 0.0 or batch == 1:
+        return np.full(batch, int(mean), dtype=np.int64)
+    z = np.random.default_rng(seed).standard_normal(batch)
+    x = np.exp(sigma * z - 0.5 * sigma * sigma)
+    x = x / x.mean() * mean
+    return np.clip(np.round(x), 16, 16 * mean).astype(np.int64)
+
+
 # ---------------------------------------------------------------------------
 # Isolated paged decode attention operands.
 # ---------------------------------------------------------------------------
