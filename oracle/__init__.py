@@ -19,8 +19,10 @@ the module docstrings below.
 from .decoder import (Decoder, ModelWeights, attention, greedy, recompute_logits, rmsnorm,
                       rope, silu)
 from .paged import gather_pages, paged_decode_attention
+from .sampling import nucleus_mask, sample_top_p, token_masses
 
 __all__ = [
     "Decoder", "ModelWeights", "attention", "greedy", "recompute_logits", "rmsnorm", "rope",
-    "silu", "gather_pages", "paged_decode_attention",
+    "silu", "gather_pages", "paged_decode_attention", "nucleus_mask", "sample_top_p",
+    "token_masses",
 ]
