@@ -18,6 +18,7 @@ prefilled: decode cost does not depend on KV values).  Prints one JSON line.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -497,6 +498,76 @@ def run_landscape(steps=8, warmup=2):
             "cells": cells, "cpu_baseline": None}
 
 
+def run_sampling(batches=(1, 16, 256, 512), vocab=128256, iters=20):
+    """Greedy argmax and temperature/top-p sampling over 8B-sized logit rows:
+    time per call (HIP events) at each batch size."""
+    import torch
+
+    import paper_2609_36899_amd as P
+    from workload import TINY
+
+    torch.cuda.set_device(0)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0)
+    # greedy sampling goes through an engine's `sample`; a tiny engine with
+    # the full vocabulary supplies it (only its vocab size matters here).
+    shape = dataclasses.replace(TINY, vocab=vocab)
+    w = gpu_weights_f32_tiny(shape)
+    E = P.Engine(shape, w, P.F32, 4 * 16 * P.kv_bytes_per_token(shape, P.F32), max_seqs=1,
+                 max_seq_len=16, max_batch=max(batches), max_chunk=16)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    rows = []
+    for b in batches:
+        logits = (torch.randn((b, vocab), device="cuda", generator=g) * 3.0).contiguous()
+        u = torch.rand(b, device="cuda", generator=g)
+        out = torch.empty(b, dtype=torch.int32, device="cuda")
+        res = {"batch": b}
+        for name, fn in (("greedy_us", lambda: E.sample(logits, out, batch=b)),
+                         ("top_p_us", lambda: P.sample_top_p(logits, out, 0.8, 0.95, u))):
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            ev0.record()
+            for _ in range(iters):
+                fn()
+            ev1.record()
+            torch.cuda.synchronize()
+            res[name] = round(ev0.elapsed_time(ev1) / iters * 1e3, 2)
+        rows.append(res)
+        log(f"sampling B={b}: {res}")
+    return {"metric": "sampling time per call over 128256-token logit rows, 1 MI355X",
+            "value": None, "unit": "us", "n_gpus": 1, "higher_is_better": False,
+            "data": "synthetic", "dtype": "f32",
+            "config": {"workload": "sampling-8b", "vocab": vocab, "temperature": 0.8,
+                       "top_p": 0.95},
+            "rows": rows, "cpu_baseline": None}
+
+
+def gpu_weights_f32_tiny(shape):
+    """fp32 weights of a small shape, drawn on the GPU and packed."""
+    import torch
+
+    import paper_2609_36899_amd as P
+    g = torch.Generator(device="cuda")
+    g.manual_seed(1)
+
+    def mat(r, c):
+        return torch.empty((r, c), device="cuda").normal_(0.0, 0.02, generator=g)
+
+    ones = lambda: torch.ones(shape.d_model, device="cuda")
+    layers = [{"wq": P.pack_weight(mat(shape.q_dim, shape.d_model)),
+               "wk": P.pack_weight(mat(shape.kv_dim, shape.d_model)),
+               "wv": P.pack_weight(mat(shape.kv_dim, shape.d_model)),
+               "wo": P.pack_weight(mat(shape.d_model, shape.q_dim)),
+               "w_gate": P.pack_weight(mat(shape.ffn_dim, shape.d_model)),
+               "w_up": P.pack_weight(mat(shape.ffn_dim, shape.d_model)),
+               "w_down": P.pack_weight(mat(shape.d_model, shape.ffn_dim)),
+               "attn_norm": ones(), "ffn_norm": ones()} for _ in range(shape.n_layers)]
+    return {"embed": mat(shape.vocab, shape.d_model),
+            "lm_head": P.pack_weight(mat(shape.vocab, shape.d_model)),
+            "final_norm": ones(), "layers": layers}
+
+
 PROJ_SHAPES = [("qkv", 6144, 4096), ("o", 4096, 4096), ("gate_up", 28672, 4096),
                ("down", 4096, 14336), ("lm_head", 128256, 4096)]
 
@@ -641,7 +712,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
                     choices=sorted(WORKLOADS) + sorted(MULTITURN)
-                    + ["kv-transfer-8b", "projections-8b", "landscape-8b"])
+                    + ["kv-transfer-8b", "projections-8b", "landscape-8b", "sampling-8b"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -655,6 +726,8 @@ def main():
         out = run_projections()
     elif args.workload == "landscape-8b":
         out = run_landscape()
+    elif args.workload == "sampling-8b":
+        out = run_sampling()
     elif args.workload in MULTITURN:
         out = run_multiturn(args.workload, segments=3, seg_steps=args.steps, warmup=args.warmup)
     else:

@@ -263,6 +263,27 @@ int sample(pdec_engine* engine, int32_t batch, const float* logits_dev, int32_t*
  * Slots past lens[b] in the last page are never read.
  * ------------------------------------------------------------------------- */
 /* ---------------------------------------------------------------------------
+ * Temperature / nucleus (top-p) sampling for RL rollouts, which sample their
+ * actions (Background, "RL Post-Training Workflow"; the paper does not state
+ * its sampler).  Random numbers are inputs: uniforms_dev holds one u in
+ * [0, 1) per row (values outside are clamped).  Per row b, with z the
+ * logits, every decision after one fp64 exponential is integer arithmetic:
+ *   q_v = rint(exp((z_v - max z) * (1/T)) * 2^40), S = sum q_v,
+ *   nucleus = shortest prefix of the tokens ordered by (q desc, index asc)
+ *             with mass >= ceil(rint(top_p * 2^24) * S / 2^24),
+ *   Z = nucleus mass, target = floor(floor(u * 2^24) * Z / 2^24),
+ *   token = first nucleus token in index order whose running mass > target.
+ * A given (logits, T, top_p, u) always yields the same token.
+ *   logits_dev: device fp32 [batch][vocab]; uniforms_dev: device fp32
+ *   [batch]; tokens_dev_out: device int32 [batch].  No scratch memory.
+ *   Asynchronous on stream.
+ * Errors: PDEC_INVALID_ARG (temperature <= 0 or not finite, top_p outside
+ * (0, 1], batch or vocab < 1, null pointer).
+ * ------------------------------------------------------------------------- */
+int sample_top_p(int32_t batch, int32_t vocab, const float* logits_dev, float temperature,
+                 float top_p, const float* uniforms_dev, int32_t* tokens_dev_out, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Weight packing.  Each decode step streams every projection matrix from HBM
  * once for the whole batch (Introduction; Design Principles, "Specialization
  * in Heterogeneous Pools"), so bf16 matrices are stored in a layout whose

@@ -44,6 +44,9 @@ hipError_t launch_attention_combine(int head_dim, int rows_per_item, int n_qbloc
 // bf16: A and W bf16, K % 64 == 0, k_split % 64 == 0.  f32: any sizes.
 hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t lda,
                        const WSegs& w, float* out, int splits, int k_split, hipStream_t stream);
+// Temperature / top-p sampling (sample.hip).
+hipError_t launch_sample_top_p(int B, int V, const float* logits, float temperature, float top_p,
+                               const float* uniforms, int32_t* tokens, hipStream_t stream);
 // bf16: pack a row-major [N][K] weight into the strip layout the GEMM kernels
 // read (((N + 15) / 16) * 16 * K elements); fp32: plain copy.
 hipError_t launch_pack_weight(int dtype, int N, int K, const void* w, void* packed,

@@ -1,0 +1,283 @@
+// Temperature / nucleus (top-p) sampling with caller-supplied uniforms.
+//
+// RL rollouts sample their actions rather than taking the argmax (paper:
+// Background, "RL Post-Training Workflow"); the paper does not state the
+// sampler, so this is the common temperature + top-p rule, defined so that
+// every decision is exact integer arithmetic after one exponential:
+//
+//   e_v = exp((z_v - max z) / T)            (fp64)
+//   q_v = rint(e_v * 2^40)                  (integer mass, 0 .. 2^40)
+//   S   = sum_v q_v
+//   nucleus: the shortest prefix of the tokens ordered by (q desc, index asc)
+//            whose mass reaches ceil(p24 * S / 2^24), p24 = rint(top_p * 2^24)
+//   Z   = nucleus mass, target = floor(u24 * Z / 2^24), u24 = floor(u * 2^24)
+//   token = the first nucleus token, in index order, whose running nucleus
+//           mass exceeds target.
+//
+// One work group of 1024 threads per row.  The nucleus threshold key is
+// found by a radix select over the 41-bit keys (digits of 11, 11, 11 and 8
+// bits) with 64-bit integer mass histograms in LDS (integer atomics: the
+// result does not depend on their order); the final index-order walk uses
+// wave-level scans over each wave's contiguous range.  Only the first round
+// needs every token's mass.  Later passes need only the tokens whose mass can
+// fall in the current key range.  A conservative test on x = (z - max z)/T
+// (the mass is monotone in x) selects them, and only they recompute the
+// exponential, so every decision stays exact without a stored row of keys.
+#include "hip_common.h"
+#include "kernels.h"
+
+namespace pdec {
+
+namespace {
+
+constexpr int kThreads = 1024, kWaves = kThreads / 64;
+constexpr int kUnroll = 8;  // loads in flight per lane: index slabs of 64
+constexpr int kRounds = 4, kMaxBins = 2048;
+// Radix digits of the 41-bit keys, most significant first: bits 40..30,
+// 29..19, 18..8, 7..0.
+__device__ constexpr int kShift[kRounds] = {30, 19, 8, 0};
+__device__ constexpr int kWidth[kRounds] = {11, 11, 11, 8};
+typedef unsigned __int128 u128;
+
+// Integer mass of one logit.  Below x = -28.5 the exponential is under
+// 2^-41 and the mass rounds to exactly 0, so the exponential is skipped.
+__device__ __forceinline__ uint64_t mass_of(float z, double m, double inv_t) {
+  const double x = ((double)z - m) * inv_t;
+  if (x < -28.5) return 0;
+  return (uint64_t)rint(exp(x) * 0x1p40);
+}
+
+__device__ __forceinline__ uint64_t wave_scan_incl(uint64_t v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint64_t o = __shfl_up(v, off, 64);
+    if (lane >= off) v += o;
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Lowest x whose mass can reach key k (k >= 1): rint(e * 2^40) >= k needs
+// e * 2^40 >= k - 1/2; a margin far above the exponential's error keeps the
+// test conservative.
+__device__ __forceinline__ double x_floor(uint64_t k) {
+  return k == 0 ? -INFINITY : log(((double)k - 0.5) * 0x1p-40) - 1e-9;
+}
+
+__global__ __launch_bounds__(kThreads) void sample_top_p_kernel(
+    int V, const float* __restrict__ logits, double inv_t, uint32_t p24,
+    const float* __restrict__ uniforms, int32_t* __restrict__ tokens) {
+  __shared__ uint64_t hist[kMaxBins];
+  __shared__ uint64_t wave_a[kWaves], wave_b[kWaves];
+  __shared__ float red_f[kWaves];
+  __shared__ uint64_t sel[3];  // digit, mass above it, T_p
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const float* z = logits + (int64_t)blockIdx.x * V;
+  // Wave w owns the index range [w0, w1), read coalesced in blocks of
+  // kUnroll slabs of 64 (all loads of a block issued before any use); index
+  // order is (wave, block, slab, lane).  Out-of-range slots read as -inf.
+  const int span = ((V + kWaves * 64 - 1) / (kWaves * 64)) * 64;
+  const int w0 = min(V, wave * span), w1 = min(V, w0 + span);
+  auto load_block = [&](int base, float (&zv)[kUnroll]) {
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int i = base + u * 64 + lane;
+      zv[u] = i < w1 ? z[i] : -INFINITY;
+    }
+  };
+
+  // Row max.
+  float mx = -INFINITY;
+  for (int base = w0; base < w1; base += 64 * kUnroll) {
+    float zv[kUnroll];
+    load_block(base, zv);
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) mx = fmaxf(mx, zv[u]);
+  }
+  mx = wave_max(mx);
+  if (lane == 0) red_f[wave] = mx;
+  __syncthreads();
+  if (t == 0) {
+    float bmax = red_f[0];
+    for (int w = 1; w < kWaves; ++w) bmax = fmaxf(bmax, red_f[w]);
+    red_f[0] = bmax;
+  }
+  __syncthreads();
+  const double m = (double)red_f[0];
+
+  // Radix select of the threshold key kappa: the largest key with
+  // mass{q >= kappa} >= T_p, where T_p = ceil(p24 * S / 2^24).  Each thread
+  // adds runs of equal digits in a register and flushes a run to the LDS
+  // histogram only when the digit changes: most tokens share one bin, and
+  // per-element atomics on one address would serialise.
+  uint64_t prefix = 0, above = 0, t_p = 0;
+  for (int r = 0; r < kRounds; ++r) {
+    const int shift = kShift[r], bins = 1 << kWidth[r];
+    for (int bin = t; bin < bins; bin += kThreads) hist[bin] = 0;
+    __syncthreads();
+    int run_bin = -1;
+    uint64_t run_sum = 0;
+    // keys of this round's range: [prefix << top, (prefix + 1) << top)
+    const int top = shift + kWidth[r];
+    const double xlo = x_floor(prefix << top), xhi = x_floor((prefix + 1) << top);
+    for (int base = w0; base < w1; base += 64 * kUnroll) {
+      float zv[kUnroll];
+      load_block(base, zv);
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const double x = ((double)zv[u] - m) * inv_t;
+        if (x < xlo || (r > 0 && x > xhi + 2e-9)) continue;
+        const uint64_t q = mass_of(zv[u], m, inv_t);
+        if (q != 0 && (q >> top) == prefix) {
+          const int d = (int)((q >> shift) & (uint64_t)(bins - 1));
+          if (d != run_bin) {
+            if (run_bin >= 0) atomicAdd((unsigned long long*)&hist[run_bin], run_sum);
+            run_bin = d;
+            run_sum = 0;
+          }
+          run_sum += q;
+        }
+      }
+    }
+    if (run_bin >= 0) atomicAdd((unsigned long long*)&hist[run_bin], run_sum);
+    __syncthreads();
+    if (r == 0) {  // S = total mass, T_p from it
+      uint64_t part = 0;
+      for (int bin = t; bin < bins; bin += kThreads) part += hist[bin];
+      part = wave_sum_u64(part);
+      if (lane == 0) wave_a[wave] = part;
+      __syncthreads();
+      if (t == 0) {
+        uint64_t total = 0;
+        for (int w = 0; w < kWaves; ++w) total += wave_a[w];
+        sel[2] = (uint64_t)(((u128)p24 * total + ((u128)1 << 24) - 1) >> 24);
+      }
+      __syncthreads();
+    }
+    t_p = sel[2];
+    // Select the digit: walking bins from the top, the first whose
+    // cumulative mass (from `above`) reaches T_p.  Thread t holds the bins
+    // ranked 2t and 2t+1 from the top; a block scan gives the cumulative sums.
+    const int per = (bins + kThreads - 1) / kThreads;  // 2 or 1
+    uint64_t mine = 0;
+    for (int j = 0; j < per; ++j) {
+      const int rank = t * per + j;
+      if (rank < bins) mine += hist[bins - 1 - rank];
+    }
+    const uint64_t incl_w = wave_scan_incl(mine, lane);
+    if (lane == 63) wave_b[wave] = incl_w;
+    __syncthreads();
+    uint64_t before = above + incl_w - mine;
+    for (int w = 0; w < wave; ++w) before += wave_b[w];
+    for (int j = 0; j < per; ++j) {
+      const int rank = t * per + j;
+      if (rank >= bins) break;
+      const uint64_t h = hist[bins - 1 - rank];
+      // The digit is the first bin reaching T_p; the lowest bin (rank
+      // bins-1) always does, by the invariant mass(prefix range) >= T_p.
+      if (before < t_p && (before + h >= t_p || rank == bins - 1)) {
+        sel[0] = (uint64_t)(bins - 1 - rank);
+        sel[1] = before;
+      }
+      before += h;
+    }
+    __syncthreads();
+    prefix = (prefix << kWidth[r]) | sel[0];
+    above = sel[1];
+    __syncthreads();
+  }
+  const uint64_t kappa = prefix;  // >= 1: zero-mass keys never enter the histograms
+  // Tokens with q == kappa join the nucleus in index order until the mass
+  // reaches T_p: the first n_tie of them.
+  const uint64_t n_tie = (t_p - above + kappa - 1) / kappa;
+
+  // One pass: ties and strict-member mass per wave (only x >= x_floor(kappa)
+  // can reach kappa).
+  const double xk = x_floor(kappa);
+  uint64_t ties = 0, strict = 0;
+  for (int base = w0; base < w1; base += 64 * kUnroll) {
+    float zv[kUnroll];
+    load_block(base, zv);
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      if (((double)zv[u] - m) * inv_t < xk) continue;
+      const uint64_t q = mass_of(zv[u], m, inv_t);
+      ties += q == kappa;
+      strict += q > kappa ? q : 0;
+    }
+  }
+  ties = wave_sum_u64(ties);
+  strict = wave_sum_u64(strict);
+  if (lane == 0) {
+    wave_a[wave] = ties;
+    wave_b[wave] = strict;
+  }
+  __syncthreads();
+  // Wave w holds ties ranked [tie_base, tie_base + ties); its member ties
+  // are those ranked below n_tie.
+  uint64_t tie_base = 0, mass_base = 0, Z = 0, own = 0, tb = 0;
+  for (int w = 0; w < kWaves; ++w) {
+    const uint64_t nt = wave_a[w];
+    const uint64_t member_ties = n_tie > tb ? min(nt, n_tie - tb) : 0;
+    const uint64_t wm = wave_b[w] + member_ties * kappa;
+    if (w < wave) mass_base += wm;
+    if (w == wave) {
+      own = wm;
+      tie_base = tb;
+    }
+    Z += wm;
+    tb += nt;
+  }
+  float u = uniforms[blockIdx.x];
+  u = fminf(fmaxf(u, 0.f), 0x1.fffffep-1f);
+  const uint64_t u24 = (uint64_t)(u * 0x1p24f);
+  const uint64_t target = (uint64_t)(((u128)u24 * Z) >> 24);
+  // The wave whose nucleus mass range [mass_base, mass_base + own) holds
+  // target walks its range in index order.
+  if (own > 0 && mass_base <= target && target < mass_base + own) {
+    uint64_t run = mass_base, rank = tie_base;
+    bool found = false;
+    for (int base = w0; base < w1 && !found; base += 64 * kUnroll) {
+      float zv[kUnroll];
+      load_block(base, zv);
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int i = base + u * 64 + lane;
+        uint64_t q = 0;
+        if (((double)zv[u] - m) * inv_t >= xk) q = mass_of(zv[u], m, inv_t);
+        const bool tie = q == kappa;  // out-of-range slots have q = 0 < kappa
+        const uint64_t tie_mask = __ballot(tie);
+        const uint64_t my_rank = rank + __popcll(tie_mask & ((1ull << lane) - 1));
+        const uint64_t mass = (q > kappa || (tie && my_rank < n_tie)) ? q : 0;
+        const uint64_t incl = run + wave_scan_incl(mass, lane);
+        const uint64_t hit = __ballot(mass > 0 && incl > target);
+        if (hit) {
+          if (lane == __ffsll((unsigned long long)hit) - 1) tokens[blockIdx.x] = i;
+          found = true;
+          break;
+        }
+        run = __shfl(incl, 63, 64);
+        rank += __popcll(tie_mask);
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_sample_top_p(int B, int V, const float* logits, float temperature, float top_p,
+                               const float* uniforms, int32_t* tokens, hipStream_t stream) {
+  if (B == 0) return hipSuccess;
+  const double inv_t = 1.0 / (double)temperature;
+  uint32_t p24 = (uint32_t)rint((double)top_p * 16777216.0);
+  p24 = p24 < 1 ? 1 : (p24 > (1u << 24) ? (1u << 24) : p24);
+  sample_top_p_kernel<<<B, kThreads, 0, stream>>>(V, logits, inv_t, p24, uniforms, tokens);
+  return hipGetLastError();
+}
+
+}  // namespace pdec

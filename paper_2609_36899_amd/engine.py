@@ -287,6 +287,21 @@ def weight_projection(x: torch.Tensor, w: PackedWeight, out: torch.Tensor,
     return out
 
 
+def sample_top_p(logits: torch.Tensor, tokens_out: torch.Tensor, temperature: float,
+                 top_p: float, uniforms: torch.Tensor,
+                 stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """Temperature / top-p sampling of each row of logits [B, V] with the
+    given uniforms [B] (see sample_top_p in include/pdec.h)."""
+    assert logits.dim() == 2 and logits.dtype == torch.float32 and logits.is_contiguous()
+    B, V = logits.shape
+    assert uniforms.dtype == torch.float32 and uniforms.numel() >= B and uniforms.is_cuda
+    assert tokens_out.dtype == torch.int32 and tokens_out.numel() >= B
+    N.check(N.load().sample_top_p(B, V, logits.data_ptr(), float(temperature), float(top_p),
+                                  uniforms.data_ptr(), tokens_out.data_ptr(),
+                                  _stream_handle(stream)))
+    return tokens_out
+
+
 def paged_attention_workspace_bytes(batch: int, n_q_heads: int, n_kv_heads: int,
                                     head_dim: int) -> int:
     return N.check(N.load().paged_attention_workspace_bytes(batch, n_q_heads, n_kv_heads,
