@@ -9,6 +9,8 @@ What it computes, for one trajectory with t the input token at position p
   per layer:
     h  = rmsnorm(x) * g1
     q, k, v = Wq h, Wk h, Wv h            reshaped to (Hq,Dh), (Hkv,Dh), (Hkv,Dh)
+    [q/k-norm variant: q = rmsnorm(q) * gq, k = rmsnorm(k) * gk per head,
+     over Dh, when the layer carries q_norm / k_norm gains]
     q, k = rope(q, p), rope(k, p)         rotate-half pairs (i, i + Dh/2),
                                           angle p * base^(-2i/Dh)
     append k, v to the trajectory's cache (the rotated k is cached)
@@ -22,8 +24,10 @@ What it computes, for one trajectory with t the input token at position p
 Readings of points the paper leaves open (it names dense Qwen3 models run by
 its inference backend, Evaluation: experimental setup, and gives no layer
 definition):
-  * Llama-style pre-norm block, no biases, no per-head q/k norm, untied LM head
-    and a final RMSNorm.
+  * Llama-style pre-norm block, no biases, untied LM head and a final RMSNorm.
+    The per-head q/k RMSNorm of the Qwen3 family (its public model
+    definition, not the paper) is an option: a layer with ``q_norm`` and
+    ``k_norm`` gains normalises each q and k head over Dh before RoPE.
   * RoPE in the rotate-half pairing with base 10000.
   * Contiguous GQA groups: query head h reads KV head floor(h*Hkv/Hq).
   * Attention is causal and includes the current token; scale 1/sqrt(Dh);
@@ -145,6 +149,9 @@ class Decoder:
             q = (lay["wq"] @ h).reshape(w.n_q_heads, w.head_dim)
             k = (lay["wk"] @ h).reshape(w.n_kv_heads, w.head_dim)
             v = (lay["wv"] @ h).reshape(w.n_kv_heads, w.head_dim)
+            if "q_norm" in lay:
+                q = rmsnorm(q, lay["q_norm"], w.rms_eps)
+                k = rmsnorm(k, lay["k_norm"], w.rms_eps)
             q = rope(q, p, w.rope_base)
             k = rope(k, p, w.rope_base)
             state["k"][li] = np.concatenate([state["k"][li], k[None]], axis=0)
@@ -181,6 +188,9 @@ def recompute_logits(weights: ModelWeights, tokens: Sequence[int]) -> np.ndarray
         q = (h @ lay["wq"].T).reshape(n, w.n_q_heads, w.head_dim)
         k = (h @ lay["wk"].T).reshape(n, w.n_kv_heads, w.head_dim)
         v = (h @ lay["wv"].T).reshape(n, w.n_kv_heads, w.head_dim)
+        if "q_norm" in lay:
+            q = rmsnorm(q, lay["q_norm"], w.rms_eps)
+            k = rmsnorm(k, lay["k_norm"], w.rms_eps)
         q = rope(q, pos, w.rope_base)
         k = rope(k, pos, w.rope_base)
         o = np.empty_like(q)

@@ -9,6 +9,7 @@
 * planted mistakes: each plausible bug in the oracle must break a pin.
 """
 
+import dataclasses
 import os
 
 import numpy as np
@@ -17,7 +18,7 @@ import torch
 
 import oracle
 from oracle import decoder as od
-from workload import PAGE_TOKENS, ModelShape, TINY, make_weights, random_tokens
+from workload import PAGE_TOKENS, ModelShape, TINY, TINY_QK, make_weights, random_tokens
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "closed_forms.txt")
 
@@ -198,6 +199,55 @@ def _close_to_hf(got, ref):
     return np.max(np.abs(got - ref)) <= 2e-5 * np.max(np.abs(ref))
 
 
+def _hf_qwen3_logits(shape, arrays, tokens):
+    """Logits from transformers' Qwen3 (per-head q/k RMSNorm) with the same weights."""
+    from transformers import Qwen3Config, Qwen3ForCausalLM
+    cfg = Qwen3Config(vocab_size=shape.vocab, hidden_size=shape.d_model,
+                      intermediate_size=shape.ffn_dim, num_hidden_layers=shape.n_layers,
+                      num_attention_heads=shape.n_q_heads, num_key_value_heads=shape.n_kv_heads,
+                      head_dim=shape.head_dim, rms_norm_eps=shape.rms_eps,
+                      rope_theta=shape.rope_base, tie_word_embeddings=False,
+                      attention_bias=False, max_position_embeddings=4096,
+                      use_sliding_window=False)
+    torch.manual_seed(0)
+    m = Qwen3ForCausalLM(cfg).double().eval()
+    t = lambda a: torch.from_numpy(np.asarray(a, dtype=np.float64))
+    with torch.no_grad():
+        m.model.embed_tokens.weight.copy_(t(arrays["embed"]))
+        m.lm_head.weight.copy_(t(arrays["lm_head"]))
+        m.model.norm.weight.copy_(t(arrays["final_norm"]))
+        for lay, hl in zip(arrays["layers"], m.model.layers):
+            hl.self_attn.q_proj.weight.copy_(t(lay["wq"]))
+            hl.self_attn.k_proj.weight.copy_(t(lay["wk"]))
+            hl.self_attn.v_proj.weight.copy_(t(lay["wv"]))
+            hl.self_attn.o_proj.weight.copy_(t(lay["wo"]))
+            hl.self_attn.q_norm.weight.copy_(t(lay["q_norm"]))
+            hl.self_attn.k_norm.weight.copy_(t(lay["k_norm"]))
+            hl.mlp.gate_proj.weight.copy_(t(lay["w_gate"]))
+            hl.mlp.up_proj.weight.copy_(t(lay["w_up"]))
+            hl.mlp.down_proj.weight.copy_(t(lay["w_down"]))
+            hl.input_layernorm.weight.copy_(t(lay["attn_norm"]))
+            hl.post_attention_layernorm.weight.copy_(t(lay["ffn_norm"]))
+        out = m(torch.tensor([list(map(int, tokens))])).logits[0].numpy()
+    return out
+
+
+@pytest.mark.parametrize("shape", [dataclasses.replace(SMALL, qk_norm=True), TINY_QK])
+def test_decoder_matches_transformers_qwen3(shape):
+    arrays = _hf_arrays(shape, seed=13)
+    rng = np.random.default_rng(14)
+    for lay in arrays["layers"]:  # q/k gains well away from 1
+        lay["q_norm"] = (1 + 0.3 * rng.standard_normal(shape.head_dim)).astype(np.float32)
+        lay["k_norm"] = (1 + 0.3 * rng.standard_normal(shape.head_dim)).astype(np.float32)
+    tokens = random_tokens(23, shape.vocab, seed=15)
+    ref = _hf_qwen3_logits(shape, arrays, tokens)
+    got = _oracle_all_logits(shape, arrays, tokens)
+    assert _close_to_hf(got, ref), np.max(np.abs(got - ref))
+    # and the cached decoder equals its own recomputation
+    full = od.recompute_logits(od.ModelWeights.from_arrays(shape, arrays), tokens)
+    np.testing.assert_allclose(got, full, rtol=0, atol=1e-10 * np.max(np.abs(full)))
+
+
 @pytest.mark.parametrize("shape", [SMALL, TINY])
 def test_decoder_matches_transformers_llama(shape):
     arrays = _hf_arrays(shape, seed=11)
@@ -293,3 +343,37 @@ def test_planted_mistake_breaks_library_pin(monkeypatch, name, attr, mutant):
     monkeypatch.setattr(od, attr, mutant)
     got = _oracle_all_logits(SMALL, arrays, tokens)
     assert not _close_to_hf(got, ref), name
+
+
+_RMSNORM = od.rmsnorm
+
+
+def _mut_qk_norm_whole_vector(x, gain, eps):
+    """Per-head norm done over all heads of q (or k) at once."""
+    if x.ndim >= 2 and gain.shape[-1] != x.shape[-1] * x.shape[-2]:
+        flat = x.reshape(*x.shape[:-2], -1)
+        ms = np.mean(flat * flat, axis=-1, keepdims=True)[..., None]
+        return x / np.sqrt(ms + eps) * gain
+    return _RMSNORM(x, gain, eps)
+
+
+def _qwen3_case():
+    shape = dataclasses.replace(SMALL, qk_norm=True)
+    arrays = _hf_arrays(shape, seed=13)
+    rng = np.random.default_rng(14)
+    for lay in arrays["layers"]:
+        lay["q_norm"] = (1 + 0.3 * rng.standard_normal(shape.head_dim)).astype(np.float32)
+        lay["k_norm"] = (1 + 0.3 * rng.standard_normal(shape.head_dim)).astype(np.float32)
+    tokens = random_tokens(23, shape.vocab, seed=15)
+    return shape, arrays, tokens
+
+
+def test_planted_qk_norm_mistakes_break_qwen3_pin(monkeypatch):
+    shape, arrays, tokens = _qwen3_case()
+    ref = _hf_qwen3_logits(shape, arrays, tokens)
+    with monkeypatch.context() as mp:
+        mp.setattr(od, "rmsnorm", _mut_qk_norm_whole_vector)
+        assert not _close_to_hf(_oracle_all_logits(shape, arrays, tokens), ref)
+    swapped = {**arrays, "layers": [{**lay, "q_norm": lay["k_norm"], "k_norm": lay["q_norm"]}
+                                    for lay in arrays["layers"]]}
+    assert not _close_to_hf(_oracle_all_logits(shape, swapped, tokens), ref)

@@ -36,6 +36,8 @@ class ModelShape:
     vocab: int
     rms_eps: float = 1e-6
     rope_base: float = 10000.0
+    # Qwen3-style per-head RMSNorm of q and k (over head_dim) before RoPE.
+    qk_norm: bool = False
 
     @property
     def q_dim(self) -> int:
@@ -56,6 +58,9 @@ EIGHT_B = ModelShape(n_layers=32, d_model=4096, n_q_heads=32, n_kv_heads=8, head
 # small enough for a float64 oracle to run in seconds.
 SMALL_BF16 = ModelShape(n_layers=2, d_model=512, n_q_heads=8, n_kv_heads=2, head_dim=128,
                         ffn_dim=1408, vocab=2048)
+# The same two with Qwen3-style q/k norm.
+TINY_QK = dataclasses.replace(TINY, qk_norm=True)
+SMALL_BF16_QK = dataclasses.replace(SMALL_BF16, qk_norm=True)
 
 
 def round_to_bf16(x: np.ndarray) -> np.ndarray:
@@ -81,7 +86,9 @@ def make_weights(shape: ModelShape, seed: int = 0, bf16: bool = False,
     """Seeded random weights in the nn.Linear ``[out, in]`` layout.
 
     Every matrix is drawn N(0, std) in the fixed order: embedding, then per
-    layer q, k, v, o, gate, up, down, then the LM head.  Norm gains are 1.0.
+    layer q, k, v, o, gate, up, down, then the LM head.  Norm gains are 1.0,
+    except that a shape with q/k norm then draws per-layer q and k gains
+    1 + 0.1 N(0, 1) (so that the gains are exercised), after everything else.
     With ``bf16`` the float32 draws are rounded to bf16 (RNE); both sides
     then use exactly the same representable values.
     """
@@ -108,6 +115,10 @@ def make_weights(shape: ModelShape, seed: int = 0, bf16: bool = False,
         weights["layers"].append(layer)
     weights["lm_head"] = draw(s.vocab, s.d_model)
     weights["final_norm"] = np.ones(s.d_model, dtype=np.float32)
+    if s.qk_norm:
+        for layer in weights["layers"]:
+            for name in ("q_norm", "k_norm"):
+                layer[name] = (1.0 + 0.1 * rng.standard_normal(s.head_dim)).astype(np.float32)
     return weights
 
 
