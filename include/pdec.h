@@ -69,6 +69,9 @@ typedef struct pdec_model_cfg {
   float rms_eps;
   float rope_base;
   int32_t dtype;     /* PDEC_F32 or PDEC_BF16 */
+  int32_t qk_norm;   /* 1: per-head RMSNorm of q and k over head_dim before RoPE,
+                        with gains weights->q_norm / k_norm (the Qwen3 family's
+                        attention; the paper's models are Qwen3); 0: none */
 } pdec_model_cfg;
 
 /* Device pointers to the weights, stored in cfg->dtype except the norm gains
@@ -92,6 +95,8 @@ typedef struct pdec_weights {
   const void* const* w_gate;     /* n_layers x [ffn_dim][d_model] */
   const void* const* w_up;       /* n_layers x [ffn_dim][d_model] */
   const void* const* w_down;     /* n_layers x [d_model][ffn_dim] */
+  const float* const* q_norm;    /* n_layers x [head_dim]; only with cfg->qk_norm */
+  const float* const* k_norm;    /* n_layers x [head_dim]; only with cfg->qk_norm */
 } pdec_weights;
 
 typedef struct pdec_engine pdec_engine;

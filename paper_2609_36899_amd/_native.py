@@ -40,7 +40,7 @@ class ModelCfg(ctypes.Structure):
     _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("n_q_heads", c_int32),
                 ("n_kv_heads", c_int32), ("head_dim", c_int32), ("ffn_dim", c_int32),
                 ("vocab", c_int32), ("rms_eps", c_float), ("rope_base", c_float),
-                ("dtype", c_int32)]
+                ("dtype", c_int32), ("qk_norm", c_int32)]
 
 
 class Weights(ctypes.Structure):
@@ -48,7 +48,8 @@ class Weights(ctypes.Structure):
                 ("attn_norm", POINTER(c_void_p)), ("wq", POINTER(c_void_p)),
                 ("wk", POINTER(c_void_p)), ("wv", POINTER(c_void_p)), ("wo", POINTER(c_void_p)),
                 ("ffn_norm", POINTER(c_void_p)), ("w_gate", POINTER(c_void_p)),
-                ("w_up", POINTER(c_void_p)), ("w_down", POINTER(c_void_p))]
+                ("w_up", POINTER(c_void_p)), ("w_down", POINTER(c_void_p)),
+                ("q_norm", POINTER(c_void_p)), ("k_norm", POINTER(c_void_p))]
 
 
 # name -> (restype, argtypes)

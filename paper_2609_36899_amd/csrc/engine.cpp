@@ -217,6 +217,7 @@ int check_cfg(const pdec_model_cfg* c) {
   if (16 % G != 0) return fail(PDEC_UNSUPPORTED, "GQA group size must divide 16");
   if (c->head_dim != 64 && c->head_dim != 128)
     return fail(PDEC_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (c->qk_norm != 0 && c->qk_norm != 1) return fail(PDEC_INVALID_ARG, "qk_norm must be 0 or 1");
   if (c->dtype == PDEC_BF16 && (c->d_model % 64 || c->ffn_dim % 64))
     return fail(PDEC_UNSUPPORTED, "bf16 path needs d_model and ffn_dim multiples of 64");
   return PDEC_OK;
@@ -291,7 +292,7 @@ struct pdec_engine {
   const void* embed = nullptr;
   const void* lm_head = nullptr;
   const float* final_norm = nullptr;
-  std::vector<const float*> attn_norm, ffn_norm;
+  std::vector<const float*> attn_norm, ffn_norm, q_norm, k_norm;
   std::vector<WSegs> w_qkv, w_o, w_gu, w_down;
 
   char* kv_pool = nullptr;
@@ -389,7 +390,9 @@ int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
     HIP_OR_FAIL(E->timer.end(s));
     HIP_OR_FAIL(launch_qkv_rope_kv(dt, M, Dh, c.n_q_heads, c.n_kv_heads, E->part, S, d_rows,
                                    E->rope_cs, E->bt, E->ws.bt_stride, E->q, E->k_layer(l),
-                                   E->v_layer(l), E->page_stride, s));
+                                   E->v_layer(l), E->page_stride,
+                                   c.qk_norm ? E->q_norm[l] : nullptr,
+                                   c.qk_norm ? E->k_norm[l] : nullptr, c.rms_eps, s));
     HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_ATTENTION, s));
     HIP_OR_FAIL(launch_attention_split(dt, Dh, rows_per_item, n_items, c.n_q_heads, c.n_kv_heads,
                                        d_it, d_qb,
@@ -471,6 +474,12 @@ int engine_create(const pdec_model_cfg* cfg, const pdec_weights* w, void* kv_poo
     if (!w->attn_norm[l] || !w->wq[l] || !w->wk[l] || !w->wv[l] || !w->wo[l] ||
         !w->ffn_norm[l] || !w->w_gate[l] || !w->w_up[l] || !w->w_down[l])
       return fail(PDEC_INVALID_ARG, "null weight pointer in layer " + std::to_string(l));
+  if (cfg->qk_norm) {
+    if (!w->q_norm || !w->k_norm) return fail(PDEC_INVALID_ARG, "qk_norm needs q_norm/k_norm");
+    for (int l = 0; l < cfg->n_layers; ++l)
+      if (!w->q_norm[l] || !w->k_norm[l])
+        return fail(PDEC_INVALID_ARG, "null q/k norm gain in layer " + std::to_string(l));
+  }
   const int64_t page_bytes = kv_token_bytes(cfg) * kPage;
   const int64_t n_pages = kv_pool_bytes / page_bytes;
   if (n_pages < 1 || n_pages > INT32_MAX)
@@ -489,6 +498,8 @@ int engine_create(const pdec_model_cfg* cfg, const pdec_weights* w, void* kv_poo
   for (int l = 0; l < cfg->n_layers; ++l) {
     E->attn_norm.push_back(w->attn_norm[l]);
     E->ffn_norm.push_back(w->ffn_norm[l]);
+    E->q_norm.push_back(cfg->qk_norm ? w->q_norm[l] : nullptr);
+    E->k_norm.push_back(cfg->qk_norm ? w->k_norm[l] : nullptr);
     WSegs a{};
     a.ptr[0] = w->wq[l];
     a.ptr[1] = w->wk[l];

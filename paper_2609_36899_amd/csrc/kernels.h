@@ -69,6 +69,7 @@ hipError_t launch_qkv_rope_kv(int dtype, int M, int head_dim, int n_q_heads, int
                               const float* part, int splits, const RowMeta* rows,
                               const float2* rope_cs, const int32_t* block_table, int32_t bt_stride,
                               void* q_out, void* k_pages, void* v_pages, int64_t page_stride_elems,
+                              const float* q_gain, const float* k_gain, float eps,
                               hipStream_t stream);
 // u[m][n] = silu(g) * up with g, up the summed partials of columns n and F+n.
 hipError_t launch_swiglu(int dtype, int M, int F, const float* part, int splits, void* u,

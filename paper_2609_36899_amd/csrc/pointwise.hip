@@ -86,14 +86,17 @@ __global__ __launch_bounds__(1024) void resid_norm_kernel(
 
 // A row is handled by gridDim.y work groups.  Pairs (i, i + Dh/2) of every q and k head are
 // rotated by the table angle of the row's position, four pairs per thread;
-// v is copied.  K goes to [page][g][slot][Dh], V to the transposed block
+// v is copied.  With q/k gains (the Qwen3 family's per-head norm), each q and
+// k head is first RMS-normalised over Dh: the Dh/8 threads of a head are
+// consecutive, aligned lanes, and reduce their sum of squares by shuffles.  K goes to [page][g][slot][Dh], V to the transposed block
 // [page][g][Dh][slot].
 template <typename T>
 __global__ __launch_bounds__(kRowThreads) void qkv_rope_kv_kernel(
     int M, int head_dim, int n_q_heads, int n_kv_heads, const float* __restrict__ part,
     int splits, const RowMeta* __restrict__ rows, const float2* __restrict__ rope_cs,
     const int32_t* __restrict__ bt, int32_t bt_stride, T* __restrict__ q_out,
-    T* __restrict__ kpool, T* __restrict__ vpool, int64_t page_stride) {
+    T* __restrict__ kpool, T* __restrict__ vpool, int64_t page_stride,
+    const float* __restrict__ q_gain, const float* __restrict__ k_gain, float eps) {
   const int row = blockIdx.x;
   const RowMeta rm = rows[row];
   const int half = head_dim / 2;
@@ -118,6 +121,18 @@ __global__ __launch_bounds__(kRowThreads) void qkv_rope_kv_kernel(
       const float4 b2 = *(const float4*)(pr + s * slab + c1);
       a.x += a2.x; a.y += a2.y; a.z += a2.z; a.w += a2.w;
       b.x += b2.x; b.y += b2.y; b.z += b2.z; b.w += b2.w;
+    }
+    if (q_gain) {
+      // All quads_per_head lanes of this head run this iteration together
+      // (heads are whole, aligned lane groups and n_quads is a multiple).
+      float ss = a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w + b.x * b.x + b.y * b.y +
+                 b.z * b.z + b.w * b.w;
+      for (int off = quads_per_head / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
+      const float r = rsqrtf(ss / (float)head_dim + eps);
+      const float* gn = hh < n_q_heads ? q_gain : k_gain;
+      const float4 ga = *(const float4*)(gn + i), gb = *(const float4*)(gn + i + half);
+      a = make_float4(a.x * r * ga.x, a.y * r * ga.y, a.z * r * ga.z, a.w * r * ga.w);
+      b = make_float4(b.x * r * gb.x, b.y * r * gb.y, b.z * r * gb.z, b.w * r * gb.w);
     }
     const float4 t01 = *(const float4*)(cs + i), t23 = *(const float4*)(cs + i + 2);
     const float4 ra = make_float4(a.x * t01.x - b.x * t01.y, a.y * t01.z - b.y * t01.w,
@@ -271,6 +286,7 @@ hipError_t launch_qkv_rope_kv(int dtype, int M, int head_dim, int n_q_heads, int
                               const float* part, int splits, const RowMeta* rows,
                               const float2* rope_cs, const int32_t* block_table, int32_t bt_stride,
                               void* q_out, void* k_pages, void* v_pages, int64_t page_stride_elems,
+                              const float* q_gain, const float* k_gain, float eps,
                               hipStream_t stream) {
   if (M == 0) return hipSuccess;
   // Enough groups per row that small batches still fill the GPU.
@@ -278,11 +294,13 @@ hipError_t launch_qkv_rope_kv(int dtype, int M, int head_dim, int n_q_heads, int
   if (dtype == 1)
     qkv_rope_kv_kernel<uint16_t><<<grid, kRowThreads, 0, stream>>>(
         M, head_dim, n_q_heads, n_kv_heads, part, splits, rows, rope_cs, block_table, bt_stride,
-        (uint16_t*)q_out, (uint16_t*)k_pages, (uint16_t*)v_pages, page_stride_elems);
+        (uint16_t*)q_out, (uint16_t*)k_pages, (uint16_t*)v_pages, page_stride_elems,
+        q_gain, k_gain, eps);
   else
     qkv_rope_kv_kernel<float><<<grid, kRowThreads, 0, stream>>>(
         M, head_dim, n_q_heads, n_kv_heads, part, splits, rows, rope_cs, block_table, bt_stride,
-        (float*)q_out, (float*)k_pages, (float*)v_pages, page_stride_elems);
+        (float*)q_out, (float*)k_pages, (float*)v_pages, page_stride_elems, q_gain,
+        k_gain, eps);
   return hipGetLastError();
 }
 

@@ -34,7 +34,7 @@ def model_cfg(shape, dtype: int) -> N.ModelCfg:
     """C struct for a shape object exposing the ModelCfg field names."""
     return N.ModelCfg(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads,
                       shape.head_dim, shape.ffn_dim, shape.vocab, float(shape.rms_eps),
-                      float(shape.rope_base), dtype)
+                      float(shape.rope_base), dtype, int(bool(getattr(shape, "qk_norm", False))))
 
 
 def kv_bytes_per_token(shape, dtype: int) -> int:
@@ -87,8 +87,9 @@ def weights_to_device(arrays: Dict, dtype: int, device="cuda") -> Dict:
            "final_norm": vec(arrays["final_norm"]), "layers": []}
     for lay in arrays["layers"]:
         d = {k: pack_weight(mat(lay[k])) for k in PROJECTIONS}
-        d["attn_norm"] = vec(lay["attn_norm"])
-        d["ffn_norm"] = vec(lay["ffn_norm"])
+        for k in ("attn_norm", "ffn_norm", "q_norm", "k_norm"):
+            if k in lay:
+                d[k] = vec(lay[k])
         out["layers"].append(d)
     return out
 
@@ -120,7 +121,10 @@ class Engine:
 
         self._keep = []
         fields = {}
-        for key in ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down"):
+        keys = ["attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down"]
+        if self.cfg.qk_norm:
+            keys += ["q_norm", "k_norm"]
+        for key in keys:
             p, a = arr(key)
             self._keep.append(a)
             fields[key] = p

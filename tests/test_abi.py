@@ -59,6 +59,10 @@ def test_host_only_calls_without_gpu():
     odd = N.ModelCfg(2, 256, 4, 2, 96, 688, 1024, 1e-6, 1e4, N.F32)
     assert lib.kv_bytes_per_token(byref(odd)) == N.UNSUPPORTED
     assert lib.paged_attention_workspace_bytes(64, 32, 8, 128, 0) > 0
+    qk = N.ModelCfg(2, 256, 4, 2, 64, 688, 1024, 1e-6, 1e4, N.F32, 1)
+    assert lib.kv_bytes_per_token(byref(qk)) == 2048
+    qk.qk_norm = 2
+    assert lib.kv_bytes_per_token(byref(qk)) == N.INVALID_ARG
     # packed weight sizes: bf16 pads N to whole 16-column strips, fp32 is row-major
     assert lib.packed_weight_bytes(N.BF16, 100, 128) == 112 * 128 * 2
     assert lib.packed_weight_bytes(N.BF16, 128256, 4096) == 128256 * 4096 * 2

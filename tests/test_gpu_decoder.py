@@ -6,6 +6,7 @@ float64 oracle, through the C ABI.
   tokens; 33 logit rows per trajectory within 1e-4 absolute;
 * bf16 decoders (small, and the 8B layer geometry with 2 layers): per-row
   normwise 2e-2;
+* the Qwen3-style per-head q/k norm variant, fp32 (Dh 64) and bf16 (Dh 128);
 * chunking, re-prefill after departure, batch-order invariance and atomic
   failure of page growth.
 """
@@ -16,7 +17,8 @@ import torch
 
 import oracle
 from oracle import decoder as od
-from workload import (EIGHT_B, SMALL_BF16, TINY, ModelShape, make_weights, random_tokens)
+from workload import (EIGHT_B, SMALL_BF16, SMALL_BF16_QK, TINY, TINY_QK, ModelShape,
+                      make_weights, random_tokens)
 
 pytestmark = pytest.mark.gpu
 
@@ -201,6 +203,44 @@ def test_bf16_8b_geometry_two_layers_parity():
                        n_kv_heads=EIGHT_B.n_kv_heads, head_dim=EIGHT_B.head_dim,
                        ffn_dim=EIGHT_B.ffn_dim, vocab=4096)
     _bf16_parity(shape, seed=6, prefix_lens=[9, 33, 48, 20], n_steps=4, chunk=32)
+
+
+def test_qk_norm_bf16_parity():
+    _bf16_parity(SMALL_BF16_QK, seed=8, prefix_lens=[7, 45, 64], n_steps=6, chunk=16)
+
+
+def test_qk_norm_fp32_parity():
+    shape = TINY_QK
+    arrays = make_weights(shape, seed=9)
+    assert "q_norm" in arrays["layers"][0]
+    w64 = od.ModelWeights.from_arrays(shape, arrays)
+    E = _engine(shape, arrays, bf16=False)
+    prefix_lens, n_steps = [17, 40, 96], 8
+    toks = [random_tokens(n + n_steps, shape.vocab, seed=900 + i)
+            for i, n in enumerate(prefix_lens)]
+    seqs, gpu = [], [[] for _ in prefix_lens]
+    buf = _logits_buf(1, shape.vocab)
+    for i, n in enumerate(prefix_lens):
+        s = E.kv_alloc(0)
+        E.kv_append_prefix(s, toks[i][:n], chunk_tokens=32, last_logits=buf)
+        gpu[i].append(buf[0].cpu().numpy().copy())
+        seqs.append(s)
+    logits = _logits_buf(len(seqs), shape.vocab)
+    for k in range(n_steps):
+        step_tok = np.array([t[n + k] for t, n in zip(toks, prefix_lens)], dtype=np.int32)
+        E.decode_step(seqs, torch.from_numpy(step_tok).cuda(), logits)
+        got = logits.cpu().numpy()
+        for i in range(len(seqs)):
+            gpu[i].append(got[i].copy())
+    for i, n in enumerate(prefix_lens):
+        ref = od.recompute_logits(w64, toks[i])[n - 1:]
+        err = np.max(np.abs(np.stack(gpu[i]) - ref))
+        assert err <= F32_TOL, (i, err)
+    # the norm is really applied: the same weights without q/k gains differ
+    plain = {**arrays, "layers": [{k: v for k, v in lay.items() if k not in ("q_norm", "k_norm")}
+                                  for lay in arrays["layers"]]}
+    ref_plain = od.recompute_logits(od.ModelWeights.from_arrays(TINY, plain), toks[0])
+    assert np.max(np.abs(ref_plain[prefix_lens[0] - 1:] - np.stack(gpu[0]))) > 100 * F32_TOL
 
 
 def test_page_growth_failure_is_atomic():
