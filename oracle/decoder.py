@@ -34,14 +34,19 @@ definition):
     no soft-cap, window or ALiBi.
   * A prefix occupies positions 0..n-1, and the first decode step after it is
     at position n.
+  * fp8 KV variant (``kv_fp8=(k_scale, v_scale)``): the cache holds k and v as
+    e4m3 codes (oracle/fp8.py), so attention reads value(code) * scale for
+    every cached position, the current one included.
 """
 
 from __future__ import annotations
 
 import dataclasses
-from typing import List, Optional, Sequence
+from typing import List, Optional, Sequence, Tuple
 
 import numpy as np
+
+from .fp8 import quantize_dequantize
 
 
 @dataclasses.dataclass
@@ -128,8 +133,9 @@ def greedy(logits: np.ndarray) -> np.ndarray:
 class Decoder:
     """Incremental decoder with a contiguous per-trajectory KV cache."""
 
-    def __init__(self, weights: ModelWeights):
+    def __init__(self, weights: ModelWeights, kv_fp8: Optional[Tuple[float, float]] = None):
         self.w = weights
+        self.kv_fp8 = kv_fp8
 
     def new_state(self) -> dict:
         w = self.w
@@ -154,6 +160,9 @@ class Decoder:
                 k = rmsnorm(k, lay["k_norm"], w.rms_eps)
             q = rope(q, p, w.rope_base)
             k = rope(k, p, w.rope_base)
+            if self.kv_fp8 is not None:
+                k = quantize_dequantize(k, self.kv_fp8[0])
+                v = quantize_dequantize(v, self.kv_fp8[1])
             state["k"][li] = np.concatenate([state["k"][li], k[None]], axis=0)
             state["v"][li] = np.concatenate([state["v"][li], v[None]], axis=0)
             o = attention(q, state["k"][li], state["v"][li])
@@ -171,7 +180,8 @@ class Decoder:
         return logits
 
 
-def recompute_logits(weights: ModelWeights, tokens: Sequence[int]) -> np.ndarray:
+def recompute_logits(weights: ModelWeights, tokens: Sequence[int],
+                     kv_fp8: Optional[Tuple[float, float]] = None) -> np.ndarray:
     """Logits at every position of ``tokens``, recomputed without any KV cache.
 
     Full causal attention over the whole sequence with dense matrices; this is
@@ -193,6 +203,9 @@ def recompute_logits(weights: ModelWeights, tokens: Sequence[int]) -> np.ndarray
             k = rmsnorm(k, lay["k_norm"], w.rms_eps)
         q = rope(q, pos, w.rope_base)
         k = rope(k, pos, w.rope_base)
+        if kv_fp8 is not None:
+            k = quantize_dequantize(k, kv_fp8[0])
+            v = quantize_dequantize(v, kv_fp8[1])
         o = np.empty_like(q)
         for hh in range(w.n_q_heads):
             g = hh // group
