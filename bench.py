@@ -46,6 +46,9 @@ WORKLOADS = {
     "decode-8b-b256-pareto": (256, ("pareto", 1.5, 1024, 65536)),
     "decode-8b-b512-pareto": (512, ("pareto", 1.5, 1024, 65536)),
 }
+# The same workloads with KV pages stored as fp8 (E4M3) codes, scales 1.
+FP8_KV = {f"{name}-fp8kv": name for name in ("decode-8b-b256-lognormal", "decode-8b-b8-long",
+                                               "decode-8b-b16-pareto", "decode-8b-b64-pareto")}
 DEFAULT_WORKLOAD = "decode-8b-b256-lognormal"
 # Multi-turn rollouts: decode segments of 128 steps separated by tool-output
 # appends of U[512, 2048] tokens per trajectory through kv_append_prefix.
@@ -203,6 +206,7 @@ def cpu_baseline(shape, lens, budget_s=15.0, seed=7):
 # ---------------------------------------------------------------------------
 
 def run_decode(workload, steps, warmup, with_cpu):
+    """One decode workload; names in FP8_KV run the same batch with fp8 KV pages."""
     import torch
 
     import paper_2609_36899_amd as P
@@ -210,24 +214,36 @@ def run_decode(workload, steps, warmup, with_cpu):
     from workload import EIGHT_B
 
     shape = EIGHT_B
-    batch, spec = WORKLOADS[workload]
+    kv_fp8 = (1.0, 1.0) if workload in FP8_KV else None
+    batch, spec = WORKLOADS[FP8_KV.get(workload, workload)]
     lens = draw_lengths(batch, spec)
     grow = warmup + steps + min(steps, 8) + 1  # warmup, timed and breakdown steps
     pages = int(np.sum((lens + grow + 15) // 16)) + 64
-    per_tok = P.kv_bytes_per_token(shape, P.BF16)
+    per_tok = P.kv_bytes_per_token(shape, P.BF16, kv_fp8)
     pool_bytes = pages * 16 * per_tok
     log(f"{workload}: B={batch}, mean context {lens.mean():.0f}, pool {pool_bytes / 2**30:.1f} GiB")
 
     torch.cuda.set_device(0)
     weights = gpu_weights(shape)
     E = P.Engine(shape, weights, P.BF16, pool_bytes, max_seqs=batch,
-                 max_seq_len=int(lens.max()) + grow + 16, max_batch=batch, max_chunk=16)
+                 max_seq_len=int(lens.max()) + grow + 16, max_batch=batch, max_chunk=16,
+                 kv_fp8=kv_fp8)
     g = torch.Generator(device="cuda")
     g.manual_seed(3)
-    pool_bf16 = E.kv_pool.view(torch.bfloat16)
     chunk = 1 << 30
-    for i in range(0, pool_bf16.numel(), chunk):
-        pool_bf16[i:i + chunk].normal_(0.0, 1.0, generator=g)
+    if kv_fp8 is None:
+        pool = E.kv_pool.view(torch.bfloat16)
+        for i in range(0, pool.numel(), chunk):
+            pool[i:i + chunk].normal_(0.0, 1.0, generator=g)
+    else:  # finite E4M3 codes sign | e << 3 | m with e in 4..9 (|x| in 2^-3 .. 2^2.9)
+        pool = E.kv_pool
+        for i in range(0, pool.numel(), chunk):
+            n = min(chunk, pool.numel() - i)
+            sign = torch.randint(0, 2, (n,), dtype=torch.uint8, device="cuda", generator=g)
+            e = torch.randint(4, 10, (n,), dtype=torch.uint8, device="cuda", generator=g)
+            m = torch.randint(0, 8, (n,), dtype=torch.uint8, device="cuda", generator=g)
+            pool[i:i + n] = (sign << 7) | (e << 3) | m
+            del sign, e, m
     ids = np.array([E.kv_alloc(0) for _ in range(batch)], dtype=np.int32)
     for sid, n in zip(ids, lens):
         E.kv_extend_uninit(int(sid), int(n))
@@ -281,7 +297,8 @@ def run_decode(workload, steps, warmup, with_cpu):
     logit_bytes = 2 * batch * shape.vocab * 4  # LM-head write + argmax read
     step_bytes = kv_read + kv_write + w_bytes + logit_bytes
     hbm = step_bytes / (ms_step / 1e3) / 1e9
-    attn_bytes = mean_keys * shape.n_kv_heads * shape.head_dim * 2 * 2  # per layer launch
+    kv_elem = 1 if kv_fp8 is not None else 2
+    attn_bytes = mean_keys * shape.n_kv_heads * shape.head_dim * 2 * kv_elem  # per layer launch
     attn_avg_ms = attn_ms / max(attn_n, 1)
     attn_gbs = attn_bytes / (attn_avg_ms / 1e3) / 1e9
     src = os.path.join(ROOT, "paper_2609_36899_amd", "csrc", "attention.hip")
@@ -295,19 +312,21 @@ def run_decode(workload, steps, warmup, with_cpu):
                    "Dh 128, FFN 14336, vocab 128256), random init",
                    "batch": int(batch), "context_mean": round(float(lens.mean()), 1),
                    "context_min": int(lens.min()), "context_max": int(lens.max()),
-                   "length_distribution": list(spec), "page_tokens": 16},
+                   "length_distribution": list(spec), "page_tokens": 16,
+                   "kv_pages": "fp8 e4m3, scales 1" if kv_fp8 is not None else "bf16"},
         "hbm_gbps": round(hbm, 1), "hbm_frac_of_peak": round(hbm / HBM_PEAK_GBS, 4),
         "step_bytes": int(step_bytes), "wall_s": round(wall, 3),
         "breakdown_ms_per_step": {"attention": round(attn_ms / steps, 3),
                                   "projections": round(gemm_ms / bsteps, 3),
                                   "lm_head": round(lm_ms / bsteps, 3)},
-        "roofline": {"kernel": "attn_split_bf16<128>", "bound": "hbm",
+        "roofline": {"kernel": "attn_split_bf16<128>" + (" (fp8 pages)" if kv_fp8 else ""),
+                     "bound": "hbm",
                      "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "bytes_per_launch": int(attn_bytes),
                      "avg_launch_ms": round(attn_avg_ms, 5), "launches": int(attn_n)},
     }
-    del E, weights, logits, pool_bf16
+    del E, weights, logits, pool
     torch.cuda.empty_cache()
     if with_cpu:
         log("timing the CPU oracle on a bounded sample")
@@ -568,6 +587,21 @@ def gpu_weights_f32_tiny(shape):
             "final_norm": ones(), "layers": layers}
 
 
+def run_copy_calibration(n=1 << 30):
+    """One device copy of n bytes (torch copy_): the reference kernel whose
+    FETCH_SIZE / WRITE_SIZE counters calibrate the HBM traffic figures."""
+    import torch
+    torch.cuda.set_device(0)
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    return {"metric": "device copy for counter calibration", "value": n, "unit": "bytes",
+            "n_gpus": 1, "config": {"workload": "copy-1gib"}, "cpu_baseline": None}
+
+
 PROJ_SHAPES = [("qkv", 6144, 4096), ("o", 4096, 4096), ("gate_up", 28672, 4096),
                ("down", 4096, 14336), ("lm_head", 128256, 4096)]
 
@@ -711,8 +745,9 @@ def main():
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
-                    choices=sorted(WORKLOADS) + sorted(MULTITURN)
-                    + ["kv-transfer-8b", "projections-8b", "landscape-8b", "sampling-8b"])
+                    choices=sorted(WORKLOADS) + sorted(FP8_KV) + sorted(MULTITURN)
+                    + ["kv-transfer-8b", "projections-8b", "landscape-8b", "sampling-8b",
+                       "copy-1gib"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -728,6 +763,8 @@ def main():
         out = run_landscape()
     elif args.workload == "sampling-8b":
         out = run_sampling()
+    elif args.workload == "copy-1gib":
+        out = run_copy_calibration()
     elif args.workload in MULTITURN:
         out = run_multiturn(args.workload, segments=3, seg_steps=args.steps, warmup=args.warmup)
     else:

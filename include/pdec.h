@@ -53,6 +53,14 @@ extern "C" {
  * cores. */
 #define PDEC_F32 0
 #define PDEC_BF16 1
+/* KV page storage only (pdec_model_cfg.kv_fp8, paged_decode_attention_fp8):
+ * OCP 8-bit E4M3FN codes (sign, 4 exponent bits with bias 7, 3 mantissa
+ * bits; subnormals m * 2^-9; largest finite 448; no infinities), written with
+ * round-to-nearest-even, saturation at +-448 and the sign kept, and read back
+ * as value(code) * scale.  Halves the bytes each decode step streams per
+ * cached token (Background, "Hardware-Workload Interaction": long-context
+ * decode is bound by KV traffic). */
+#define PDEC_FP8_E4M3 2
 
 /* Llama-style pre-norm decoder: RMSNorm, rotary position embedding
  * (rotate-half pairing), grouped-query attention with contiguous groups
@@ -72,6 +80,10 @@ typedef struct pdec_model_cfg {
   int32_t qk_norm;   /* 1: per-head RMSNorm of q and k over head_dim before RoPE,
                         with gains weights->q_norm / k_norm (the Qwen3 family's
                         attention; the paper's models are Qwen3); 0: none */
+  int32_t kv_fp8;    /* 1: KV pages hold PDEC_FP8_E4M3 codes of k / kv_scale_k and
+                        v / kv_scale_v (bf16 path only); 0: pages in dtype */
+  float kv_scale_k;  /* > 0, used when kv_fp8 */
+  float kv_scale_v;
 } pdec_model_cfg;
 
 /* Device pointers to the weights, stored in cfg->dtype except the norm gains
@@ -332,6 +344,18 @@ int paged_decode_attention(int32_t dtype, int32_t batch, int32_t n_q_heads, int3
                            const void* v_pages, const int32_t* block_table_dev, int32_t bt_stride,
                            const int32_t* lens_host, float* out, void* workspace,
                            int64_t workspace_bytes, void* stream);
+
+/* The same with PDEC_FP8_E4M3 pages: q is bf16 [batch][n_q_heads][head_dim];
+ * k_pages / v_pages hold codes in the page layout above (one byte per
+ * element) that read back as value(code) * k_scale and value(code) * v_scale.
+ * Errors as paged_decode_attention, and PDEC_INVALID_ARG for scales that are
+ * not positive and finite. */
+int paged_decode_attention_fp8(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                               int32_t head_dim, const void* q, const void* k_pages,
+                               const void* v_pages, float k_scale, float v_scale,
+                               const int32_t* block_table_dev, int32_t bt_stride,
+                               const int32_t* lens_host, float* out, void* workspace,
+                               int64_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -5,7 +5,7 @@ this package only builds it (``build``) and marshals torch tensors into its
 calls (``engine``).
 """
 
-from ._native import PAGE_TOKENS, PdecError, BF16, F32  # noqa: F401
+from ._native import PAGE_TOKENS, PdecError, BF16, F32, FP8_E4M3  # noqa: F401
 
 
 def __getattr__(name):
@@ -14,7 +14,8 @@ def __getattr__(name):
     if name in ("Engine", "paged_decode_attention", "paged_attention_workspace_bytes",
                 "kv_bytes_per_token", "weights_to_device", "model_cfg", "weight_projection",
                 "weight_projection_workspace_bytes", "pack_weight",
-                "PackedWeight", "sample_top_p"):
+                "PackedWeight", "sample_top_p",
+                "paged_decode_attention_fp8"):
         from . import engine
         return getattr(engine, name)
     raise AttributeError(name)

@@ -24,6 +24,7 @@ PAGE_TOKENS = 16
 TIMER_ATTENTION, TIMER_GEMM, TIMER_LM_HEAD = 0, 1, 2
 F32 = 0
 BF16 = 1
+FP8_E4M3 = 2
 
 _CODE_NAMES = {INVALID_ARG: "INVALID_ARG", OUT_OF_PAGES: "OUT_OF_PAGES", BAD_SEQ: "BAD_SEQ",
                SEQ_TOO_LONG: "SEQ_TOO_LONG", HIP_ERROR: "HIP_ERROR",
@@ -40,7 +41,8 @@ class ModelCfg(ctypes.Structure):
     _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("n_q_heads", c_int32),
                 ("n_kv_heads", c_int32), ("head_dim", c_int32), ("ffn_dim", c_int32),
                 ("vocab", c_int32), ("rms_eps", c_float), ("rope_base", c_float),
-                ("dtype", c_int32), ("qk_norm", c_int32)]
+                ("dtype", c_int32), ("qk_norm", c_int32), ("kv_fp8", c_int32),
+                ("kv_scale_k", c_float), ("kv_scale_v", c_float)]
 
 
 class Weights(ctypes.Structure):
@@ -89,6 +91,10 @@ SIGNATURES = {
     "paged_decode_attention": (c_int32, [c_int32, c_int32, c_int32, c_int32, c_int32, c_void_p,
                                          c_void_p, c_void_p, c_void_p, c_int32, POINTER(c_int32),
                                          c_void_p, c_void_p, c_int64, c_void_p]),
+    "paged_decode_attention_fp8": (c_int32, [c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
+                                             c_void_p, c_float, c_float, c_void_p, c_int32,
+                                             POINTER(c_int32), c_void_p, c_void_p, c_int64,
+                                             c_void_p]),
 }
 
 _lib = None

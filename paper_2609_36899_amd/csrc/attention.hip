@@ -15,7 +15,7 @@
 // query row; that keeps every softmax statistic lane-private and lets the
 // score registers feed the P operand of O^T = V^T P^T without any shuffle.
 // V pages are stored transposed ([Dh][16]) so each lane's V^T operand is one
-// contiguous 16-byte load.
+// contiguous 16-byte load (8 bytes with fp8 pages).
 #include "hip_common.h"
 #include "kernels.h"
 
@@ -24,6 +24,15 @@ namespace pdec {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+// Eight consecutive K or V elements as a bf16 MFMA fragment.  fp8 pages are
+// read as 8 bytes (half the traffic) and decoded in registers; the decode is
+// exact, so both products still run on bf16 MFMAs.
+template <typename KT>
+__device__ __forceinline__ bf16x8 load_kv8(const KT* p) {
+  if constexpr (sizeof(KT) == 2) return load_stream<bf16x8>(p);
+  else return e4m3x8_to_bf16(load_stream<u32x2>(p));
+}
 
 // ---------------------------------------------------------------------------
 // bf16, MFMA.  One wave per work group.  Lane l: c16 = l % 16, q4 = l / 16.
@@ -41,18 +50,37 @@ constexpr float kLog2e = 1.4426950408889634f;
 // take interleaved page pairs of the item for the same 16 rows and are merged
 // through LDS at the end, so one item (and one partial) covers PW times the
 // pages a single wave streams.
-template <int DH, int RW, int PW>
-__global__ __launch_bounds__(64 * RW * PW) __attribute__((amdgpu_waves_per_eu(3))) void attn_split_bf16(
+//
+// KT is the KV page element: uint16_t (bf16) or uint8_t (fp8 E4M3 codes,
+// load_kv8).  The K scale is folded into scale_log2 by the host and the V
+// scale multiplies the partial output.
+template <int DH, int RW, int PW, typename KT>
+__global__ __launch_bounds__(64 * RW * PW)
+__attribute__((amdgpu_waves_per_eu(sizeof(KT) == 1 ? 2 : 3))) void attn_split_bf16(
     const AttnItem* __restrict__ items, const AttnQBlock* __restrict__ qblocks,
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
-    const uint16_t* __restrict__ vpool, int64_t page_stride, const int32_t* __restrict__ bt,
-    int32_t bt_stride, int32_t n_q_heads, int32_t n_kv_heads, float scale_log2,
+    const uint16_t* __restrict__ q, const KT* __restrict__ kpool,
+    const KT* __restrict__ vpool, int64_t page_stride, const int32_t* __restrict__ bt,
+    int32_t bt_stride, int32_t n_q_heads, int32_t n_kv_heads, float scale_log2, float v_scale,
     float* __restrict__ part_ml, float* __restrict__ part_acc) {
   constexpr int KC = DH / 32;  // k-steps of QK^T
   constexpr int DT = DH / 16;  // 16-wide dim tiles of PV
   constexpr int R = 16 * RW;  // query rows per item
+  // Head dims of k-step c for lane group q4 in the Q K^T product (any
+  // permutation works if Q and K share it).  bf16: chunk q4 of 32-dim block c,
+  // so a load instruction covers 64 contiguous bytes of each key row.  fp8:
+  // lane group q4 owns the contiguous span [q4 * DH/4, (q4 + 1) * DH/4), so a
+  // 16-byte load covers two k-steps and again 64 bytes per key row.
+  auto qk_dim = [](int c, int q4) {
+    return sizeof(KT) == 1 ? q4 * (DH / 4) + c * 8 : c * 32 + q4 * 8;
+  };
   static_assert(RW == 1 || PW == 1, "waves split either rows or pages");
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  // fp8: the wave index lives in a scalar register, so page-table reads
+  // indexed by it are scalar loads that never wait behind the prefetched page
+  // loads (vector loads complete in order).  The bf16 loop has no prefetch
+  // and measured 1.5% faster with the vector form.
+  const int wave = sizeof(KT) == 1 ? __builtin_amdgcn_readfirstlane(threadIdx.x >> 6)
+                                   : (int)(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   const int rw = wave % RW, pw = wave / RW;
   const int c16 = lane & 15, q4 = lane >> 4;
   // The KV heads of one item are adjacent in the grid, so the work groups in
@@ -73,7 +101,7 @@ __global__ __launch_bounds__(64 * RW * PW) __attribute__((amdgpu_waves_per_eu(3)
   if (row_valid) {
     const uint16_t* qrow = q + ((int64_t)(qb.q_row0 + jq) * n_q_heads + head) * DH;
 #pragma unroll
-    for (int c = 0; c < KC; ++c) qf[c] = *(const bf16x8*)(qrow + c * 32 + q4 * 8);
+    for (int c = 0; c < KC; ++c) qf[c] = *(const bf16x8*)(qrow + qk_dim(c, q4));
   } else {
 #pragma unroll
     for (int c = 0; c < KC; ++c) qf[c] = bf16x8{};
@@ -103,26 +131,37 @@ __global__ __launch_bounds__(64 * RW * PW) __attribute__((amdgpu_waves_per_eu(3)
   for (int t = 0; t < DT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int n_iter = (it.n_pages + 1) >> 1;
-  for (int iter = pw; iter < n_iter; iter += PW) {
+  constexpr bool kFp8 = sizeof(KT) == 1;
+  // This lane's K and V fragment bases of page pair `iter`.
+  auto pair_bases = [&](int iter, const KT*& kb, const KT*& vb) {
     const int pi = 2 * iter;
     const int page0 = btrow[pi];
     const int page1 = (pi + 1 < it.n_pages) ? btrow[pi + 1] : page0;
     const int64_t base0 = (int64_t)page0 * page_stride + head_off;
     const int64_t base1 = (int64_t)page1 * page_stride + head_off;
-
-    // K: 2 tiles x KC loads of 16 B; V: DT loads of 16 B.
-    const uint16_t* kb = kpool + (k_page_sel ? base1 : base0);
-    bf16x8 kf[2][KC];
+    kb = kpool + (k_page_sel ? base1 : base0);
+    vb = vpool + (v_page_sel ? base1 : base0) + v_tok0;
+  };
+  // fp8 pages: the raw codes of the wave's next page pair are loaded one
+  // iteration ahead (the index is clamped to the last pair: the final
+  // prefetch re-reads it).  A lane's K dims are one contiguous span, so each
+  // 16-byte load holds two k-steps.
+  u32x4 kr[2][KC / 2];
+  u32x2 vr[DT];
+  auto load_raw = [&](int iter, u32x4(&k)[2][KC / 2], u32x2(&v)[DT]) {
+    const KT *kb, *vb;
+    pair_bases(iter, kb, vb);
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int c = 0; c < KC; ++c)
-        kf[u][c] = load_stream<bf16x8>(kb + (k_tok + 4 * u) * DH + c * 32 + q4 * 8);
-    const uint16_t* vb = vpool + (v_page_sel ? base1 : base0) + v_tok0;
-    u16x8 vf[DT];
+      for (int j = 0; j < KC / 2; ++j)
+        k[u][j] = load_stream<u32x4>(kb + (k_tok + 4 * u) * DH + qk_dim(2 * j, q4));
 #pragma unroll
-    for (int t = 0; t < DT; ++t) vf[t] = load_stream<u16x8>(vb + (t * 16 + c16) * kPage);
-
+    for (int t = 0; t < DT; ++t) v[t] = load_stream<u32x2>(vb + (t * 16 + c16) * kPage);
+  };
+  // One page pair: scores, online softmax and the PV product.
+  auto step = [&](int iter, const bf16x8(&kf)[2][KC], u16x8(&vf)[DT]) {
+    const int pi = 2 * iter;
     f32x4 s[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
@@ -171,7 +210,7 @@ __global__ __launch_bounds__(64 * RW * PW) __attribute__((amdgpu_waves_per_eu(3)
     }
     u16x8 pbits = __builtin_bit_cast(u16x8, u32x4{pw4[0], pw4[1], pw4[2], pw4[3]});
 
-    if (key0 + (pi + 2) * kPage > kv_lim) {  // wave-uniform: the block's last keys
+    if (__builtin_expect(key0 + (pi + 2) * kPage > kv_lim, 0)) {  // wave-uniform: the block's last keys
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         if (kbase + e >= kv_lim)
@@ -184,6 +223,61 @@ __global__ __launch_bounds__(64 * RW * PW) __attribute__((amdgpu_waves_per_eu(3)
     for (int t = 0; t < DT; ++t)
       acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[t]), pf,
                                                        acc[t], 0, 0, 0);
+  };
+  if constexpr (kFp8) {
+    // Two raw buffers in turn: while one pair is decoded and used, the
+    // wave's next pair streams into the other (no register copies, which
+    // would wait for the loads).
+    u32x4 kr2[2][KC / 2];
+    u32x2 vr2[DT];
+    auto decode = [&](const u32x4(&k)[2][KC / 2], const u32x2(&v)[DT], bf16x8(&kf)[2][KC],
+                      u16x8(&vf)[DT]) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int j = 0; j < KC / 2; ++j) {
+          kf[u][2 * j] = e4m3x8_to_bf16(u32x2{k[u][j].x, k[u][j].y});
+          kf[u][2 * j + 1] = e4m3x8_to_bf16(u32x2{k[u][j].z, k[u][j].w});
+        }
+#pragma unroll
+      for (int t = 0; t < DT; ++t) vf[t] = __builtin_bit_cast(u16x8, e4m3x8_to_bf16(v[t]));
+    };
+    if (pw < n_iter) load_raw(pw, kr, vr);
+    for (int iter = pw; iter < n_iter; iter += 2 * PW) {
+      bf16x8 kf[2][KC];
+      u16x8 vf[DT];
+      load_raw(min(iter + PW, n_iter - 1), kr2, vr2);
+      __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the decode's waits
+      decode(kr, vr, kf, vf);
+      step(iter, kf, vf);
+      if (iter + PW >= n_iter) break;  // wave-uniform
+      load_raw(min(iter + 2 * PW, n_iter - 1), kr, vr);
+      __builtin_amdgcn_sched_barrier(0);
+      decode(kr2, vr2, kf, vf);
+      step(iter + PW, kf, vf);
+    }
+  } else {
+    for (int iter = pw; iter < n_iter; iter += PW) {
+      // K: 2 tiles x KC fragments of 16 B; V: DT fragments of 16 B.
+      const int pi = 2 * iter;
+      const int page0 = btrow[pi];
+      const int page1 = (pi + 1 < it.n_pages) ? btrow[pi + 1] : page0;
+      const int64_t base0 = (int64_t)page0 * page_stride + head_off;
+      const int64_t base1 = (int64_t)page1 * page_stride + head_off;
+      const KT* kb = kpool + (k_page_sel ? base1 : base0);
+      bf16x8 kf[2][KC];
+      u16x8 vf[DT];
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int c = 0; c < KC; ++c)
+          kf[u][c] = load_kv8(kb + (k_tok + 4 * u) * DH + qk_dim(c, q4));
+      const KT* vb = vpool + (v_page_sel ? base1 : base0) + v_tok0;
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+        vf[t] = __builtin_bit_cast(u16x8, load_kv8(vb + (t * 16 + c16) * kPage));
+      step(iter, kf, vf);
+    }
   }
 
   l += __shfl_xor(l, 16, 64);
@@ -225,7 +319,10 @@ __global__ __launch_bounds__(64 * RW * PW) __attribute__((amdgpu_waves_per_eu(3)
     }
     float* pa = part_acc + prow * DH;
 #pragma unroll
-    for (int t = 0; t < DT; ++t) *(f32x4*)(pa + t * 16 + 4 * q4) = acc[t];
+    for (int t = 0; t < DT; ++t) {
+      if constexpr (sizeof(KT) == 1) acc[t] *= v_scale;
+      *(f32x4*)(pa + t * 16 + 4 * q4) = acc[t];
+    }
   }
 }
 
@@ -372,7 +469,8 @@ __global__ __launch_bounds__(256) void attn_combine(const AttnQBlock* __restrict
 
 }  // namespace
 
-hipError_t launch_attention_split(int dtype, int head_dim, int rows_per_item, int n_items,
+hipError_t launch_attention_split(int dtype, int kv_fp8, float k_scale, float v_scale,
+                                  int head_dim, int rows_per_item, int n_items,
                                   int n_q_heads, int n_kv_heads, const AttnItem* items,
                                   const AttnQBlock* qblocks, const void* q, const void* k_pages,
                                   const void* v_pages, int64_t page_stride_elems,
@@ -380,21 +478,27 @@ hipError_t launch_attention_split(int dtype, int head_dim, int rows_per_item, in
                                   float* part_acc, hipStream_t stream) {
   if (n_items == 0) return hipSuccess;
   const dim3 grid(n_kv_heads, n_items);
-  const float scale_log2 = kLog2e / sqrtf((float)head_dim);
+  const float scale_log2 = kLog2e / sqrtf((float)head_dim) * (kv_fp8 ? k_scale : 1.f);
   if (dtype == 1) {
-    const uint16_t *qq = (const uint16_t*)q, *kk = (const uint16_t*)k_pages,
-                   *vv = (const uint16_t*)v_pages;
-#define PDEC_ATTN_BF16(DH_, RW_, PW_)                                                        \
-  attn_split_bf16<DH_, RW_, PW_><<<grid, dim3(64 * RW_ * PW_), 0, stream>>>(                \
-      items, qblocks, qq, kk, vv, page_stride_elems, block_table, bt_stride, n_q_heads,     \
-      n_kv_heads, scale_log2, part_ml, part_acc)
+    const uint16_t* qq = (const uint16_t*)q;
+#define PDEC_ATTN_BF16(DH_, RW_, PW_, KT_)                                                   \
+  attn_split_bf16<DH_, RW_, PW_, KT_><<<grid, dim3(64 * RW_ * PW_), 0, stream>>>(           \
+      items, qblocks, qq, (const KT_*)k_pages, (const KT_*)v_pages, page_stride_elems,       \
+      block_table, bt_stride, n_q_heads, n_kv_heads, scale_log2, v_scale, part_ml, part_acc)
+#define PDEC_ATTN_KT(KT_)                                                                    \
+  if (head_dim == 128) {                                                                     \
+    if (rows_per_item == 64) PDEC_ATTN_BF16(128, 4, 1, KT_); else PDEC_ATTN_BF16(128, 1, 4, KT_); \
+  } else {                                                                                   \
+    if (rows_per_item == 64) PDEC_ATTN_BF16(64, 4, 1, KT_); else PDEC_ATTN_BF16(64, 1, 4, KT_); \
+  }
     // 64-row items (prefill): waves split rows.  16-row items (decode): waves
     // split pages.
-    if (head_dim == 128) {
-      if (rows_per_item == 64) PDEC_ATTN_BF16(128, 4, 1); else PDEC_ATTN_BF16(128, 1, 4);
+    if (kv_fp8) {
+      PDEC_ATTN_KT(uint8_t)
     } else {
-      if (rows_per_item == 64) PDEC_ATTN_BF16(64, 4, 1); else PDEC_ATTN_BF16(64, 1, 4);
+      PDEC_ATTN_KT(uint16_t)
     }
+#undef PDEC_ATTN_KT
 #undef PDEC_ATTN_BF16
   } else {
     if (head_dim == 128)

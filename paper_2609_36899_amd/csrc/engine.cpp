@@ -42,6 +42,7 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 int64_t elem_bytes(int32_t dtype) { return dtype == PDEC_BF16 ? 2 : 4; }
+int64_t kv_elem_bytes(const pdec_model_cfg* c) { return c->kv_fp8 ? 1 : elem_bytes(c->dtype); }
 
 // ---------------------------------------------------------------------------
 // Pinned staging ring for host-to-device metadata copies.
@@ -218,13 +219,20 @@ int check_cfg(const pdec_model_cfg* c) {
   if (c->head_dim != 64 && c->head_dim != 128)
     return fail(PDEC_UNSUPPORTED, "head_dim must be 64 or 128");
   if (c->qk_norm != 0 && c->qk_norm != 1) return fail(PDEC_INVALID_ARG, "qk_norm must be 0 or 1");
+  if (c->kv_fp8 != 0 && c->kv_fp8 != 1) return fail(PDEC_INVALID_ARG, "kv_fp8 must be 0 or 1");
+  if (c->kv_fp8) {
+    if (c->dtype != PDEC_BF16) return fail(PDEC_UNSUPPORTED, "fp8 KV pages need the bf16 path");
+    if (!(c->kv_scale_k > 0.f) || !(c->kv_scale_v > 0.f) || !std::isfinite(c->kv_scale_k) ||
+        !std::isfinite(c->kv_scale_v))
+      return fail(PDEC_INVALID_ARG, "fp8 KV scales must be positive and finite");
+  }
   if (c->dtype == PDEC_BF16 && (c->d_model % 64 || c->ffn_dim % 64))
     return fail(PDEC_UNSUPPORTED, "bf16 path needs d_model and ffn_dim multiples of 64");
   return PDEC_OK;
 }
 
 int64_t kv_token_bytes(const pdec_model_cfg* c) {
-  return (int64_t)c->n_layers * 2 * c->n_kv_heads * c->head_dim * elem_bytes(c->dtype);
+  return (int64_t)c->n_layers * 2 * c->n_kv_heads * c->head_dim * kv_elem_bytes(c);
 }
 
 size_t part_elems_for(const pdec_model_cfg* c, int64_t rows_cap) {
@@ -321,9 +329,10 @@ struct pdec_engine {
   int32_t epoch = 0;
 
   int64_t ab() const { return elem_bytes(cfg.dtype); }
-  char* k_layer(int l) const { return kv_pool + (int64_t)(2 * l) * n_pages * page_stride * ab(); }
+  int64_t kvb() const { return kv_elem_bytes(&cfg); }
+  char* k_layer(int l) const { return kv_pool + (int64_t)(2 * l) * n_pages * page_stride * kvb(); }
   char* v_layer(int l) const {
-    return kv_pool + (int64_t)(2 * l + 1) * n_pages * page_stride * ab();
+    return kv_pool + (int64_t)(2 * l + 1) * n_pages * page_stride * kvb();
   }
 };
 
@@ -388,13 +397,15 @@ int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
     HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_GEMM, s));
     HIP_OR_FAIL(launch_gemm(dt, M, nqkv, d, E->h, d, E->w_qkv[l], E->part, S, ks, s));
     HIP_OR_FAIL(E->timer.end(s));
-    HIP_OR_FAIL(launch_qkv_rope_kv(dt, M, Dh, c.n_q_heads, c.n_kv_heads, E->part, S, d_rows,
+    HIP_OR_FAIL(launch_qkv_rope_kv(dt, c.kv_fp8, c.kv_scale_k, c.kv_scale_v, M, Dh, c.n_q_heads,
+                                   c.n_kv_heads, E->part, S, d_rows,
                                    E->rope_cs, E->bt, E->ws.bt_stride, E->q, E->k_layer(l),
                                    E->v_layer(l), E->page_stride,
                                    c.qk_norm ? E->q_norm[l] : nullptr,
                                    c.qk_norm ? E->k_norm[l] : nullptr, c.rms_eps, s));
     HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_ATTENTION, s));
-    HIP_OR_FAIL(launch_attention_split(dt, Dh, rows_per_item, n_items, c.n_q_heads, c.n_kv_heads,
+    HIP_OR_FAIL(launch_attention_split(dt, c.kv_fp8, c.kv_scale_k, c.kv_scale_v, Dh, rows_per_item,
+                                       n_items, c.n_q_heads, c.n_kv_heads,
                                        d_it, d_qb,
                                        E->q, E->k_layer(l), E->v_layer(l), E->page_stride, E->bt,
                                        E->ws.bt_stride, E->att_ml, E->att_acc, s));
@@ -745,7 +756,7 @@ int enqueue_page_copy(pdec_engine* E, const std::vector<int32_t>& pages, int n_p
   int rc = flush_deltas(E);
   if (rc != PDEC_OK) return rc;
   HIP_OR_FAIL(E->staging.upload(E->delta, pages.data(), (size_t)n_pages * 4, E->stream));
-  const int64_t block_bytes = E->page_stride * E->ab();
+  const int64_t block_bytes = E->page_stride * E->kvb();
   HIP_OR_FAIL(launch_kv_page_copy(n_pages, (const int32_t*)E->delta, E->cfg.n_layers, E->n_pages,
                                   block_bytes, E->kv_pool, host_dev, to_host, E->stream));
   return PDEC_OK;
@@ -878,13 +889,15 @@ int64_t paged_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_
                    align_up(items_cap * n_kv_heads * 16 * (int64_t)head_dim * 4));
 }
 
-int paged_decode_attention(int32_t dtype, int32_t B, int32_t Hq, int32_t Hkv, int32_t Dh,
-                           const void* q, const void* k_pages, const void* v_pages,
-                           const int32_t* bt, int32_t bt_stride, const int32_t* lens,
-                           float* out, void* workspace, int64_t ws_bytes, void* stream) {
+// kv_dtype: PDEC_F32 (fp32 q and pages), PDEC_BF16 (bf16 q and pages) or
+// PDEC_FP8_E4M3 (bf16 q, E4M3 pages with scales).
+static int paged_attention_impl(int32_t kv_dtype, float k_scale, float v_scale, int32_t B,
+                                int32_t Hq, int32_t Hkv, int32_t Dh, const void* q,
+                                const void* k_pages, const void* v_pages, const int32_t* bt,
+                                int32_t bt_stride, const int32_t* lens, float* out,
+                                void* workspace, int64_t ws_bytes, void* stream) {
   if (!q || !k_pages || !v_pages || !bt || !lens || !out || !workspace)
     return fail(PDEC_INVALID_ARG, "null argument");
-  if (dtype != PDEC_F32 && dtype != PDEC_BF16) return fail(PDEC_INVALID_ARG, "bad dtype");
   if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || bt_stride < 1)
     return fail(PDEC_INVALID_ARG, "bad sizes");
   if (16 % (Hq / Hkv)) return fail(PDEC_UNSUPPORTED, "GQA group size must divide 16");
@@ -926,7 +939,9 @@ int paged_decode_attention(int32_t dtype, int32_t B, int32_t Hq, int32_t Hkv, in
     HIP_OR_FAIL(g_attn_staging->upload(base, hm.data(), o_ml, s));
   }
   const int64_t page_stride = (int64_t)Hkv * kPage * Dh;
-  HIP_OR_FAIL(launch_attention_split(dtype, Dh, kDecodeRows, (int)items.size(), Hq, Hkv,
+  HIP_OR_FAIL(launch_attention_split(kv_dtype == PDEC_F32 ? PDEC_F32 : PDEC_BF16,
+                                     kv_dtype == PDEC_FP8_E4M3, k_scale, v_scale, Dh, kDecodeRows,
+                                     (int)items.size(), Hq, Hkv,
                                      (const AttnItem*)(base + o_it),
                                      (const AttnQBlock*)(base + o_qb), q, k_pages, v_pages,
                                      page_stride, bt, bt_stride, (float*)(base + o_ml),
@@ -935,6 +950,26 @@ int paged_decode_attention(int32_t dtype, int32_t B, int32_t Hq, int32_t Hkv, in
                                        (const AttnQBlock*)(base + o_qb),
                                        (float*)(base + o_ml), (float*)(base + o_acc), out, 0, s));
   return PDEC_OK;
+}
+
+int paged_decode_attention(int32_t dtype, int32_t B, int32_t Hq, int32_t Hkv, int32_t Dh,
+                           const void* q, const void* k_pages, const void* v_pages,
+                           const int32_t* bt, int32_t bt_stride, const int32_t* lens,
+                           float* out, void* workspace, int64_t ws_bytes, void* stream) {
+  if (dtype != PDEC_F32 && dtype != PDEC_BF16) return fail(PDEC_INVALID_ARG, "bad dtype");
+  return paged_attention_impl(dtype, 1.f, 1.f, B, Hq, Hkv, Dh, q, k_pages, v_pages, bt,
+                              bt_stride, lens, out, workspace, ws_bytes, stream);
+}
+
+int paged_decode_attention_fp8(int32_t B, int32_t Hq, int32_t Hkv, int32_t Dh, const void* q,
+                               const void* k_pages, const void* v_pages, float k_scale,
+                               float v_scale, const int32_t* bt, int32_t bt_stride,
+                               const int32_t* lens, float* out, void* workspace,
+                               int64_t ws_bytes, void* stream) {
+  if (!(k_scale > 0.f) || !(v_scale > 0.f) || !std::isfinite(k_scale) || !std::isfinite(v_scale))
+    return fail(PDEC_INVALID_ARG, "scales must be positive and finite");
+  return paged_attention_impl(PDEC_FP8_E4M3, k_scale, v_scale, B, Hq, Hkv, Dh, q, k_pages,
+                              v_pages, bt, bt_stride, lens, out, workspace, ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -10,6 +10,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
@@ -17,8 +18,12 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 // tiles): the non-temporal hint keeps them from displacing reused lines.
 template <typename V>
 __device__ __forceinline__ V load_stream(const void* p) {
-  const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
-  return __builtin_bit_cast(V, v);
+  static_assert(sizeof(V) == 16 || sizeof(V) == 8, "16- or 8-byte loads");
+  if constexpr (sizeof(V) == 16) {
+    return __builtin_bit_cast(V, __builtin_nontemporal_load((const u32x4*)p));
+  } else {
+    return __builtin_bit_cast(V, __builtin_nontemporal_load((const u32x2*)p));
+  }
 }
 
 // bf16 storage is handled as raw 16-bit patterns.
@@ -69,6 +74,36 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   float t = 0.f;
   for (int i = 0; i < nw; ++i) t += red[i];
   return t;
+}
+
+// ---- fp8 (OCP E4M3FN) KV codes -------------------------------------------
+// sign, 4 exponent bits (bias 7), 3 mantissa bits; subnormals m * 2^-9;
+// largest finite 448; S.1111.111 is NaN (never produced here).
+// Round to nearest, ties to even, saturating at +-448; the sign is kept on
+// values that round to zero.  Exact integer steps on the float's bits.
+__device__ __forceinline__ uint32_t e4m3_from_f32(float x) {
+  const uint32_t b = __float_as_uint(x);
+  const uint32_t sign = (b >> 24) & 0x80u;
+  const float a = fabsf(x);
+  if (!(a < 448.f)) return sign | 0x7Eu;  // saturate (NaN inputs too)
+  if (a < 0x1p-6f) return sign | (uint32_t)rintf(a * 512.f);  // subnormal step 2^-9; 8 -> 0x08
+  const uint32_t mant = b & 0x7FFFFFu;
+  const uint32_t r = mant + 0x7FFFFu + ((mant >> 20) & 1u);  // RNE to 3 mantissa bits
+  const int e = (int)((b >> 23) & 0xFFu) - 127 + (int)(r >> 23);
+  return sign | ((uint32_t)(e + 7) << 3) | ((r >> 20) & 7u);
+}
+
+// Eight codes (two dwords, code i in byte i) to eight bf16 values: the
+// hardware fp8 -> f32 conversion, then f32 -> bf16, both exact (every e4m3
+// value is a bf16 value).
+__device__ __forceinline__ bf16x8 e4m3x8_to_bf16(u32x2 w) {
+  const f32x2 a = __builtin_amdgcn_cvt_pk_f32_fp8((int)w.x, false);
+  const f32x2 b = __builtin_amdgcn_cvt_pk_f32_fp8((int)w.x, true);
+  const f32x2 c = __builtin_amdgcn_cvt_pk_f32_fp8((int)w.y, false);
+  const f32x2 d = __builtin_amdgcn_cvt_pk_f32_fp8((int)w.y, true);
+  const bf16x2 pa = __builtin_convertvector(a, bf16x2), pb = __builtin_convertvector(b, bf16x2);
+  const bf16x2 pc = __builtin_convertvector(c, bf16x2), pd = __builtin_convertvector(d, bf16x2);
+  return bf16x8{pa[0], pa[1], pb[0], pb[1], pc[0], pc[1], pd[0], pd[1]};
 }
 
 }  // namespace pdec

@@ -23,7 +23,9 @@ struct WSegs {
 // waves (rows_per_item = 16 or 64).  Writes per-row partial softmax
 // statistics part_ml [items][Hkv][rows_per_item][2] = (max in log2 units,
 // sum) and unnormalised outputs part_acc [items][Hkv][rows_per_item][head_dim].
-hipError_t launch_attention_split(int dtype, int head_dim, int rows_per_item, int n_items,
+// kv_fp8: K/V pages hold E4M3 codes read back as code * k_scale / v_scale.
+hipError_t launch_attention_split(int dtype, int kv_fp8, float k_scale, float v_scale,
+                                  int head_dim, int rows_per_item, int n_items,
                                   int n_q_heads,
                                   int n_kv_heads, const AttnItem* items,
                                   const AttnQBlock* qblocks, const void* q, const void* k_pages,
@@ -65,10 +67,11 @@ hipError_t launch_resid_norm(int dtype, int M, int d, const float* part, int spl
 // Sum the q|k|v partials, rotate q and k at each row's position (cos/sin
 // table [pos][head_dim/2] of float2), write q to q_out [M][Hq][Dh] and k, v
 // into the row's page slot of this layer's pool.
-hipError_t launch_qkv_rope_kv(int dtype, int M, int head_dim, int n_q_heads, int n_kv_heads,
-                              const float* part, int splits, const RowMeta* rows,
-                              const float2* rope_cs, const int32_t* block_table, int32_t bt_stride,
-                              void* q_out, void* k_pages, void* v_pages, int64_t page_stride_elems,
+hipError_t launch_qkv_rope_kv(int dtype, int kv_fp8, float k_scale, float v_scale, int M,
+                              int head_dim, int n_q_heads, int n_kv_heads, const float* part,
+                              int splits, const RowMeta* rows, const float2* rope_cs,
+                              const int32_t* block_table, int32_t bt_stride, void* q_out,
+                              void* k_pages, void* v_pages, int64_t page_stride_elems,
                               const float* q_gain, const float* k_gain, float eps,
                               hipStream_t stream);
 // u[m][n] = silu(g) * up with g, up the summed partials of columns n and F+n.

@@ -51,6 +51,23 @@ struct Pack4<uint16_t> {
   }
 };
 
+// KV page stores: bf16 / fp32 as above; fp8 pages hold E4M3 codes of x / scale.
+template <typename T>
+struct KvStore {
+  static __device__ __forceinline__ void store4(T* p, float4 v, float) { Pack4<T>::store(p, v); }
+  static __device__ __forceinline__ T one(float v, float) { return Store<T>::from(v); }
+};
+template <>
+struct KvStore<uint8_t> {
+  static __device__ __forceinline__ void store4(uint8_t* p, float4 v, float scale) {
+    *(uint32_t*)p = e4m3_from_f32(v.x / scale) | (e4m3_from_f32(v.y / scale) << 8) |
+                    (e4m3_from_f32(v.z / scale) << 16) | (e4m3_from_f32(v.w / scale) << 24);
+  }
+  static __device__ __forceinline__ uint8_t one(float v, float scale) {
+    return (uint8_t)e4m3_from_f32(v / scale);
+  }
+};
+
 // One work group of up to 1024 threads per row, float4 accesses (d % 4 == 0).
 template <typename HT>
 __global__ __launch_bounds__(1024) void resid_norm_kernel(
@@ -86,17 +103,19 @@ __global__ __launch_bounds__(1024) void resid_norm_kernel(
 
 // A row is handled by gridDim.y work groups.  Pairs (i, i + Dh/2) of every q and k head are
 // rotated by the table angle of the row's position, four pairs per thread;
-// v is copied.  With q/k gains (the Qwen3 family's per-head norm), each q and
+// v is copied.  KV pages take the element type KVT (fp8 pages store codes of
+// k / k_scale and v / v_scale).  With q/k gains (the Qwen3 family's per-head norm), each q and
 // k head is first RMS-normalised over Dh: the Dh/8 threads of a head are
 // consecutive, aligned lanes, and reduce their sum of squares by shuffles.  K goes to [page][g][slot][Dh], V to the transposed block
 // [page][g][Dh][slot].
-template <typename T>
+template <typename T, typename KVT>
 __global__ __launch_bounds__(kRowThreads) void qkv_rope_kv_kernel(
     int M, int head_dim, int n_q_heads, int n_kv_heads, const float* __restrict__ part,
     int splits, const RowMeta* __restrict__ rows, const float2* __restrict__ rope_cs,
     const int32_t* __restrict__ bt, int32_t bt_stride, T* __restrict__ q_out,
-    T* __restrict__ kpool, T* __restrict__ vpool, int64_t page_stride,
-    const float* __restrict__ q_gain, const float* __restrict__ k_gain, float eps) {
+    KVT* __restrict__ kpool, KVT* __restrict__ vpool, int64_t page_stride,
+    const float* __restrict__ q_gain, const float* __restrict__ k_gain, float eps,
+    float k_scale, float v_scale) {
   const int row = blockIdx.x;
   const RowMeta rm = rows[row];
   const int half = head_dim / 2;
@@ -139,11 +158,15 @@ __global__ __launch_bounds__(kRowThreads) void qkv_rope_kv_kernel(
                                   a.z * t23.x - b.z * t23.y, a.w * t23.z - b.w * t23.w);
     const float4 rb = make_float4(a.x * t01.y + b.x * t01.x, a.y * t01.w + b.y * t01.z,
                                   a.z * t23.y + b.z * t23.x, a.w * t23.w + b.w * t23.z);
-    T* dst = (hh < n_q_heads)
-                 ? q_out + ((int64_t)row * n_q_heads + hh) * head_dim
-                 : kpool + page_base + ((int64_t)(hh - n_q_heads) * kPage + slot) * head_dim;
-    Pack4<T>::store(dst + i, ra);
-    Pack4<T>::store(dst + i + half, rb);
+    if (hh < n_q_heads) {
+      T* dst = q_out + ((int64_t)row * n_q_heads + hh) * head_dim;
+      Pack4<T>::store(dst + i, ra);
+      Pack4<T>::store(dst + i + half, rb);
+    } else {
+      KVT* dst = kpool + page_base + ((int64_t)(hh - n_q_heads) * kPage + slot) * head_dim;
+      KvStore<KVT>::store4(dst + i, ra, k_scale);
+      KvStore<KVT>::store4(dst + i + half, rb, k_scale);
+    }
   }
   const int vcol0 = (n_q_heads + n_kv_heads) * head_dim;
   for (int idx = part_id * kRowThreads + threadIdx.x; idx < n_kv_heads * head_dim;
@@ -151,7 +174,7 @@ __global__ __launch_bounds__(kRowThreads) void qkv_rope_kv_kernel(
     float v = 0.f;
     for (int s = 0; s < splits; ++s) v += pr[s * slab + vcol0 + idx];
     const int g = idx / head_dim, dd = idx % head_dim;
-    vpool[page_base + ((int64_t)g * head_dim + dd) * kPage + slot] = Store<T>::from(v);
+    vpool[page_base + ((int64_t)g * head_dim + dd) * kPage + slot] = KvStore<KVT>::one(v, v_scale);
   }
 }
 
@@ -282,25 +305,28 @@ hipError_t launch_resid_norm(int dtype, int M, int d, const float* part, int spl
   return hipGetLastError();
 }
 
-hipError_t launch_qkv_rope_kv(int dtype, int M, int head_dim, int n_q_heads, int n_kv_heads,
-                              const float* part, int splits, const RowMeta* rows,
-                              const float2* rope_cs, const int32_t* block_table, int32_t bt_stride,
-                              void* q_out, void* k_pages, void* v_pages, int64_t page_stride_elems,
+hipError_t launch_qkv_rope_kv(int dtype, int kv_fp8, float k_scale, float v_scale, int M,
+                              int head_dim, int n_q_heads, int n_kv_heads, const float* part,
+                              int splits, const RowMeta* rows, const float2* rope_cs,
+                              const int32_t* block_table, int32_t bt_stride, void* q_out,
+                              void* k_pages, void* v_pages, int64_t page_stride_elems,
                               const float* q_gain, const float* k_gain, float eps,
                               hipStream_t stream) {
   if (M == 0) return hipSuccess;
   // Enough groups per row that small batches still fill the GPU.
   const dim3 grid(M, M >= 64 ? 2 : 8);
-  if (dtype == 1)
-    qkv_rope_kv_kernel<uint16_t><<<grid, kRowThreads, 0, stream>>>(
-        M, head_dim, n_q_heads, n_kv_heads, part, splits, rows, rope_cs, block_table, bt_stride,
-        (uint16_t*)q_out, (uint16_t*)k_pages, (uint16_t*)v_pages, page_stride_elems,
-        q_gain, k_gain, eps);
+#define PDEC_QKV(T_, KVT_)                                                                   \
+  qkv_rope_kv_kernel<T_, KVT_><<<grid, kRowThreads, 0, stream>>>(                             \
+      M, head_dim, n_q_heads, n_kv_heads, part, splits, rows, rope_cs, block_table, bt_stride, \
+      (T_*)q_out, (KVT_*)k_pages, (KVT_*)v_pages, page_stride_elems, q_gain, k_gain, eps,     \
+      k_scale, v_scale)
+  if (dtype == 1 && kv_fp8)
+    PDEC_QKV(uint16_t, uint8_t);
+  else if (dtype == 1)
+    PDEC_QKV(uint16_t, uint16_t);
   else
-    qkv_rope_kv_kernel<float><<<grid, kRowThreads, 0, stream>>>(
-        M, head_dim, n_q_heads, n_kv_heads, part, splits, rows, rope_cs, block_table, bt_stride,
-        (float*)q_out, (float*)k_pages, (float*)v_pages, page_stride_elems, q_gain,
-        k_gain, eps);
+    PDEC_QKV(float, float);
+#undef PDEC_QKV
   return hipGetLastError();
 }
 

@@ -30,15 +30,19 @@ def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
     return None if t is None else t.data_ptr()
 
 
-def model_cfg(shape, dtype: int) -> N.ModelCfg:
-    """C struct for a shape object exposing the ModelCfg field names."""
+def model_cfg(shape, dtype: int, kv_fp8: Optional[Sequence[float]] = None) -> N.ModelCfg:
+    """C struct for a shape object exposing the ModelCfg field names.
+
+    ``kv_fp8=(k_scale, v_scale)`` stores the KV pages as E4M3 codes."""
+    ks, vs = (float(kv_fp8[0]), float(kv_fp8[1])) if kv_fp8 is not None else (1.0, 1.0)
     return N.ModelCfg(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads,
                       shape.head_dim, shape.ffn_dim, shape.vocab, float(shape.rms_eps),
-                      float(shape.rope_base), dtype, int(bool(getattr(shape, "qk_norm", False))))
+                      float(shape.rope_base), dtype, int(bool(getattr(shape, "qk_norm", False))),
+                      int(kv_fp8 is not None), ks, vs)
 
 
-def kv_bytes_per_token(shape, dtype: int) -> int:
-    cfg = model_cfg(shape, dtype)
+def kv_bytes_per_token(shape, dtype: int, kv_fp8: Optional[Sequence[float]] = None) -> int:
+    cfg = model_cfg(shape, dtype, kv_fp8)
     return N.check(N.load().kv_bytes_per_token(byref(cfg)))
 
 
@@ -99,11 +103,13 @@ class Engine:
 
     def __init__(self, shape, weights: Dict, dtype: int, kv_pool_bytes: int, max_seqs: int,
                  max_seq_len: int, max_batch: int, max_chunk: int, device="cuda",
-                 stream: Optional[torch.cuda.Stream] = None):
+                 stream: Optional[torch.cuda.Stream] = None,
+                 kv_fp8: Optional[Sequence[float]] = None):
         self.lib = N.load()
         self.shape = shape
         self.dtype = dtype
-        self.cfg = model_cfg(shape, dtype)
+        self.kv_fp8 = kv_fp8
+        self.cfg = model_cfg(shape, dtype, kv_fp8)
         self.weights = weights  # keep the tensors alive
         self.kv_token_bytes = N.check(self.lib.kv_bytes_per_token(byref(self.cfg)))
         page_bytes = self.kv_token_bytes * PAGE_TOKENS
@@ -153,7 +159,7 @@ class Engine:
     # ---- pool views (layout [layer][K|V][page][Hkv][16 * Dh]) -------------
     def _pool_view(self):
         s = self.shape
-        t = self.kv_pool.view(_TORCH_DTYPE[self.dtype])
+        t = self.kv_pool if self.kv_fp8 is not None else self.kv_pool.view(_TORCH_DTYPE[self.dtype])
         return t.view(s.n_layers, 2, self.n_pages, s.n_kv_heads, PAGE_TOKENS * s.head_dim)
 
     def k_pages(self, layer: int) -> torch.Tensor:
@@ -310,6 +316,39 @@ def paged_attention_workspace_bytes(batch: int, n_q_heads: int, n_kv_heads: int,
                                     head_dim: int) -> int:
     return N.check(N.load().paged_attention_workspace_bytes(batch, n_q_heads, n_kv_heads,
                                                             head_dim, 0))
+
+
+def paged_decode_attention_fp8(q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tensor,
+                               k_scale: float, v_scale: float, block_table: torch.Tensor,
+                               lens: Sequence[int], out: torch.Tensor,
+                               workspace: Optional[torch.Tensor] = None,
+                               stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """Isolated paged decode attention over E4M3 code pages (uint8
+    [P][Hkv][16][Dh] and [P][Hkv][Dh][16]) with bf16 q; see include/pdec.h."""
+    B, Hq, Dh = q.shape
+    P, Hkv, page, Dh2 = k_pages.shape
+    assert page == PAGE_TOKENS and Dh2 == Dh and tuple(v_pages.shape) == (P, Hkv, Dh, PAGE_TOKENS)
+    assert q.dtype == torch.bfloat16 and k_pages.dtype == v_pages.dtype == torch.uint8
+    assert q.is_contiguous() and k_pages.is_contiguous() and v_pages.is_contiguous()
+    assert block_table.dtype == torch.int32 and block_table.dim() == 2
+    assert block_table.shape[0] == B and block_table.is_contiguous()
+    assert out.dtype == torch.float32 and tuple(out.shape) == (B, Hq, Dh) and out.is_contiguous()
+    ln = np.ascontiguousarray(np.asarray(lens, dtype=np.int32))
+    assert ln.shape == (B,) and (ln >= 1).all() and (ln <= block_table.shape[1] * PAGE_TOKENS).all()
+    bt = block_table.cpu().numpy()
+    for b in range(B):
+        used = bt[b, :(int(ln[b]) + PAGE_TOKENS - 1) // PAGE_TOKENS]
+        if used.size and (used.min() < 0 or used.max() >= P):
+            raise PdecError(N.INVALID_ARG, f"block table row {b} names a page outside the pool")
+    need = paged_attention_workspace_bytes(B, Hq, Hkv, Dh)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    N.check(N.load().paged_decode_attention_fp8(
+        B, Hq, Hkv, Dh, q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(), float(k_scale),
+        float(v_scale), block_table.data_ptr(), block_table.shape[1],
+        ln.ctypes.data_as(POINTER(c_int32)), out.data_ptr(), workspace.data_ptr(),
+        workspace.numel(), _stream_handle(stream)))
+    return out
 
 
 def paged_decode_attention(q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tensor,

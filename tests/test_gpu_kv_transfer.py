@@ -20,18 +20,19 @@ def _P():
     return P
 
 
-def _engine(shape, bf16, pool_tokens=2048):
+def _engine(shape, bf16, pool_tokens=2048, kv_fp8=None):
     P = _P()
     dt = P.BF16 if bf16 else P.F32
     w = P.weights_to_device(make_weights(shape, seed=7, bf16=bf16), dt)
-    per_tok = P.kv_bytes_per_token(shape, dt)
+    per_tok = P.kv_bytes_per_token(shape, dt, kv_fp8)
     return P.Engine(shape, w, dt, pool_tokens * per_tok, max_seqs=8, max_seq_len=1024,
-                    max_batch=4, max_chunk=32)
+                    max_batch=4, max_chunk=32, kv_fp8=kv_fp8)
 
 
-@pytest.mark.parametrize("shape,bf16", [(TINY, False), (SMALL_BF16, True)])
-def test_snapshot_restore_continues_bitwise(shape, bf16):
-    E = _engine(shape, bf16)
+@pytest.mark.parametrize("shape,bf16,kv_fp8", [(TINY, False, None), (SMALL_BF16, True, None),
+                                               (SMALL_BF16, True, (0.5, 0.5))])
+def test_snapshot_restore_continues_bitwise(shape, bf16, kv_fp8):
+    E = _engine(shape, bf16, kv_fp8=kv_fp8)
     toks = random_tokens(90, shape.vocab, seed=3)
     logits = torch.empty((1, shape.vocab), dtype=torch.float32, device="cuda")
     a = E.kv_alloc(0)

@@ -226,6 +226,62 @@ def paged_attention_case(batch: int, n_q_heads: int, n_kv_heads: int, head_dim: 
 
 
 @dataclasses.dataclass
+class PagedAttentionCaseFp8:
+    """Isolated decode-attention operands with E4M3 code pages (uint8)."""
+
+    q: np.ndarray          # [B, Hq, Dh] float32, bf16-representable
+    k_codes: np.ndarray    # [P, Hkv, 16, Dh] uint8
+    v_codes: np.ndarray    # [P, Hkv, 16, Dh] uint8
+    block_table: np.ndarray
+    lens: np.ndarray
+
+
+def paged_attention_case_fp8(batch: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                             lens: np.ndarray, n_pool_pages: int, seed: int,
+                             exponents=(4, 9), all_codes: bool = False) -> PagedAttentionCaseFp8:
+    """Random E4M3 K/V codes built from their bit fields, and block tables.
+
+    Each code is sign << 7 | e << 3 | m with a random sign, e uniform in
+    ``exponents`` (inclusive; bias 7, so (4, 9) spans about 2^-3 .. 2^2.9) and
+    m uniform in 0..7; with ``all_codes`` every finite code (all but
+    0x7F and 0xFF) is equally likely.  Pages come from one random permutation
+    of the pool as in paged_attention_case, and slots past a sequence's length
+    hold the NaN code 0x7F, which a correct kernel never reads.
+    """
+    rng = np.random.default_rng(seed)
+    lens = np.asarray(lens, dtype=np.int64)
+    npages = (lens + PAGE_TOKENS - 1) // PAGE_TOKENS
+    if int(npages.sum()) > n_pool_pages:
+        raise ValueError("pool too small for the requested lengths")
+    perm = rng.permutation(n_pool_pages).astype(np.int32)
+    bt = np.full((batch, max(int(npages.max()), 1)), -1, dtype=np.int32)
+    cursor = 0
+    for b in range(batch):
+        bt[b, :npages[b]] = perm[cursor:cursor + npages[b]]
+        cursor += int(npages[b])
+    shape = (n_pool_pages, n_kv_heads, PAGE_TOKENS, head_dim)
+
+    def codes():
+        if all_codes:
+            finite = np.array([c for c in range(256) if c not in (0x7F, 0xFF)], dtype=np.uint8)
+            return finite[rng.integers(0, finite.size, size=shape)]
+        sign = rng.integers(0, 2, size=shape, dtype=np.uint8)
+        e = rng.integers(exponents[0], exponents[1] + 1, size=shape, dtype=np.uint8)
+        m = rng.integers(0, 8, size=shape, dtype=np.uint8)
+        return (sign << 7) | (e << 3) | m
+
+    k_codes, v_codes = codes(), codes()
+    q = round_to_bf16(rng.standard_normal((batch, n_q_heads, head_dim), dtype=np.float32))
+    for b in range(batch):
+        tail = int(lens[b] % PAGE_TOKENS)
+        if tail:
+            last = bt[b, npages[b] - 1]
+            k_codes[last, :, tail:, :] = 0x7F
+            v_codes[last, :, tail:, :] = 0x7F
+    return PagedAttentionCaseFp8(q=q, k_codes=k_codes, v_codes=v_codes, block_table=bt, lens=lens)
+
+
+@dataclasses.dataclass
 class LazyPagedAttentionCase:
     """Isolated decode-attention operands for a big pool, drawn per sequence.
 
