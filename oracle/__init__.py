@@ -21,10 +21,11 @@ from .decoder import (Decoder, ModelWeights, attention, greedy, recompute_logits
 from .paged import gather_pages, paged_decode_attention
 from .sampling import nucleus_mask, sample_top_p, token_masses
 from .fp8 import e4m3_decode, e4m3_encode, paged_decode_attention_fp8, quantize_dequantize
+from .pacing import footprint, pacing_plan
 
 __all__ = [
     "Decoder", "ModelWeights", "attention", "greedy", "recompute_logits", "rmsnorm", "rope",
     "silu", "gather_pages", "paged_decode_attention", "nucleus_mask", "sample_top_p",
     "token_masses", "e4m3_decode", "e4m3_encode", "quantize_dequantize",
-    "paged_decode_attention_fp8",
+    "paged_decode_attention_fp8", "footprint", "pacing_plan",
 ]
