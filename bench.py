@@ -602,6 +602,65 @@ def run_copy_calibration(n=1 << 30):
             "n_gpus": 1, "config": {"workload": "copy-1gib"}, "cpu_baseline": None}
 
 
+def run_paced_rollout(n_traj=160, decode=256, max_batch=160, pool_frac=0.5, delta=16):
+    """Headroom-paced rollout (pacing_plan + PacedRollout) on the 8B shape.
+
+    n_traj trajectories with lognormal prompts (median 1024, clamped to
+    [256, 4096]) each decode ``decode`` teacher-forced tokens; the KV pool
+    holds pool_frac of their final KV and at most max_batch reside at once;
+    decode growth outruns the per-resident reserve delta, so the rollout
+    evicts (longest first below the floor) and places (shortest first above
+    the reserve).  New prompts are staged without
+    computing KV, as in the decode workloads; evicted trajectories come back
+    by KV snapshot restore or by re-prefill, one run each.
+    """
+    import torch
+
+    import paper_2609_36899_amd as P
+    from workload import EIGHT_B, lengths_lognormal, random_tokens
+
+    shape = EIGHT_B
+    torch.cuda.set_device(0)
+    weights = gpu_weights(shape)
+    prompts = lengths_lognormal(n_traj, 1024, 0.8, 256, 4096, seed=21)
+    per_tok = P.kv_bytes_per_token(shape, P.BF16)
+    final_tokens = int(np.sum((prompts + decode + 15) // 16 * 16))
+    pool_bytes = int(final_tokens * pool_frac) // 16 * 16 * per_tok
+    runs = {}
+    for restore in ("snapshot", "reprefill"):
+        E = P.Engine(shape, weights, P.BF16, pool_bytes, max_seqs=n_traj + 8,
+                     max_seq_len=int(prompts.max()) + decode + 32, max_batch=max_batch,
+                     max_chunk=2048)
+        drv = P.PacedRollout(E, h_min=max_batch * 16, delta=delta, restore=restore,
+                             chunk_tokens=2048)
+        for i, n in enumerate(prompts):
+            drv.add(i, random_tokens(int(n) + decode, shape.vocab, seed=500 + i), int(n),
+                    staged=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        steps = decoded = 0
+        while not drv.finished and steps < 50 * decode:
+            decoded += len(drv.step())
+            steps += 1
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        assert drv.finished
+        runs[restore] = {"decode_tokens_per_s": round(decoded / wall, 1), "wall_s": round(wall, 3),
+                         "steps": steps, "decoded_tokens": decoded, **drv.stats}
+        log(f"paced rollout ({restore}): {runs[restore]}")
+        E.close()
+        del E, drv
+        torch.cuda.empty_cache()
+    return {"metric": "decode tokens/s of a headroom-paced rollout, 1 MI355X",
+            "value": runs["snapshot"]["decode_tokens_per_s"], "unit": "tokens/s", "n_gpus": 1,
+            "higher_is_better": True, "data": "synthetic", "dtype": "bf16",
+            "config": {"workload": "paced-rollout-8b", "trajectories": n_traj,
+                       "decode_tokens": decode, "max_batch": max_batch, "pool_fraction": pool_frac,
+                       "prompt_lengths": ["lognormal", 1024, 0.8, 256, 4096],
+                       "h_min_tokens": max_batch * 16, "delta_tokens": delta},
+            "runs": runs, "cpu_baseline": None}
+
+
 PROJ_SHAPES = [("qkv", 6144, 4096), ("o", 4096, 4096), ("gate_up", 28672, 4096),
                ("down", 4096, 14336), ("lm_head", 128256, 4096)]
 
@@ -747,7 +806,7 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
                     choices=sorted(WORKLOADS) + sorted(FP8_KV) + sorted(MULTITURN)
                     + ["kv-transfer-8b", "projections-8b", "landscape-8b", "sampling-8b",
-                       "copy-1gib"])
+                       "copy-1gib", "paced-rollout-8b"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -765,6 +824,8 @@ def main():
         out = run_sampling()
     elif args.workload == "copy-1gib":
         out = run_copy_calibration()
+    elif args.workload == "paced-rollout-8b":
+        out = run_paced_rollout()
     elif args.workload in MULTITURN:
         out = run_multiturn(args.workload, segments=3, seg_steps=args.steps, warmup=args.warmup)
     else:

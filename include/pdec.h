@@ -280,6 +280,32 @@ int sample(pdec_engine* engine, int32_t batch, const float* logits_dev, int32_t*
  * Slots past lens[b] in the last page are never read.
  * ------------------------------------------------------------------------- */
 /* ---------------------------------------------------------------------------
+ * Headroom pacing on this worker (Design, "Separating Departure from
+ * Placement": pacing thresholds; Alg. pacing restricted to one worker, the
+ * only one a single GPU holds).  A host-only decision; the caller carries it
+ * out with kv_export / kv_free (eviction) and kv_alloc / kv_import or
+ * kv_append_prefix (placement).
+ *   Phase 1: while headroom_tokens < h_min_tokens and residents remain, evict
+ *     the longest resident (ties: lower id); the headroom rises by its
+ *     active_held_tokens (its pages x 16, reserve included).
+ *   Phase 2: the pending trajectories, evicted ones included, in ascending
+ *     length (ties: lower id): r is placed when headroom - footprint(r) >=
+ *     h_min_tokens + (residents + 1) * delta_tokens, footprint(r) =
+ *     ceil(length / 16) * 16; the headroom then falls by footprint(r).
+ *   active_*: n_active entries (ids are the caller's); pending_*: n_pending.
+ *   evict_out: capacity n_active, in eviction order; place_out: capacity
+ *     n_active + n_pending, in placement order; counts in *n_evict_out,
+ *     *n_place_out.  Host memory throughout.
+ * Errors: PDEC_INVALID_ARG (negative counts, lengths or thresholds, null
+ * arrays).
+ * ------------------------------------------------------------------------- */
+int pacing_plan(int64_t headroom_tokens, int64_t h_min_tokens, int64_t delta_tokens,
+                int32_t n_active, const int32_t* active_ids, const int32_t* active_len,
+                const int64_t* active_held_tokens, int32_t n_pending, const int32_t* pending_ids,
+                const int32_t* pending_len, int32_t* evict_out, int32_t* n_evict_out,
+                int32_t* place_out, int32_t* n_place_out);
+
+/* ---------------------------------------------------------------------------
  * Temperature / nucleus (top-p) sampling for RL rollouts, which sample their
  * actions (Background, "RL Post-Training Workflow"; the paper does not state
  * its sampler).  Random numbers are inputs: uniforms_dev holds one u in

@@ -18,4 +18,7 @@ def __getattr__(name):
                 "paged_decode_attention_fp8"):
         from . import engine
         return getattr(engine, name)
+    if name in ("PacedRollout", "pacing_plan"):
+        from . import driver
+        return getattr(driver, name)
     raise AttributeError(name)

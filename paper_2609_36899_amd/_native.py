@@ -80,6 +80,10 @@ SIGNATURES = {
     "sample": (c_int32, [c_void_p, c_int32, c_void_p, c_void_p, c_int32]),
     "kv_export": (c_int32, [c_void_p, c_int32, c_void_p, c_int64, POINTER(c_int32)]),
     "kv_import": (c_int32, [c_void_p, c_int32, c_void_p, c_int64, c_int32]),
+    "pacing_plan": (c_int32, [c_int64, c_int64, c_int64, c_int32, POINTER(c_int32),
+                              POINTER(c_int32), POINTER(c_int64), c_int32, POINTER(c_int32),
+                              POINTER(c_int32), POINTER(c_int32), POINTER(c_int32),
+                              POINTER(c_int32), POINTER(c_int32)]),
     "sample_top_p": (c_int32, [c_int32, c_int32, c_void_p, c_float, c_float, c_void_p, c_void_p,
                                c_void_p]),
     "packed_weight_bytes": (c_int64, [c_int32, c_int32, c_int32]),

@@ -4,7 +4,7 @@
 
 produces, next to this file:
   libpdec.so       -- HIP kernels + C ABI (include/pdec.h), built by hipcc for gfx950
-  libpdec_host.so  -- page pool and attention planner only, built by g++ (CPU tests)
+  libpdec_host.so  -- page pool, attention planner and pacing only, built by g++ (CPU tests)
 """
 
 from __future__ import annotations
@@ -22,7 +22,7 @@ BUILD = os.path.join(PKG, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 HIP_SOURCES = ["attention.hip", "gemm.hip", "pointwise.hip", "kvcopy.hip", "sample.hip",
-               "engine.cpp", "pagepool.cpp"]
+               "engine.cpp", "pagepool.cpp", "pacing.cpp"]
 HIP_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
     # Packed fp32 VALU ops are kept out of the device code.
@@ -66,7 +66,8 @@ def build_host() -> str:
     tmp = lib + ".tmp"
     _run(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-Wall",
           f"-I{os.path.join(ROOT, 'include')}",
-          os.path.join(CSRC, "pagepool.cpp"), os.path.join(CSRC, "host_capi.cpp"), "-o", tmp])
+          os.path.join(CSRC, "pagepool.cpp"), os.path.join(CSRC, "pacing.cpp"),
+          os.path.join(CSRC, "host_capi.cpp"), "-o", tmp])
     os.replace(tmp, lib)
     return lib
 

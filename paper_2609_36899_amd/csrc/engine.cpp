@@ -18,6 +18,7 @@
 
 #include "../../include/pdec.h"
 #include "kernels.h"
+#include "pacing.h"
 #include "pagepool.h"
 
 using namespace pdec;
@@ -812,6 +813,38 @@ int sample(pdec_engine* E, int32_t B, const float* logits_dev, int32_t* tokens_d
   if (mode != 0) return fail(PDEC_UNSUPPORTED, "only greedy sampling (mode 0) is implemented");
   if (B < 1) return fail(PDEC_INVALID_ARG, "batch must be >= 1");
   HIP_OR_FAIL(launch_argmax(B, E->cfg.vocab, logits_dev, tokens_dev_out, E->stream));
+  return PDEC_OK;
+}
+
+int pacing_plan(int64_t headroom_tokens, int64_t h_min_tokens, int64_t delta_tokens,
+                int32_t n_active, const int32_t* active_ids, const int32_t* active_len,
+                const int64_t* active_held_tokens, int32_t n_pending, const int32_t* pending_ids,
+                const int32_t* pending_len, int32_t* evict_out, int32_t* n_evict_out,
+                int32_t* place_out, int32_t* n_place_out) {
+  if (n_active < 0 || n_pending < 0 || !n_evict_out || !n_place_out)
+    return fail(PDEC_INVALID_ARG, "bad counts or null output");
+  if ((n_active && (!active_ids || !active_len || !active_held_tokens || !evict_out)) ||
+      (n_pending && (!pending_ids || !pending_len)) || (n_active + n_pending && !place_out))
+    return fail(PDEC_INVALID_ARG, "null array argument");
+  if (h_min_tokens < 0 || delta_tokens < 0)
+    return fail(PDEC_INVALID_ARG, "h_min and delta must be >= 0");
+  std::vector<PacingResident> act(n_active);
+  for (int i = 0; i < n_active; ++i) {
+    if (active_len[i] < 0 || active_held_tokens[i] < 0)
+      return fail(PDEC_INVALID_ARG, "negative length or held tokens");
+    act[i] = {active_ids[i], active_len[i], active_held_tokens[i]};
+  }
+  std::vector<PacingPending> pend(n_pending);
+  for (int i = 0; i < n_pending; ++i) {
+    if (pending_len[i] < 0) return fail(PDEC_INVALID_ARG, "negative pending length");
+    pend[i] = {pending_ids[i], pending_len[i]};
+  }
+  std::vector<int32_t> ev, pl;
+  pdec::pacing_plan(headroom_tokens, h_min_tokens, delta_tokens, act, pend, &ev, &pl);
+  for (size_t i = 0; i < ev.size(); ++i) evict_out[i] = ev[i];
+  for (size_t i = 0; i < pl.size(); ++i) place_out[i] = pl[i];
+  *n_evict_out = (int32_t)ev.size();
+  *n_place_out = (int32_t)pl.size();
   return PDEC_OK;
 }
 

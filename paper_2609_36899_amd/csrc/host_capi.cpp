@@ -8,6 +8,7 @@
 #include <string>
 #include <vector>
 
+#include "pacing.h"
 #include "pagepool.h"
 
 using namespace pdec;
@@ -127,6 +128,25 @@ int64_t pp_total_key_pages(const int32_t* specs, int32_t n) {
   for (int i = 0; i < n; ++i)
     sp[i] = {specs[4 * i], specs[4 * i + 1], specs[4 * i + 2], specs[4 * i + 3]};
   return total_key_pages(sp);
+}
+
+// Pacing decision (the same code the device library exports as pacing_plan).
+int32_t pp_pacing_plan(int64_t headroom, int64_t h_min, int64_t delta, int32_t n_active,
+                       const int32_t* active_ids, const int32_t* active_len,
+                       const int64_t* active_held, int32_t n_pending, const int32_t* pending_ids,
+                       const int32_t* pending_len, int32_t* evict_out, int32_t* n_evict,
+                       int32_t* place_out, int32_t* n_place) {
+  std::vector<PacingResident> act(n_active);
+  for (int i = 0; i < n_active; ++i) act[i] = {active_ids[i], active_len[i], active_held[i]};
+  std::vector<PacingPending> pend(n_pending);
+  for (int i = 0; i < n_pending; ++i) pend[i] = {pending_ids[i], pending_len[i]};
+  std::vector<int32_t> ev, pl;
+  pacing_plan(headroom, h_min, delta, act, pend, &ev, &pl);
+  for (size_t i = 0; i < ev.size(); ++i) evict_out[i] = ev[i];
+  for (size_t i = 0; i < pl.size(); ++i) place_out[i] = pl[i];
+  *n_evict = (int32_t)ev.size();
+  *n_place = (int32_t)pl.size();
+  return 0;
 }
 
 }  // extern "C"
