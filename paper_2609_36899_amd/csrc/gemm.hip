@@ -139,29 +139,37 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(int M, int N, int K, int
 
 // Larger batches (M > 32): (64 WM) x 128 output tiles, 2 WM waves in a WM x 2
 // grid of 64 x 64 sub-tiles.  Per k-step of 64 the A tile and the W tile are
-// staged once through LDS (double-buffered) and each is shared by the waves
-// that need it; the tiles of the next NS k-steps are prefetched into a
-// register ring meanwhile (NS even: ring slot s also names the LDS buffer
-// s & 1).  The W tile is 8 strips x 2 blocks, copied in packed order (eight
-// 2 KiB runs from HBM; fragment reads from LDS are linear, hence free of bank
-// conflicts); the A tile is row-major with 16-byte chunks XOR-swizzled by
-// row.  WM = 4 covers 256 rows, so up to that batch size W is read from HBM
-// exactly once per step.  Larger batches take several M-blocks, laid out so
-// the M-blocks of one column tile are dispatched back to back (ids L and L+8
-// share an XCD).
-template <int WM, int NS>
+// staged once through LDS and each is shared by the waves that need it.  The
+// tiles travel from memory straight into LDS (16-byte LDS-DMA loads, no
+// register staging), through a ring of three stages: while step it is
+// computed, steps it+1 and it+2 are in flight.  One barrier per step: after
+// it, every wave has finished step it-1, whose stage then takes step it+2.
+// The W tile is 8 strips x 2 blocks, copied in packed order (eight 2 KiB runs
+// from HBM; fragment reads from LDS are linear, hence free of bank
+// conflicts); the A tile is row-major with its 16-byte chunks XOR-swizzled by
+// row (the swizzle is applied to the source address, as the DMA writes each
+// wave's 64 chunks contiguously).  WM = 4 covers 256 rows, so up to that
+// batch size W is read from HBM exactly once per step.  Larger batches take
+// several M-blocks, laid out so the M-blocks of one column tile are
+// dispatched back to back (ids L and L+8 share an XCD).
+template <int WM>
 __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, int k_split,
                                                           int n_mb, int n_nb,
                                                           const uint16_t* __restrict__ A,
                                                           int64_t lda, WSegs w,
                                                           float* __restrict__ out) {
-  constexpr int MT = 4, NT = 4;
+  constexpr int MT = 4, NT = 4, D = 3;
   constexpr int THREADS = 128 * WM, ROWS = 64 * WM;
-  constexpr int RSTEP = THREADS / 8;  // A rows covered by one chunk column of the group
-  constexpr int ACH = ROWS / RSTEP;   // A chunks per thread (4)
-  constexpr int WCH = 1024 / THREADS; // W chunks per thread (16 KiB tile)
-  __shared__ __attribute__((aligned(16))) uint16_t la_s[2][ROWS * 64];
-  __shared__ __attribute__((aligned(16))) uint16_t lw_s[2][128 * 64];
+  constexpr int ACH = ROWS * 8 / THREADS;  // A chunks per thread per stage (4)
+  constexpr int WCH = 1024 / THREADS;      // W chunks per thread per stage (16 KiB tile)
+  constexpr int LPS = ACH + WCH;           // loads per thread per stage
+  constexpr int SA = ROWS * 64, STAGE = SA + 128 * 64;
+  // One array per stage: the compiler then tells the stages' LDS apart and
+  // does not wait for every DMA in flight before reading a landed stage.
+  __shared__ __attribute__((aligned(16))) uint16_t lds0[STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t lds1[STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t lds2[STAGE];
+  auto stage_ptr = [&](int b) -> uint16_t* { return b == 0 ? lds0 : b == 1 ? lds1 : lds2; };
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int c16 = lane & 15, q4 = lane >> 4;
   const int L = blockIdx.x;
@@ -175,22 +183,25 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
   const int wm = wave >> 1, wn = wave & 1;
   const int n_strips = (N + 15) / 16;
 
-  const int r = tid >> 3, c = tid & 7;
-  const int dst = r * 64 + ((c ^ (r & 7)) * 8);  // + j * RSTEP * 64 for chunk j
+  // Chunk id = j * THREADS + tid lands at LDS chunk id of the stage (the DMA
+  // of wave w, load j, fills chunks j * THREADS + 64 w .. +63).  A: chunk id
+  // is row id >> 3, slot id & 7, holding source chunk slot ^ (row & 7).
   const uint16_t* asrc[ACH];
+#pragma unroll
+  for (int j = 0; j < ACH; ++j) {
+    const int id = j * THREADS + tid, r = id >> 3, slot = id & 7;
+    asrc[j] = A + (int64_t)min(m_blk + r, M - 1) * lda + kbeg + ((slot ^ (r & 7)) * 8);
+  }
   const uint16_t* wsrc[WCH];
 #pragma unroll
-  for (int j = 0; j < ACH; ++j)
-    asrc[j] = A + (int64_t)min(m_blk + r + RSTEP * j, M - 1) * lda + kbeg + c * 8;
-#pragma unroll
   for (int j = 0; j < WCH; ++j) {
-    const int id = tid + j * THREADS;  // chunk id in the tile: strip id >> 7
+    const int id = j * THREADS + tid;  // strip id >> 7 of the tile
     wsrc[j] = strip_base(w, min(nb * 8 + (id >> 7), n_strips - 1), K) + (int64_t)kbeg * 16 +
               (id & 127) * 8;
   }
   int aoff[MT][2];
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
+  for (int t = 0; t < MT; ++t)
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int ra = wm * 64 + t * 16 + c16, cc = h * 4 + q4;
@@ -203,27 +214,16 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // The A and W tiles of the next NS k-steps are in flight in a register
-  // ring.  As in the streaming kernel, the steady-state loop is branch-free
-  // (prefetch index clamped to the last step), so each LDS store waits only
-  // for its own slot's loads and the younger slots stay in flight.
-  static_assert(NS % 2 == 0, "ring depth must be even");
-  u16x8 ra_[NS][ACH], rw_[NS][WCH];
-  auto gload = [&](int i, u16x8(&ra)[ACH], u16x8(&rw)[WCH]) {
+  auto issue = [&](int i, int b) {
+    uint16_t* base = stage_ptr(b) + wave * 64 * 8;
 #pragma unroll
-    for (int j = 0; j < WCH; ++j) rw[j] = *(const u16x8*)(wsrc[j] + i * 1024);
+    for (int j = 0; j < ACH; ++j) dma16(asrc[j] + i * 64, base + j * THREADS * 8);
 #pragma unroll
-    for (int j = 0; j < ACH; ++j) ra[j] = *(const u16x8*)(asrc[j] + i * 64);
+    for (int j = 0; j < WCH; ++j) dma16(wsrc[j] + i * 1024, base + SA + j * THREADS * 8);
   };
-  auto stage = [&](int buf, const u16x8(&ra)[ACH], const u16x8(&rw)[WCH]) {
-#pragma unroll
-    for (int j = 0; j < ACH; ++j) *(u16x8*)(la_s[buf] + dst + j * RSTEP * 64) = ra[j];
-#pragma unroll
-    for (int j = 0; j < WCH; ++j) *(u16x8*)(lw_s[buf] + (tid + j * THREADS) * 8) = rw[j];
-  };
-  auto compute = [&](int buf) {
-    const uint16_t* la = la_s[buf];
-    const uint16_t* lw = lw_s[buf];
+  auto compute = [&](int b) {
+    const uint16_t* la = stage_ptr(b);
+    const uint16_t* lw = la + SA;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       bf16x8 af[MT], bf[NT];
@@ -239,29 +239,36 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
   };
+  // Every step issues one stage (the prefetch index clamped to the last
+  // step, so the tail re-reads it into a stage nobody reads), which keeps
+  // the count of loads in flight fixed: waiting until D - 2 stages are
+  // outstanding means this wave's part of step it has landed; the barrier
+  // then covers the other waves' parts.
   const int last = n_iter - 1;
 #pragma unroll
-  for (int s = 0; s < NS; ++s) gload(min(s, last), ra_[s], rw_[s]);
-  int it0 = 0;
-  for (; it0 + NS <= n_iter; it0 += NS) {
+  for (int s = 0; s < D - 1; ++s) issue(min(s, last), s);
+  int it = 0;
+  for (; it + D <= n_iter; it += D) {
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      // step it0 + s uses LDS buffer s & 1 (it0 is a multiple of NS, which is even)
-      stage(s & 1, ra_[s], rw_[s]);
-      __syncthreads();
-      gload(min(it0 + s + NS, last), ra_[s], rw_[s]);
+    for (int s = 0; s < D; ++s) {
+      wait_vmem<(D - 2) * LPS>();
+      wg_barrier();
+      issue(min(it + s + D - 1, last), (s + D - 1) % D);
       __builtin_amdgcn_sched_barrier(0);
-      compute(s & 1);
+      compute(s);
     }
   }
-  const int tail = n_iter - it0;  // uniform over the work group
+  const int tail = n_iter - it;  // uniform over the work group
 #pragma unroll
-  for (int s = 0; s < NS; ++s)
+  for (int s = 0; s < D; ++s)
     if (s < tail) {
-      stage(s & 1, ra_[s], rw_[s]);
-      __syncthreads();
-      compute(s & 1);
+      wait_vmem<(D - 2) * LPS>();
+      wg_barrier();
+      issue(min(it + s + D - 1, last), (s + D - 1) % D);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(s);
     }
+  wait_vmem<0>();  // no LDS write may still be in flight when the group ends
 
   float* o = out + (int64_t)blockIdx.z * M * N;
 #pragma unroll
@@ -357,11 +364,8 @@ int gemm_plan_splits(int dtype, int M, int N, int K, int* k_split) {
     }
     // Measured on the 8B shapes with weights streamed from HBM: the best
     // split count fills one round of work groups on the 256 CUs (a partial
-    // second round costs 15-30%), except that the 128-row tile prefers two
-    // short rounds to one long one when the column tiles alone nearly fill
-    // the chip.
+    // second round costs 15-30%).
     s = (int)std::max<int64_t>(1, 256 / groups);
-    if (M > kStreamMaxRows && tile_rows(M) == 128 && s == 1 && groups <= 256) s = 2;
     s = std::min(s, 8);
   } else {
     const int64_t groups = (int64_t)((N + 63) / 64) * ((M + 31) / 32);
@@ -401,11 +405,11 @@ hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t ld
       const int n_mb = (M + rows - 1) / rows, n_nb = (N + 127) / 128;
       const dim3 grid(((n_nb + 7) / 8) * 8 * n_mb, 1, splits);
       if (rows == 128)
-        gemm_bf16_tile<2, 2><<<grid, dim3(256), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a,
-                                                               lda, w, out);
+        gemm_bf16_tile<2><<<grid, dim3(256), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a, lda,
+                                                            w, out);
       else
-        gemm_bf16_tile<4, 2><<<grid, dim3(512), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a,
-                                                               lda, w, out);
+        gemm_bf16_tile<4><<<grid, dim3(512), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a, lda,
+                                                            w, out);
     }
   } else {
     const dim3 grid((N + 63) / 64, (M + 31) / 32, splits);

@@ -26,6 +26,32 @@ __device__ __forceinline__ V load_stream(const void* p) {
   }
 }
 
+// 16 bytes per lane from global memory straight into LDS (gfx950 LDS-DMA):
+// lane i's bytes land at lds + 16 i, where lds is uniform over the wave.  The
+// load counts in the vector-memory counter until its data is in LDS.
+__device__ __forceinline__ void dma16(const void* src, void* lds) {
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                   (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding
+// (loads retire in issue order), leaving the other counters alone.
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Work-group barrier without the fence of __syncthreads, whose release would
+// wait for every load in flight (LDS-DMA loads included).  Callers order
+// their memory with explicit counter waits; the empty asm statements keep
+// the compiler from moving memory accesses across the barrier.
+__device__ __forceinline__ void wg_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // bf16 storage is handled as raw 16-bit patterns.
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __uint_as_float(((uint32_t)b) << 16);
