@@ -406,14 +406,14 @@ __device__ __forceinline__ void merge_into(float& m, float& l, float* o, float m
   m = mn;
 }
 
-template <int DH, typename OutT>
-__global__ __launch_bounds__(256) void attn_combine(const AttnQBlock* __restrict__ qblocks,
-                                                   const float* __restrict__ part_ml,
-                                                   const float* __restrict__ part_acc,
-                                                   int32_t n_q_heads, int32_t n_kv_heads, int32_t R,
-                                                   OutT* __restrict__ out) {
+template <int DH, typename OutT, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_combine(const AttnQBlock* __restrict__ qblocks,
+                                                       const float* __restrict__ part_ml,
+                                                       const float* __restrict__ part_acc,
+                                                       int32_t n_q_heads, int32_t n_kv_heads,
+                                                       int32_t R, OutT* __restrict__ out) {
   constexpr int DPL = DH / 16;
-  __shared__ float sh[4][64][DPL + 2];
+  __shared__ float sh[NW][64][DPL + 2];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int rsub = lane >> 4, d0 = (lane & 15) * DPL;
   const AttnQBlock qb = qblocks[blockIdx.x];
@@ -426,12 +426,12 @@ __global__ __launch_bounds__(256) void attn_combine(const AttnQBlock* __restrict
 #pragma unroll
     for (int e = 0; e < DPL; ++e) o[e] = 0.f;
     // Items i0 + 4u (u = 0..3) of this wave's stride, loads issued first.
-    for (int i0 = qb.item_begin + wave; i0 < qb.item_end; i0 += 16) {
+    for (int i0 = qb.item_begin + wave; i0 < qb.item_end; i0 += 4 * NW) {
       float2 ml[4];
       float a[4][DPL];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int i = min(i0 + 4 * u, qb.item_end - 1);
+        const int i = min(i0 + NW * u, qb.item_end - 1);
         const int64_t prow = ((int64_t)i * n_kv_heads + g) * R + r;
         ml[u] = *(const float2*)(part_ml + prow * 2);
 #pragma unroll
@@ -445,7 +445,7 @@ __global__ __launch_bounds__(256) void attn_combine(const AttnQBlock* __restrict
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        if (i0 + 4 * u >= qb.item_end) break;
+        if (i0 + NW * u >= qb.item_end) break;
         merge_into<DPL>(m, l, o, ml[u].x, ml[u].y, a[u]);
       }
     }
@@ -455,7 +455,7 @@ __global__ __launch_bounds__(256) void attn_combine(const AttnQBlock* __restrict
     for (int e = 0; e < DPL; ++e) sh[wave][lane][2 + e] = o[e];
     __syncthreads();
     if (wave == 0 && r0 + rsub < rows) {
-      for (int w = 1; w < 4; ++w)
+      for (int w = 1; w < NW; ++w)
         merge_into<DPL>(m, l, o, sh[w][lane][0], sh[w][lane][1], &sh[w][lane][2]);
       const float inv = 1.f / l;
       const int jq = r / G, head = g * G + r % G;
@@ -516,20 +516,31 @@ hipError_t launch_attention_split(int dtype, int kv_fp8, float k_scale, float v_
 }
 
 hipError_t launch_attention_combine(int head_dim, int rows_per_item, int n_qblocks,
-                                    int n_q_heads, int n_kv_heads, const AttnQBlock* qblocks,
-                                    const float* part_ml, const float* part_acc, void* out,
-                                    int out_bf16, hipStream_t stream) {
+                                    int max_items, int n_q_heads, int n_kv_heads,
+                                    const AttnQBlock* qblocks, const float* part_ml,
+                                    const float* part_acc, void* out, int out_bf16,
+                                    hipStream_t stream) {
   if (n_qblocks == 0) return hipSuccess;
-  const dim3 grid(n_qblocks, n_kv_heads), block(256);
+  const dim3 grid(n_qblocks, n_kv_heads);
+  // Each wave merges four items per round: enough waves that the query block
+  // with the most items (the longest context) needs a single round, up to 16.
+  const int nw = max_items <= 16 ? 4 : max_items <= 32 ? 8 : 16;
+#define PDEC_COMBINE_NW(DH_, T_, NW_)                                                        \
+  attn_combine<DH_, T_, NW_><<<grid, dim3(64 * NW_), 0, stream>>>(                           \
+      qblocks, part_ml, part_acc, n_q_heads, n_kv_heads, rows_per_item, (T_*)out)
 #define PDEC_COMBINE(DH_, T_)                                                                \
-  attn_combine<DH_, T_><<<grid, block, 0, stream>>>(qblocks, part_ml, part_acc, n_q_heads, \
-                                                    n_kv_heads, rows_per_item, (T_*)out)
+  do {                                                                                       \
+    if (nw == 4) PDEC_COMBINE_NW(DH_, T_, 4);                                                \
+    else if (nw == 8) PDEC_COMBINE_NW(DH_, T_, 8);                                           \
+    else PDEC_COMBINE_NW(DH_, T_, 16);                                                       \
+  } while (0)
   if (head_dim == 128) {
     if (out_bf16) PDEC_COMBINE(128, uint16_t); else PDEC_COMBINE(128, float);
   } else {
     if (out_bf16) PDEC_COMBINE(64, uint16_t); else PDEC_COMBINE(64, float);
   }
 #undef PDEC_COMBINE
+#undef PDEC_COMBINE_NW
   return hipGetLastError();
 }
 

@@ -352,6 +352,12 @@ int flush_deltas(pdec_engine* E) {
   return PDEC_OK;
 }
 
+int max_items_per_qblock(const std::vector<AttnQBlock>& qblocks) {
+  int m = 0;
+  for (const AttnQBlock& q : qblocks) m = std::max(m, q.item_end - q.item_begin);
+  return m;
+}
+
 // Runs the decoder over M rows whose metadata is given; writes the LM-head
 // logits of every row (lm_last_only = false) or of the last row only.
 int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
@@ -389,6 +395,7 @@ int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
   const int qd = c.n_q_heads * Dh, nqkv = qd + 2 * c.n_kv_heads * Dh;
   hipStream_t s = E->stream;
   const int n_items = (int)items.size(), n_qb = (int)qblocks.size();
+  const int max_items = max_items_per_qblock(qblocks);
 
   HIP_OR_FAIL(launch_embed_norm(dt, M, d, c.vocab, d_tok, E->embed, E->attn_norm[0], c.rms_eps, E->x,
                                 E->h, s));
@@ -411,8 +418,9 @@ int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
                                        E->q, E->k_layer(l), E->v_layer(l), E->page_stride, E->bt,
                                        E->ws.bt_stride, E->att_ml, E->att_acc, s));
     HIP_OR_FAIL(E->timer.end(s));
-    HIP_OR_FAIL(launch_attention_combine(Dh, rows_per_item, n_qb, c.n_q_heads, c.n_kv_heads, d_qb,
-                                         E->att_ml, E->att_acc, E->o, dt == PDEC_BF16, s));
+    HIP_OR_FAIL(launch_attention_combine(Dh, rows_per_item, n_qb, max_items, c.n_q_heads,
+                                         c.n_kv_heads, d_qb, E->att_ml, E->att_acc, E->o,
+                                         dt == PDEC_BF16, s));
     S = gemm_plan_splits(dt, M, d, qd, &ks);
     HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_GEMM, s));
     HIP_OR_FAIL(launch_gemm(dt, M, d, qd, E->o, qd, E->w_o[l], E->part, S, ks, s));
@@ -979,8 +987,8 @@ static int paged_attention_impl(int32_t kv_dtype, float k_scale, float v_scale, 
                                      (const AttnQBlock*)(base + o_qb), q, k_pages, v_pages,
                                      page_stride, bt, bt_stride, (float*)(base + o_ml),
                                      (float*)(base + o_acc), s));
-  HIP_OR_FAIL(launch_attention_combine(Dh, kDecodeRows, B, Hq, Hkv,
-                                       (const AttnQBlock*)(base + o_qb),
+  HIP_OR_FAIL(launch_attention_combine(Dh, kDecodeRows, B, max_items_per_qblock(qblocks), Hq,
+                                       Hkv, (const AttnQBlock*)(base + o_qb),
                                        (float*)(base + o_ml), (float*)(base + o_acc), out, 0, s));
   return PDEC_OK;
 }

@@ -36,7 +36,7 @@ hipError_t launch_attention_split(int dtype, int kv_fp8, float k_scale, float v_
 // Merge pass: one work group per (query block, KV head); writes
 // out [rows][n_q_heads][head_dim] as fp32 (out_bf16 = 0) or bf16.
 hipError_t launch_attention_combine(int head_dim, int rows_per_item, int n_qblocks,
-                                    int n_q_heads, int n_kv_heads,
+                                    int max_items, int n_q_heads, int n_kv_heads,
                                     const AttnQBlock* qblocks, const float* part_ml,
                                     const float* part_acc, void* out, int out_bf16,
                                     hipStream_t stream);

@@ -12,6 +12,40 @@ namespace {
 
 constexpr int kRowThreads = 256;
 
+// Split-K partials: partial s of element i is at p[s * slab + i].  These add
+// v + p[0] + p[slab] + ... + p[(n - 1) slab] in that order, with the loads of
+// up to eight splits issued together so that their latencies overlap.
+__device__ __forceinline__ float4 add_splits4(float4 v, const float* p, int64_t slab, int n) {
+  for (int s0 = 0; s0 < n; s0 += 8) {
+    float4 t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (s0 + u < n) t[u] = *(const float4*)(p + (int64_t)(s0 + u) * slab);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (s0 + u < n) {
+        v.x += t[u].x;
+        v.y += t[u].y;
+        v.z += t[u].z;
+        v.w += t[u].w;
+      }
+  }
+  return v;
+}
+
+__device__ __forceinline__ float add_splits1(float v, const float* p, int64_t slab, int n) {
+  for (int s0 = 0; s0 < n; s0 += 8) {
+    float t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (s0 + u < n) t[u] = p[(int64_t)(s0 + u) * slab];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (s0 + u < n) v += t[u];
+  }
+  return v;
+}
+
 // Token ids from the caller's device buffer cannot be checked on the host
 // without a synchronisation; out-of-range ids are clamped so that they read
 // a valid embedding row instead of faulting.
@@ -73,32 +107,43 @@ template <typename HT>
 __global__ __launch_bounds__(1024) void resid_norm_kernel(
     int M, int d, const float* __restrict__ part, int splits, float* __restrict__ x,
     const float* __restrict__ gain, float eps, HT* __restrict__ h) {
+  constexpr int RC = 4;  // float4s per thread kept in registers between the passes
   __shared__ float red[16];
   const int row = blockIdx.x;
   float* xr = x + (int64_t)row * d;
   const int64_t slab = (int64_t)M * d;
   const float* pr = part + (int64_t)row * d;
+  const int stride = blockDim.x * 4;
+  float4 keep[RC];
   float ss = 0.f;
-  for (int i = threadIdx.x * 4; i < d; i += blockDim.x * 4) {
-    float4 v = *(const float4*)(xr + i);
-    for (int s = 0; s < splits; ++s) {
-      const float4 p = *(const float4*)(pr + s * slab + i);
-      v.x += p.x;
-      v.y += p.y;
-      v.z += p.z;
-      v.w += p.w;
+#pragma unroll
+  for (int k = 0; k < RC; ++k) {
+    const int i = threadIdx.x * 4 + k * stride;
+    if (i < d) {
+      const float4 v = add_splits4(*(const float4*)(xr + i), pr + i, slab, splits);
+      *(float4*)(xr + i) = v;
+      keep[k] = v;
+      ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
     }
+  }
+  for (int i = threadIdx.x * 4 + RC * stride; i < d; i += stride) {  // rows wider than kept
+    const float4 v = add_splits4(*(const float4*)(xr + i), pr + i, slab, splits);
     *(float4*)(xr + i) = v;
     ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   const float inv = rsqrtf(block_sum(ss, red) / (float)d + eps);
   HT* hr = h + (int64_t)row * d;
-  for (int i = threadIdx.x * 4; i < d; i += blockDim.x * 4) {
-    const float4 v = *(const float4*)(xr + i);
+  auto put = [&](int i, float4 v) {
     const float4 g = *(const float4*)(gain + i);
     Pack4<HT>::store(hr + i, make_float4(v.x * inv * g.x, v.y * inv * g.y, v.z * inv * g.z,
                                          v.w * inv * g.w));
+  };
+#pragma unroll
+  for (int k = 0; k < RC; ++k) {
+    const int i = threadIdx.x * 4 + k * stride;
+    if (i < d) put(i, keep[k]);
   }
+  for (int i = threadIdx.x * 4 + RC * stride; i < d; i += stride) put(i, *(const float4*)(xr + i));
 }
 
 // A row is handled by gridDim.y work groups.  Pairs (i, i + Dh/2) of every q and k head are
@@ -134,13 +179,8 @@ __global__ __launch_bounds__(kRowThreads) void qkv_rope_kv_kernel(
   for (int qd = part_id * kRowThreads + threadIdx.x; qd < n_quads; qd += n_parts * kRowThreads) {
     const int hh = qd / quads_per_head, i = (qd % quads_per_head) * 4;
     const int c0 = hh * head_dim + i, c1 = c0 + half;
-    float4 a = *(const float4*)(pr + c0), b = *(const float4*)(pr + c1);
-    for (int s = 1; s < splits; ++s) {
-      const float4 a2 = *(const float4*)(pr + s * slab + c0);
-      const float4 b2 = *(const float4*)(pr + s * slab + c1);
-      a.x += a2.x; a.y += a2.y; a.z += a2.z; a.w += a2.w;
-      b.x += b2.x; b.y += b2.y; b.z += b2.z; b.w += b2.w;
-    }
+    float4 a = add_splits4(*(const float4*)(pr + c0), pr + slab + c0, slab, splits - 1);
+    float4 b = add_splits4(*(const float4*)(pr + c1), pr + slab + c1, slab, splits - 1);
     if (q_gain) {
       // All quads_per_head lanes of this head run this iteration together
       // (heads are whole, aligned lane groups and n_quads is a multiple).
@@ -171,8 +211,7 @@ __global__ __launch_bounds__(kRowThreads) void qkv_rope_kv_kernel(
   const int vcol0 = (n_q_heads + n_kv_heads) * head_dim;
   for (int idx = part_id * kRowThreads + threadIdx.x; idx < n_kv_heads * head_dim;
        idx += n_parts * kRowThreads) {
-    float v = 0.f;
-    for (int s = 0; s < splits; ++s) v += pr[s * slab + vcol0 + idx];
+    const float v = add_splits1(0.f, pr + vcol0 + idx, slab, splits);
     const int g = idx / head_dim, dd = idx % head_dim;
     vpool[page_base + ((int64_t)g * head_dim + dd) * kPage + slot] = KvStore<KVT>::one(v, v_scale);
   }
@@ -189,12 +228,8 @@ __global__ __launch_bounds__(256) void swiglu_kernel(int M, int F, const float* 
     const int64_t idx = q * 4;
     const int64_t m = idx / F, c = idx % F;
     const float* pg = part + m * 2 * F + c;
-    float4 gt = *(const float4*)pg, up = *(const float4*)(pg + F);
-    for (int s = 1; s < splits; ++s) {
-      const float4 g2 = *(const float4*)(pg + s * slab), u2 = *(const float4*)(pg + s * slab + F);
-      gt.x += g2.x; gt.y += g2.y; gt.z += g2.z; gt.w += g2.w;
-      up.x += u2.x; up.y += u2.y; up.z += u2.z; up.w += u2.w;
-    }
+    const float4 gt = add_splits4(*(const float4*)pg, pg + slab, slab, splits - 1);
+    const float4 up = add_splits4(*(const float4*)(pg + F), pg + slab + F, slab, splits - 1);
     const float4 r = make_float4(gt.x / (1.f + expf(-gt.x)) * up.x, gt.y / (1.f + expf(-gt.y)) * up.y,
                                  gt.z / (1.f + expf(-gt.z)) * up.z, gt.w / (1.f + expf(-gt.w)) * up.w);
     Pack4<HT>::store(u + idx, r);
@@ -206,11 +241,8 @@ __global__ __launch_bounds__(256) void sum_splits_kernel(int64_t n4, const float
                                                          int splits, float* __restrict__ out) {
   for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n4;
        q += (int64_t)gridDim.x * blockDim.x) {
-    float4 v = *(const float4*)(part + q * 4);
-    for (int s = 1; s < splits; ++s) {
-      const float4 p = *(const float4*)(part + (int64_t)s * n4 * 4 + q * 4);
-      v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
-    }
+    const float4 v =
+        add_splits4(*(const float4*)(part + q * 4), part + n4 * 4 + q * 4, n4 * 4, splits - 1);
     *(float4*)(out + q * 4) = v;
   }
 }

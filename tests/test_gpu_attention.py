@@ -85,6 +85,19 @@ def test_bf16_config2_shape_small_batch():
     _check_rows(got, ref, BF16_TOL, normwise=True)
 
 
+@pytest.mark.parametrize("lens", [[2048], [2049, 100], [4096, 17], [4097], [25600, 5, 2049]])
+def test_bf16_combine_wave_counts(lens):
+    """Query blocks with 16 / 17 / 32 / 33 / 200 items of 8 pages (the
+    combine's work group grows from 4 to 8 to 16 waves at those counts; 200
+    items take several rounds)."""
+    lens = np.array(lens)
+    case = paged_attention_case(len(lens), 32, 8, 128, lens, n_pool_pages=2000, seed=11)
+    got = _run(case, "bf16")
+    ref = oracle.paged_decode_attention(case.q, case.k_pool, case.v_pool, case.block_table,
+                                        case.lens)
+    _check_rows(got, ref, BF16_TOL, normwise=True)
+
+
 def test_page_permutation_is_bitwise_invariant():
     lens = np.array([5, 16, 17, 700, 1500, 33])
     case = paged_attention_case(len(lens), 32, 8, 128, lens, n_pool_pages=400, seed=5)
