@@ -90,8 +90,8 @@ typedef struct pdec_model_cfg {
  * (always fp32).  The embedding table is row-major [vocab][d_model].  The
  * projection matrices (wq ... w_down, lm_head), listed below in their
  * nn.Linear [out][in] shape, are passed as produced by pack_weight: for bf16
- * that is the strip layout the weight-streaming kernels read, for fp32 the
- * row-major matrix itself.
+ * that is the group-major layout the weight-streaming kernels read, for fp32
+ * the row-major matrix itself.
  * The per-layer members are HOST arrays of n_layers DEVICE pointers; the
  * arrays are copied by engine_create and may be freed afterwards. */
 typedef struct pdec_weights {
@@ -330,13 +330,16 @@ int sample_top_p(int32_t batch, int32_t vocab, const float* logits_dev, float te
  * Weight packing.  Each decode step streams every projection matrix from HBM
  * once for the whole batch (Introduction; Design Principles, "Specialization
  * in Heterogeneous Pools"), so bf16 matrices are stored in a layout whose
- * stream is long contiguous runs: strip j holds columns 16j .. 16j+15 (the
- * last strip zero-padded) for all K, as K/32 blocks of 16 x 32 elements, each
- * block 1 KiB in the lane order of the MFMA B operand; element (n, k) is at
- *   ((j * K/32 + b) * 64 + q * 16 + c) * 8 + e,  n = 16j + c, k = 32b + 8q + e.
+ * stream is long contiguous runs.  Columns form groups of 128 (the last group
+ * zero-padded), each group 8 strips of 16 columns; a 16 x 32 block (strip s,
+ * k-block b) is 1 KiB in the lane order of the MFMA B operand, and the eight
+ * blocks of one k-block of a group are adjacent, so one k-step of 64 of a
+ * group is a single 16 KiB run.  Element (n, k) is at
+ *   (((G * K/32 + b) * 8 + s) * 64 + q * 16 + c) * 8 + e,
+ *   n = 128 G + 16 s + c,  k = 32 b + 8 q + e.
  * fp32 matrices keep the row-major layout (pack_weight copies them).
  *   packed_weight_bytes: size of the packed form of an [N][K] matrix
- *     (bf16: ceil(N/16)*16*K*2 bytes, fp32: N*K*4), or a negative status.
+ *     (bf16: ceil(N/128)*128*K*2 bytes, fp32: N*K*4), or a negative status.
  *   pack_weight: w is a device row-major [N][K] matrix in dtype; packed is a
  *     caller-owned device buffer of packed_weight_bytes(...) bytes, not
  *     overlapping w.  Asynchronous on stream.

@@ -874,7 +874,7 @@ int64_t packed_weight_bytes(int32_t dtype, int32_t N, int32_t K) {
     return fail(PDEC_INVALID_ARG, "bad weight shape");
   if (dtype == PDEC_BF16) {
     if (K % 64) return fail(PDEC_UNSUPPORTED, "bf16 weights need K % 64 == 0");
-    return (int64_t)((N + 15) / 16) * 16 * K * 2;
+    return (int64_t)((N + 127) / 128) * 128 * K * 2;
   }
   return (int64_t)N * K * 4;
 }

@@ -24,56 +24,68 @@ namespace pdec {
 
 namespace {
 
-// Base of strip j (16 columns, all K) of a weight given as up to three
-// packed segments; every segment but the last holds a multiple of 16 columns.
-__device__ __forceinline__ const uint16_t* strip_base(const WSegs& w, int j, int K) {
-  int start = 0;
-  for (int s = 0; s < w.n_seg; ++s) {
-    if (16 * j < w.row_end[s] || s == w.n_seg - 1)
-      return (const uint16_t*)w.ptr[s] + (int64_t)(j - start / 16) * K * 16;
-    start = w.row_end[s];
-  }
-  return (const uint16_t*)w.ptr[0];
+constexpr int kGroupCols = 128;  // columns per packed group (8 strips of 16)
+
+// Group g of a bf16 weight given as up to three packed segments.
+struct GroupRef {
+  const uint16_t* base;  // the group's K/32 x 8 blocks of 512 elements
+  int col0;              // its first output column
+  int col_end;           // end of its segment's output columns
+};
+__device__ __forceinline__ GroupRef group_ref(const WSegs& w, int g, int K) {
+  int s = 0;
+  while (s < w.n_seg - 1 && g >= w.grp_end[s]) ++s;
+  const int g0 = s ? w.grp_end[s - 1] : 0, c0 = s ? w.row_end[s - 1] : 0;
+  return {(const uint16_t*)w.ptr[s] + (int64_t)(g - g0) * kGroupCols * K,
+          c0 + (g - g0) * kGroupCols, w.row_end[s]};
 }
 
+// Packed bf16 layout (group-major): element (n, k) of an [N][K] matrix is at
+//   (((G * K/32 + b) * 8 + s) * 64 + q * 16 + c) * 8 + e,
+//   n = 128 G + 16 s + c,  k = 32 b + 8 q + e,
+// columns past N zero.  A 16 x 32 block (s, b) is 1 KiB in the lane order of
+// the MFMA B operand, and the eight blocks of one k-block of a group are
+// adjacent: per k-step of 64 a group's weight tile is one contiguous 16 KiB
+// run, so the streams a projection reads from HBM are few and long.
 __global__ __launch_bounds__(256) void pack_weight_kernel(const uint16_t* __restrict__ W, int N,
                                                           int K, uint16_t* __restrict__ P) {
   const int KB = K / 32;
   const int64_t chunk = (int64_t)blockIdx.x * 256 + threadIdx.x;  // one 8-element chunk
-  if (chunk >= (int64_t)((N + 15) / 16) * KB * 64) return;
+  if (chunk >= (int64_t)((N + kGroupCols - 1) / kGroupCols) * KB * 8 * 64) return;
   const int l = (int)(chunk & 63);
-  const int64_t jb = chunk >> 6;
-  const int b = (int)(jb % KB), j = (int)(jb / KB);
-  const int n = 16 * j + (l & 15), k = 32 * b + 8 * (l >> 4);
+  const int64_t r = chunk >> 6;
+  const int s = (int)(r & 7);
+  const int64_t gb = r >> 3;
+  const int b = (int)(gb % KB), G = (int)(gb / KB);
+  const int n = G * kGroupCols + 16 * s + (l & 15), k = 32 * b + 8 * (l >> 4);
   u32x4 v = {0u, 0u, 0u, 0u};
   if (n < N) v = *(const u32x4*)(W + (int64_t)n * K + k);
   *(u32x4*)(P + chunk * 8) = v;
 }
 
-// Small batches (M <= 32): each wave owns WS strips and every row of the
-// batch (MT tiles of 16 rows), so no two waves share weight bytes and no LDS
-// or barrier is needed.  The weight fragments and the matching activation
-// fragments (L2-resident) of the next NS k-steps are in flight in a register
-// ring.  The steady-state loop is branch-free (the prefetch index is clamped
-// to the last step) and pinned to consume-then-refill order per slot, so the
-// compiler keeps all NS slots in flight instead of draining the ring.
-template <int MT, int WS, int NS>
+// Small batches (M <= 32): a work group owns one 128-column group, each of
+// its four waves two strips of it and every row of the batch (MT tiles of 16
+// rows), so no two waves share weight bytes and no LDS or barrier is needed.
+// The weight fragments and the matching activation fragments (L2-resident)
+// of the next NS k-steps are in flight in a register ring.  The steady-state
+// loop is branch-free (the prefetch index is clamped to the last step) and
+// pinned to consume-then-refill order per slot, so the compiler keeps all NS
+// slots in flight instead of draining the ring.
+template <int MT, int NS>
 __global__ __launch_bounds__(256) void gemm_bf16_stream(int M, int N, int K, int k_split,
                                                         const uint16_t* __restrict__ A,
                                                         int64_t lda, WSegs w,
                                                         float* __restrict__ out) {
+  constexpr int WS = 2;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int c16 = lane & 15, q4 = lane >> 4;
-  const int n_strips = (N + 15) / 16;
-  const int j0 = (blockIdx.x * 4 + wave) * WS;
   const int kbeg = blockIdx.z * k_split;
   const int n_iter = (min(K, kbeg + k_split) - kbeg) / 64;
-  if (j0 >= n_strips || n_iter <= 0) return;  // no barriers in this kernel
+  if (n_iter <= 0) return;  // no barriers in this kernel
+  const GroupRef gr = group_ref(w, blockIdx.x, K);
 
-  const uint16_t* wp[WS];
-#pragma unroll
-  for (int s = 0; s < WS; ++s)
-    wp[s] = strip_base(w, min(j0 + s, n_strips - 1), K) + (int64_t)kbeg * 16 + lane * 8;
+  // Strip 2 wave + s, k-block kb of the group: gr.base + (kb * 8 + 2 wave + s) * 512.
+  const uint16_t* wp = gr.base + ((int64_t)(kbeg / 32) * 8 + 2 * wave) * 512 + lane * 8;
   const uint16_t* ap[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t)
@@ -88,8 +100,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(int M, int N, int K, int
   auto load = [&](int i, bf16x8(&wr)[WS][2], bf16x8(&ar)[MT][2]) {
 #pragma unroll
     for (int s = 0; s < WS; ++s) {
-      wr[s][0] = load_stream<bf16x8>(wp[s] + i * 1024);
-      wr[s][1] = load_stream<bf16x8>(wp[s] + i * 1024 + 512);
+      wr[s][0] = load_stream<bf16x8>(wp + (int64_t)(2 * i) * 4096 + s * 512);
+      wr[s][1] = load_stream<bf16x8>(wp + (int64_t)(2 * i + 1) * 4096 + s * 512);
     }
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
@@ -128,11 +140,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(int M, int N, int K, int
   for (int t = 0; t < MT; ++t)
 #pragma unroll
     for (int s = 0; s < WS; ++s) {
-      const int col = (j0 + s) * 16 + c16;
+      const int col = gr.col0 + (2 * wave + s) * 16 + c16;
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int row = t * 16 + 4 * q4 + rr;
-        if (row < M && col < N) o[(int64_t)row * N + col] = acc[t][s][rr];
+        if (row < M && col < gr.col_end) o[(int64_t)row * N + col] = acc[t][s][rr];
       }
     }
 }
@@ -144,9 +156,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(int M, int N, int K, int
 // register staging), through a ring of three stages: while step it is
 // computed, steps it+1 and it+2 are in flight.  One barrier per step: after
 // it, every wave has finished step it-1, whose stage then takes step it+2.
-// The W tile is 8 strips x 2 blocks, copied in packed order (eight 2 KiB runs
-// from HBM; fragment reads from LDS are linear, hence free of bank
-// conflicts); the A tile is row-major with its 16-byte chunks XOR-swizzled by
+// The W tile (one packed group, 2 k-blocks x 8 strips) is one contiguous
+// 16 KiB run in HBM, copied in packed order (fragment reads from LDS are
+// linear, hence free of bank conflicts); the A tile is row-major with its
+// 16-byte chunks XOR-swizzled by
 // row (the swizzle is applied to the source address, as the DMA writes each
 // wave's 64 chunks contiguously).  WM = 4 covers 256 rows, so up to that
 // batch size W is read from HBM exactly once per step.  Larger batches take
@@ -179,9 +192,9 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
   const int kbeg = blockIdx.z * k_split;
   const int n_iter = (min(K, kbeg + k_split) - kbeg) / 64;
   if (n_iter <= 0) return;
-  const int m_blk = mb * ROWS, n_blk = nb * 128;
+  const int m_blk = mb * ROWS;
   const int wm = wave >> 1, wn = wave & 1;
-  const int n_strips = (N + 15) / 16;
+  const GroupRef gr = group_ref(w, nb, K);
 
   // Chunk id = j * THREADS + tid lands at LDS chunk id of the stage (the DMA
   // of wave w, load j, fills chunks j * THREADS + 64 w .. +63).  A: chunk id
@@ -192,13 +205,12 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
     const int id = j * THREADS + tid, r = id >> 3, slot = id & 7;
     asrc[j] = A + (int64_t)min(m_blk + r, M - 1) * lda + kbeg + ((slot ^ (r & 7)) * 8);
   }
+  // W: chunk id of step i is chunk id of the step's 16 KiB run (k-block
+  // 2i + (id >> 9), strip (id >> 6) & 7, lane id & 63).
   const uint16_t* wsrc[WCH];
 #pragma unroll
-  for (int j = 0; j < WCH; ++j) {
-    const int id = j * THREADS + tid;  // strip id >> 7 of the tile
-    wsrc[j] = strip_base(w, min(nb * 8 + (id >> 7), n_strips - 1), K) + (int64_t)kbeg * 16 +
-              (id & 127) * 8;
-  }
+  for (int j = 0; j < WCH; ++j)
+    wsrc[j] = gr.base + (int64_t)(kbeg / 32) * 4096 + (j * THREADS + tid) * 8;
   int aoff[MT][2];
 #pragma unroll
   for (int t = 0; t < MT; ++t)
@@ -219,7 +231,7 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
 #pragma unroll
     for (int j = 0; j < ACH; ++j) dma16(asrc[j] + i * 64, base + j * THREADS * 8);
 #pragma unroll
-    for (int j = 0; j < WCH; ++j) dma16(wsrc[j] + i * 1024, base + SA + j * THREADS * 8);
+    for (int j = 0; j < WCH; ++j) dma16(wsrc[j] + (int64_t)i * 8192, base + SA + j * THREADS * 8);
   };
   auto compute = [&](int b) {
     const uint16_t* la = stage_ptr(b);
@@ -231,7 +243,7 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
       for (int t = 0; t < MT; ++t) af[t] = *(const bf16x8*)(la + aoff[t][h]);
 #pragma unroll
       for (int t = 0; t < NT; ++t)
-        bf[t] = *(const bf16x8*)(lw + (((wn * 4 + t) * 2 + h) * 64 + lane) * 8);
+        bf[t] = *(const bf16x8*)(lw + ((h * 8 + wn * 4 + t) * 64 + lane) * 8);
 #pragma unroll
       for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -275,11 +287,11 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
   for (int i = 0; i < MT; ++i)
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
-      const int col = n_blk + wn * 64 + j * 16 + c16;
+      const int col = gr.col0 + wn * 64 + j * 16 + c16;
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int row = m_blk + wm * 64 + i * 16 + 4 * q4 + rr;
-        if (row < M && col < N) o[(int64_t)row * N + col] = acc[i][j][rr];
+        if (row < M && col < gr.col_end) o[(int64_t)row * N + col] = acc[i][j][rr];
       }
     }
 }
@@ -355,13 +367,9 @@ int gemm_plan_splits(int dtype, int M, int N, int K, int* k_split) {
   const int ksteps = (K + kq - 1) / kq;
   int s = 1;
   if (dtype == 1) {
-    int64_t groups;
-    if (M <= kStreamMaxRows) {
-      groups = ((N + 15) / 16 + 7) / 8;  // 4 waves x 2 strips
-    } else {
-      const int rows = tile_rows(M);
-      groups = (int64_t)((N + 127) / 128) * ((M + rows - 1) / rows);
-    }
+    // Work groups per split: one per 128-column group (times the M-blocks).
+    int64_t groups = (N + kGroupCols - 1) / kGroupCols;
+    if (M > kStreamMaxRows) groups *= (M + tile_rows(M) - 1) / tile_rows(M);
     // Measured on the 8B shapes with weights streamed from HBM: the best
     // split count fills one round of work groups on the 256 CUs (a partial
     // second round costs 15-30%).
@@ -382,27 +390,35 @@ hipError_t launch_pack_weight(int dtype, int N, int K, const void* w, void* pack
   if (N <= 0 || K <= 0) return hipSuccess;
   if (dtype != 1)
     return hipMemcpyAsync(packed, w, (size_t)N * K * 4, hipMemcpyDeviceToDevice, stream);
-  const int64_t chunks = (int64_t)((N + 15) / 16) * (K / 32) * 64;
+  const int64_t chunks = (int64_t)((N + kGroupCols - 1) / kGroupCols) * (K / 32) * 8 * 64;
   pack_weight_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, stream>>>(
       (const uint16_t*)w, N, K, (uint16_t*)packed);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t lda,
-                       const WSegs& w, float* out, int splits, int k_split, hipStream_t stream) {
+                       const WSegs& w_in, float* out, int splits, int k_split, hipStream_t stream) {
   if (M <= 0 || N <= 0) return hipSuccess;
   const dim3 block(256);
   if (dtype == 1) {
+    // Each segment is padded to whole groups; count them.
+    WSegs w = w_in;
+    int start = 0, n_groups = 0;
+    for (int s = 0; s < w.n_seg; ++s) {
+      n_groups += (w.row_end[s] - start + kGroupCols - 1) / kGroupCols;
+      w.grp_end[s] = n_groups;
+      start = w.row_end[s];
+    }
     const uint16_t* a = (const uint16_t*)A;
     if (M <= kStreamMaxRows) {
-      const dim3 grid(((N + 15) / 16 + 7) / 8, 1, splits);
+      const dim3 grid(n_groups, 1, splits);
       if (M <= 16)
-        gemm_bf16_stream<1, 2, 2><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out);
+        gemm_bf16_stream<1, 2><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out);
       else
-        gemm_bf16_stream<2, 2, 2><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out);
+        gemm_bf16_stream<2, 2><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out);
     } else {
       const int rows = tile_rows(M);
-      const int n_mb = (M + rows - 1) / rows, n_nb = (N + 127) / 128;
+      const int n_mb = (M + rows - 1) / rows, n_nb = n_groups;
       const dim3 grid(((n_nb + 7) / 8) * 8 * n_mb, 1, splits);
       if (rows == 128)
         gemm_bf16_tile<2><<<grid, dim3(256), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a, lda,
@@ -413,7 +429,8 @@ hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t ld
     }
   } else {
     const dim3 grid((N + 63) / 64, (M + 31) / 32, splits);
-    gemm_f32_tiled<<<grid, block, 0, stream>>>(M, N, K, k_split, (const float*)A, lda, w, out);
+    gemm_f32_tiled<<<grid, block, 0, stream>>>(M, N, K, k_split, (const float*)A, lda, w_in,
+                                               out);
   }
   return hipGetLastError();
 }

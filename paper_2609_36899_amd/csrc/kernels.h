@@ -12,10 +12,14 @@ namespace pdec {
 
 // Weight matrix made of up to 3 row segments stacked along N (e.g. q|k|v or
 // gate|up).  Segment s covers output columns [row_end[s-1], row_end[s]).
+// bf16 segments are packed separately, each padded to whole 128-column
+// groups; grp_end[s] counts the groups of segments 0..s (launch_gemm fills
+// it from row_end).
 struct WSegs {
   const void* ptr[3];
   int32_t row_end[3];
   int32_t n_seg;
+  int32_t grp_end[3];
 };
 
 // ---- attention --------------------------------------------------------------

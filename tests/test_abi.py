@@ -63,8 +63,9 @@ def test_host_only_calls_without_gpu():
     assert lib.kv_bytes_per_token(byref(qk)) == 2048
     qk.qk_norm = 2
     assert lib.kv_bytes_per_token(byref(qk)) == N.INVALID_ARG
-    # packed weight sizes: bf16 pads N to whole 16-column strips, fp32 is row-major
-    assert lib.packed_weight_bytes(N.BF16, 100, 128) == 112 * 128 * 2
+    # packed weight sizes: bf16 pads N to whole 128-column groups, fp32 is row-major
+    assert lib.packed_weight_bytes(N.BF16, 100, 128) == 128 * 128 * 2
+    assert lib.packed_weight_bytes(N.BF16, 129, 64) == 256 * 64 * 2
     assert lib.packed_weight_bytes(N.BF16, 128256, 4096) == 128256 * 4096 * 2
     assert lib.packed_weight_bytes(N.F32, 100, 96) == 100 * 96 * 4
     assert lib.packed_weight_bytes(N.BF16, 100, 96) == N.UNSUPPORTED  # K % 64

@@ -2,7 +2,7 @@
 
 Covers every kernel the planner picks: the weight-streaming MFMA kernel (one
 and two 16-row tiles), the 128-row and 256-row MFMA tiles, split-K, ragged M
-and N (a zero-padded last strip of the packed weight).  Inputs are
+and N (a zero-padded last group of the packed weight).  Inputs are
 bf16-representable values, so the only difference from the float64 product
 is fp32 accumulation: per row, max|gpu - ref| <= 1e-4 * max|ref|.
 The packed layout itself is checked element by element against its
@@ -57,24 +57,25 @@ def test_f32(M):
     _run(M, 688, 256, bf16=False, seed=M)
 
 
-@pytest.mark.parametrize("N,K", [(64, 64), (1412, 576), (40, 128)])
+@pytest.mark.parametrize("N,K", [(64, 64), (1412, 576), (40, 128), (256, 64)])
 def test_pack_layout(N, K):
-    """Element (n, k) sits at ((j*K/32 + b)*64 + q*16 + c)*8 + e with n = 16j + c,
-    k = 32b + 8q + e; the columns of the padded last strip are zero."""
+    """Element (n, k) sits at (((G*K/32 + b)*8 + s)*64 + q*16 + c)*8 + e with
+    n = 128G + 16s + c, k = 32b + 8q + e; the columns of the padded last group
+    are zero."""
     import paper_2609_36899_amd as P
     w = np.arange(N * K, dtype=np.int64).reshape(N, K) % 65521
     wd = torch.from_numpy(w.astype(np.int16)).cuda().view(torch.bfloat16)
     pw = P.pack_weight(wd.contiguous())
     torch.cuda.synchronize()
     got = pw.data.view(torch.int16).cpu().numpy().astype(np.int64) % 65536
-    n_strips = (N + 15) // 16
-    assert got.size == n_strips * 16 * K
-    expect = np.zeros(n_strips * 16 * K, dtype=np.int64)
+    n_groups = (N + 127) // 128
+    assert got.size == n_groups * 128 * K
+    expect = np.zeros(n_groups * 128 * K, dtype=np.int64)
     for n in range(N):
-        j, c = divmod(n, 16)
+        G, r = divmod(n, 128)
+        s, c = divmod(r, 16)
         for k in range(K):
-            b, r = divmod(k, 32)
-            q, e = divmod(r, 8)
-            expect[((j * (K // 32) + b) * 64 + q * 16 + c) * 8 + e] = w[n, k] % 65536
+            b, r2 = divmod(k, 32)
+            q, e = divmod(r2, 8)
+            expect[(((G * (K // 32) + b) * 8 + s) * 64 + q * 16 + c) * 8 + e] = w[n, k] % 65536
     np.testing.assert_array_equal(got, expect)
-
