@@ -86,8 +86,12 @@ struct QBlockSpec {
   int32_t q_row0, n_q, slot, pos0;
 };
 
-// Work groups the attention split pass aims for (four waves each).
-constexpr int64_t kDecodeTargetGroups = 4096;
+// Work groups the attention split pass aims for (four waves each).  Decode:
+// six per CU, i.e. two rounds at the kernel's three resident groups per CU;
+// measured against 1024..8192 on the 8B decode shapes (B = 8..256), fewer
+// groups leave long-context batches unbalanced and more groups pay the
+// per-item query load, partial write and combine.
+constexpr int64_t kDecodeTargetGroups = 1536;
 constexpr int64_t kPrefillTargetGroups = 2048;
 
 // Items per KV head the planner aims for.
