@@ -157,15 +157,21 @@ int engine_set_stream(pdec_engine* engine, void* stream);
 
 /* Launch timing for measurement.  engine_profile(engine, classes) takes a
  * bitmask of the classes below ((1 << PDEC_TIMER_ATTENTION) | ...; 0 turns
- * timing off).  Every launch of a selected class is bracketed by a pair of HIP
- * events on the engine's stream (each pair adds a few microseconds to the
- * step, so select only what is being measured); engine_profile_read
- * synchronises on them and returns the summed elapsed time (ms) and the
- * launch count of one class, clearing those records. */
+ * timing off).  A timed launch records its own begin and end in a pair of
+ * HIP events (hipExtLaunchKernelGGL), which still leaves the GPU idle for a
+ * few microseconds around that launch, so select only what is being
+ * measured.  engine_profile_every(engine, every) times one launch in every
+ * `every` of each selected class (launches counted per class from this call;
+ * every >= 1, default 1 = all); with every = n_layers + 1 a decode step
+ * carries about one timed launch and the timed layer rotates from step to
+ * step.  engine_profile_read synchronises on the events and returns the
+ * summed elapsed time (ms) and the count of timed launches of one class,
+ * clearing those records. */
 #define PDEC_TIMER_ATTENTION 0 /* paged split-K attention pass, one per layer */
 #define PDEC_TIMER_GEMM 1      /* the four weight projections of each layer */
 #define PDEC_TIMER_LM_HEAD 2   /* the LM-head projection */
 int engine_profile(pdec_engine* engine, int32_t classes);
+int engine_profile_every(pdec_engine* engine, int32_t every);
 int engine_profile_read(pdec_engine* engine, int32_t kind, double* total_ms, int64_t* launches);
 
 /* Admit an empty trajectory and reserve ceil(reserve_tokens / 16) pages for

@@ -66,6 +66,7 @@ SIGNATURES = {
     "engine_destroy": (None, [c_void_p]),
     "engine_set_stream": (c_int32, [c_void_p, c_void_p]),
     "engine_profile": (c_int32, [c_void_p, c_int32]),
+    "engine_profile_every": (c_int32, [c_void_p, c_int32]),
     "engine_profile_read": (c_int32, [c_void_p, c_int32, POINTER(ctypes.c_double),
                                       POINTER(c_int64)]),
     "kv_alloc": (c_int32, [c_void_p, c_int32, POINTER(c_int32)]),

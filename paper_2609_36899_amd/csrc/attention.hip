@@ -475,16 +475,18 @@ hipError_t launch_attention_split(int dtype, int kv_fp8, float k_scale, float v_
                                   const AttnQBlock* qblocks, const void* q, const void* k_pages,
                                   const void* v_pages, int64_t page_stride_elems,
                                   const int32_t* block_table, int32_t bt_stride, float* part_ml,
-                                  float* part_acc, hipStream_t stream) {
+                                  float* part_acc, hipStream_t stream, hipEvent_t ev_start,
+                                  hipEvent_t ev_stop) {
   if (n_items == 0) return hipSuccess;
   const dim3 grid(n_kv_heads, n_items);
   const float scale_log2 = kLog2e / sqrtf((float)head_dim) * (kv_fp8 ? k_scale : 1.f);
   if (dtype == 1) {
     const uint16_t* qq = (const uint16_t*)q;
 #define PDEC_ATTN_BF16(DH_, RW_, PW_, KT_)                                                   \
-  attn_split_bf16<DH_, RW_, PW_, KT_><<<grid, dim3(64 * RW_ * PW_), 0, stream>>>(           \
-      items, qblocks, qq, (const KT_*)k_pages, (const KT_*)v_pages, page_stride_elems,       \
-      block_table, bt_stride, n_q_heads, n_kv_heads, scale_log2, v_scale, part_ml, part_acc)
+  return launch_timed(attn_split_bf16<DH_, RW_, PW_, KT_>, grid, dim3(64 * RW_ * PW_), stream,  \
+                      ev_start, ev_stop, items, qblocks, qq, (const KT_*)k_pages,             \
+                      (const KT_*)v_pages, page_stride_elems, block_table, bt_stride,         \
+                      n_q_heads, n_kv_heads, scale_log2, v_scale, part_ml, part_acc)
 #define PDEC_ATTN_KT(KT_)                                                                    \
   if (head_dim == 128) {                                                                     \
     if (rows_per_item == 64) PDEC_ATTN_BF16(128, 4, 1, KT_); else PDEC_ATTN_BF16(128, 1, 4, KT_); \
@@ -502,15 +504,15 @@ hipError_t launch_attention_split(int dtype, int kv_fp8, float k_scale, float v_
 #undef PDEC_ATTN_BF16
   } else {
     if (head_dim == 128)
-      attn_split_f32<128><<<grid, dim3(64), 0, stream>>>(
-          items, qblocks, (const float*)q, (const float*)k_pages, (const float*)v_pages,
-          page_stride_elems, block_table, bt_stride, n_q_heads, n_kv_heads, rows_per_item,
-          scale_log2, part_ml, part_acc);
+      return launch_timed(attn_split_f32<128>, grid, dim3(64), stream, ev_start, ev_stop, items,
+                          qblocks, (const float*)q, (const float*)k_pages,
+                          (const float*)v_pages, page_stride_elems, block_table, bt_stride,
+                          n_q_heads, n_kv_heads, rows_per_item, scale_log2, part_ml, part_acc);
     else
-      attn_split_f32<64><<<grid, dim3(64), 0, stream>>>(
-          items, qblocks, (const float*)q, (const float*)k_pages, (const float*)v_pages,
-          page_stride_elems, block_table, bt_stride, n_q_heads, n_kv_heads, rows_per_item,
-          scale_log2, part_ml, part_acc);
+      return launch_timed(attn_split_f32<64>, grid, dim3(64), stream, ev_start, ev_stop, items,
+                          qblocks, (const float*)q, (const float*)k_pages,
+                          (const float*)v_pages, page_stride_elems, block_table, bt_stride,
+                          n_q_heads, n_kv_heads, rows_per_item, scale_log2, part_ml, part_acc);
   }
   return hipGetLastError();
 }

@@ -108,35 +108,37 @@ class Staging {
 };
 
 // ---------------------------------------------------------------------------
-// Optional per-launch timing: event pairs around chosen launch classes.
+// Optional per-launch timing of chosen launch classes.  The launch records
+// the kernel's own begin and end into the pair (see launch_timed), so timing
+// adds no marker packets between kernels.
 // ---------------------------------------------------------------------------
 class LaunchTimer {
  public:
   ~LaunchTimer() { reset_pool(); }
   void enable(uint32_t mask) { mask_ = mask; }
-  bool on() const { return mask_ != 0; }
-  // Classes not in the mask push an empty record so that end() pairs up.
-  hipError_t begin(int kind, hipStream_t s) {
-    if (!mask_) return hipSuccess;
-    if (!(mask_ >> kind & 1u)) {
-      open_.push_back({-1, nullptr, nullptr});
-      return hipSuccess;
-    }
-    hipEvent_t a, b;
-    hipError_t e = take(&a);
-    if (e == hipSuccess) e = take(&b);
-    if (e == hipSuccess) e = hipEventRecord(a, s);
-    if (e != hipSuccess) return e;
-    open_.push_back({kind, a, b});
-    return hipSuccess;
+  // Time one launch in every `every` of each selected class.
+  void sample(int every) {
+    every_ = every;
+    for (int64_t& c : count_) c = 0;
   }
-  hipError_t end(hipStream_t s) {
-    if (!mask_ || open_.empty()) return hipSuccess;
-    Rec r = open_.back();
-    open_.pop_back();
-    if (r.kind < 0) return hipSuccess;
-    done_.push_back(r);
-    return hipEventRecord(r.b, s);
+  bool on() const { return mask_ != 0; }
+  // Events for one launch of class kind, or nulls when it is not timed.
+  hipError_t pair(int kind, hipEvent_t* a, hipEvent_t* b) {
+    *a = *b = nullptr;
+    if (!(mask_ >> kind & 1u)) return hipSuccess;
+    if (count_[kind]++ % every_ != 0) return hipSuccess;
+    hipEvent_t ea, eb;
+    hipError_t e = take(&ea);
+    if (e != hipSuccess) return e;
+    e = take(&eb);
+    if (e != hipSuccess) {
+      free_.push_back(ea);
+      return e;
+    }
+    done_.push_back({kind, ea, eb});
+    *a = ea;
+    *b = eb;
+    return hipSuccess;
   }
   // Sum of elapsed times (ms) and launch count of one kind; clears records.
   hipError_t read(int kind, double* ms, int64_t* count) {
@@ -182,10 +184,11 @@ class LaunchTimer {
     all_.clear();
     free_.clear();
     done_.clear();
-    open_.clear();
   }
   uint32_t mask_ = 0;
-  std::vector<Rec> open_, done_;
+  int every_ = 1;
+  int64_t count_[3] = {0, 0, 0};
+  std::vector<Rec> done_;
   std::vector<hipEvent_t> free_, all_;
 };
 
@@ -401,40 +404,36 @@ int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
                                 E->h, s));
   for (int l = 0; l < c.n_layers; ++l) {
     int ks, S;
+    hipEvent_t ea, eb;
     S = gemm_plan_splits(dt, M, nqkv, d, &ks);
-    HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_GEMM, s));
-    HIP_OR_FAIL(launch_gemm(dt, M, nqkv, d, E->h, d, E->w_qkv[l], E->part, S, ks, s));
-    HIP_OR_FAIL(E->timer.end(s));
+    HIP_OR_FAIL(E->timer.pair(PDEC_TIMER_GEMM, &ea, &eb));
+    HIP_OR_FAIL(launch_gemm(dt, M, nqkv, d, E->h, d, E->w_qkv[l], E->part, S, ks, s, ea, eb));
     HIP_OR_FAIL(launch_qkv_rope_kv(dt, c.kv_fp8, c.kv_scale_k, c.kv_scale_v, M, Dh, c.n_q_heads,
                                    c.n_kv_heads, E->part, S, d_rows,
                                    E->rope_cs, E->bt, E->ws.bt_stride, E->q, E->k_layer(l),
                                    E->v_layer(l), E->page_stride,
                                    c.qk_norm ? E->q_norm[l] : nullptr,
                                    c.qk_norm ? E->k_norm[l] : nullptr, c.rms_eps, s));
-    HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_ATTENTION, s));
+    HIP_OR_FAIL(E->timer.pair(PDEC_TIMER_ATTENTION, &ea, &eb));
     HIP_OR_FAIL(launch_attention_split(dt, c.kv_fp8, c.kv_scale_k, c.kv_scale_v, Dh, rows_per_item,
                                        n_items, c.n_q_heads, c.n_kv_heads,
                                        d_it, d_qb,
                                        E->q, E->k_layer(l), E->v_layer(l), E->page_stride, E->bt,
-                                       E->ws.bt_stride, E->att_ml, E->att_acc, s));
-    HIP_OR_FAIL(E->timer.end(s));
+                                       E->ws.bt_stride, E->att_ml, E->att_acc, s, ea, eb));
     HIP_OR_FAIL(launch_attention_combine(Dh, rows_per_item, n_qb, max_items, c.n_q_heads,
                                          c.n_kv_heads, d_qb, E->att_ml, E->att_acc, E->o,
                                          dt == PDEC_BF16, s));
     S = gemm_plan_splits(dt, M, d, qd, &ks);
-    HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_GEMM, s));
-    HIP_OR_FAIL(launch_gemm(dt, M, d, qd, E->o, qd, E->w_o[l], E->part, S, ks, s));
-    HIP_OR_FAIL(E->timer.end(s));
+    HIP_OR_FAIL(E->timer.pair(PDEC_TIMER_GEMM, &ea, &eb));
+    HIP_OR_FAIL(launch_gemm(dt, M, d, qd, E->o, qd, E->w_o[l], E->part, S, ks, s, ea, eb));
     HIP_OR_FAIL(launch_resid_norm(dt, M, d, E->part, S, E->x, E->ffn_norm[l], c.rms_eps, E->h, s));
     S = gemm_plan_splits(dt, M, 2 * F, d, &ks);
-    HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_GEMM, s));
-    HIP_OR_FAIL(launch_gemm(dt, M, 2 * F, d, E->h, d, E->w_gu[l], E->part, S, ks, s));
-    HIP_OR_FAIL(E->timer.end(s));
+    HIP_OR_FAIL(E->timer.pair(PDEC_TIMER_GEMM, &ea, &eb));
+    HIP_OR_FAIL(launch_gemm(dt, M, 2 * F, d, E->h, d, E->w_gu[l], E->part, S, ks, s, ea, eb));
     HIP_OR_FAIL(launch_swiglu(dt, M, F, E->part, S, E->u, s));
     S = gemm_plan_splits(dt, M, d, F, &ks);
-    HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_GEMM, s));
-    HIP_OR_FAIL(launch_gemm(dt, M, d, F, E->u, F, E->w_down[l], E->part, S, ks, s));
-    HIP_OR_FAIL(E->timer.end(s));
+    HIP_OR_FAIL(E->timer.pair(PDEC_TIMER_GEMM, &ea, &eb));
+    HIP_OR_FAIL(launch_gemm(dt, M, d, F, E->u, F, E->w_down[l], E->part, S, ks, s, ea, eb));
     const float* next_gain = (l + 1 < c.n_layers) ? E->attn_norm[l + 1] : E->final_norm;
     HIP_OR_FAIL(launch_resid_norm(dt, M, d, E->part, S, E->x, next_gain, c.rms_eps, E->h, s));
   }
@@ -444,9 +443,10 @@ int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
     lm.row_end[0] = c.vocab;
     lm.n_seg = 1;
     const char* a = E->h + (lm_last_only ? (int64_t)(M - 1) * d * E->ab() : 0);
-    HIP_OR_FAIL(E->timer.begin(PDEC_TIMER_LM_HEAD, s));
-    HIP_OR_FAIL(launch_gemm(dt, lm_last_only ? 1 : M, c.vocab, d, a, d, lm, logits, 1, d, s));
-    HIP_OR_FAIL(E->timer.end(s));
+    hipEvent_t ea, eb;
+    HIP_OR_FAIL(E->timer.pair(PDEC_TIMER_LM_HEAD, &ea, &eb));
+    HIP_OR_FAIL(launch_gemm(dt, lm_last_only ? 1 : M, c.vocab, d, a, d, lm, logits, 1, d, s, ea,
+                            eb));
   }
   return PDEC_OK;
 }
@@ -598,6 +598,13 @@ void engine_destroy(pdec_engine* E) {
 int engine_profile(pdec_engine* E, int32_t classes) {
   if (!E) return fail(PDEC_INVALID_ARG, "null engine");
   E->timer.enable((uint32_t)classes & 7u);
+  return PDEC_OK;
+}
+
+int engine_profile_every(pdec_engine* E, int32_t every) {
+  if (!E) return fail(PDEC_INVALID_ARG, "null engine");
+  if (every < 1) return fail(PDEC_INVALID_ARG, "every must be >= 1");
+  E->timer.sample(every);
   return PDEC_OK;
 }
 

@@ -397,7 +397,8 @@ hipError_t launch_pack_weight(int dtype, int N, int K, const void* w, void* pack
 }
 
 hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t lda,
-                       const WSegs& w_in, float* out, int splits, int k_split, hipStream_t stream) {
+                       const WSegs& w_in, float* out, int splits, int k_split, hipStream_t stream,
+                       hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (M <= 0 || N <= 0) return hipSuccess;
   const dim3 block(256);
   if (dtype == 1) {
@@ -413,24 +414,24 @@ hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t ld
     if (M <= kStreamMaxRows) {
       const dim3 grid(n_groups, 1, splits);
       if (M <= 16)
-        gemm_bf16_stream<1, 2><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out);
-      else
-        gemm_bf16_stream<2, 2><<<grid, block, 0, stream>>>(M, N, K, k_split, a, lda, w, out);
+        return launch_timed(gemm_bf16_stream<1, 2>, grid, block, stream, ev_start, ev_stop, M, N,
+                            K, k_split, a, lda, w, out);
+      return launch_timed(gemm_bf16_stream<2, 2>, grid, block, stream, ev_start, ev_stop, M, N,
+                          K, k_split, a, lda, w, out);
     } else {
       const int rows = tile_rows(M);
       const int n_mb = (M + rows - 1) / rows, n_nb = n_groups;
       const dim3 grid(((n_nb + 7) / 8) * 8 * n_mb, 1, splits);
       if (rows == 128)
-        gemm_bf16_tile<2><<<grid, dim3(256), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a, lda,
-                                                            w, out);
-      else
-        gemm_bf16_tile<4><<<grid, dim3(512), 0, stream>>>(M, N, K, k_split, n_mb, n_nb, a, lda,
-                                                            w, out);
+        return launch_timed(gemm_bf16_tile<2>, grid, dim3(256), stream, ev_start, ev_stop, M, N,
+                            K, k_split, n_mb, n_nb, a, lda, w, out);
+      return launch_timed(gemm_bf16_tile<4>, grid, dim3(512), stream, ev_start, ev_stop, M, N, K,
+                          k_split, n_mb, n_nb, a, lda, w, out);
     }
   } else {
     const dim3 grid((N + 63) / 64, (M + 31) / 32, splits);
-    gemm_f32_tiled<<<grid, block, 0, stream>>>(M, N, K, k_split, (const float*)A, lda, w_in,
-                                               out);
+    return launch_timed(gemm_f32_tiled, grid, block, stream, ev_start, ev_stop, M, N, K, k_split,
+                        (const float*)A, lda, w_in, out);
   }
   return hipGetLastError();
 }

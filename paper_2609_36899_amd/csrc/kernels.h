@@ -35,7 +35,8 @@ hipError_t launch_attention_split(int dtype, int kv_fp8, float k_scale, float v_
                                   const AttnQBlock* qblocks, const void* q, const void* k_pages,
                                   const void* v_pages, int64_t page_stride_elems,
                                   const int32_t* block_table, int32_t bt_stride, float* part_ml,
-                                  float* part_acc, hipStream_t stream);
+                                  float* part_acc, hipStream_t stream,
+                                  hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 
 // Merge pass: one work group per (query block, KV head); writes
 // out [rows][n_q_heads][head_dim] as fp32 (out_bf16 = 0) or bf16.
@@ -48,13 +49,16 @@ hipError_t launch_attention_combine(int head_dim, int rows_per_item, int n_qbloc
 // ---- projections ------------------------------------------------------------
 // out[s][m][n] = sum_{k in split s} A[m][k] * W[n][k]  (fp32 partial sums).
 // bf16: A and W bf16, K % 64 == 0, k_split % 64 == 0.  f32: any sizes.
+// Launchers taking ev_start/ev_stop record the kernel's own begin and end in
+// them when given (timing without marker packets between kernels).
 hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t lda,
-                       const WSegs& w, float* out, int splits, int k_split, hipStream_t stream);
+                       const WSegs& w, float* out, int splits, int k_split, hipStream_t stream,
+                       hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 // Temperature / top-p sampling (sample.hip).
 hipError_t launch_sample_top_p(int B, int V, const float* logits, float temperature, float top_p,
                                const float* uniforms, int32_t* tokens, hipStream_t stream);
-// bf16: pack a row-major [N][K] weight into the strip layout the GEMM kernels
-// read (((N + 15) / 16) * 16 * K elements); fp32: plain copy.
+// bf16: pack a row-major [N][K] weight into the group-major layout the GEMM
+// kernels read (((N + 127) / 128) * 128 * K elements); fp32: plain copy.
 hipError_t launch_pack_weight(int dtype, int N, int K, const void* w, void* packed,
                               hipStream_t stream);
 // Number of K splits the launcher plans for this shape (and the split size).

@@ -174,12 +174,14 @@ class Engine:
         return self._pool_view()[layer, 1].view(self.n_pages, s.n_kv_heads, s.head_dim,
                                                 PAGE_TOKENS)
 
-    def profile(self, kinds: Sequence[int] = ()) -> None:
-        """Bracket the launches of the given timer classes (N.TIMER_*) with HIP
-        events; an empty sequence turns timing off (see engine_profile)."""
+    def profile(self, kinds: Sequence[int] = (), every: int = 1) -> None:
+        """Time the launches of the given timer classes (N.TIMER_*), one in
+        every `every` of each; an empty sequence turns timing off (see
+        engine_profile, engine_profile_every)."""
         mask = 0
         for k in kinds:
             mask |= 1 << int(k)
+        N.check(self.lib.engine_profile_every(self.handle, int(every)))
         N.check(self.lib.engine_profile(self.handle, mask))
 
     def profile_read(self, kind: int):
