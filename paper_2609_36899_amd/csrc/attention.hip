@@ -327,6 +327,237 @@ __attribute__((amdgpu_waves_per_eu(sizeof(KT) == 1 ? 2 : 3))) void attn_split_bf
 }
 
 // ---------------------------------------------------------------------------
+// Prefill, bf16 pages.  A work group of 4 waves takes one (item, KV head) of
+// a 64-row query block (16/G queries x G heads per 16 rows); wave w owns rows
+// 16w .. 16w+15.  All four waves need every key of the item, so the pages
+// pass through LDS two at a time (a stage: K of both pages, then V^T of
+// both), fetched by LDS-DMA into a ring of four stages and read from there by
+// every wave: each page crosses L2 once per work group rather than once per
+// wave, and two stages stay in flight while one is used.  The math per page
+// pair is the split kernel's (S^T = K Q^T, online softmax, O^T = V^T P^T).
+//
+// K rows in LDS: the 16-byte chunk j of key k of page p sits in slot
+// j ^ kswz(k, p), so that the lanes of one fragment read (8 or 16 keys of the
+// same chunk column) hit distinct banks; the swizzle goes on the DMA's source
+// address.  V^T blocks are copied as they are (a fragment read covers 16
+// dims x 32 bytes, already conflict-free).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int kswz(int k, int p) {
+  return (k & 3) | (((k >> 3) & 1) << 2) | (p << 3);  // < 16 chunks per 128-dim key row
+}
+
+template <int DH>  // 128
+__global__ __launch_bounds__(256) void attn_prefill_bf16(
+    const AttnItem* __restrict__ items, const AttnQBlock* __restrict__ qblocks,
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
+    const uint16_t* __restrict__ vpool, int64_t page_stride, const int32_t* __restrict__ bt,
+    int32_t bt_stride, int32_t n_q_heads, int32_t n_kv_heads, float scale_log2,
+    float* __restrict__ part_ml, float* __restrict__ part_acc) {
+  constexpr int KC = DH / 32;   // k-steps of QK^T
+  constexpr int DT = DH / 16;   // 16-wide dim tiles of PV
+  constexpr int R = 64;         // query rows per item
+  constexpr int BLK = kPage * DH;          // elements of one page's K (or V^T) block
+  constexpr int STAGE = 4 * BLK;           // K0 K1 V0 V1
+  constexpr int CPK = DH / 8;              // 16-byte chunks per K row
+  constexpr int LPT = STAGE * 2 / 16 / 256;  // DMA loads per thread per stage
+  constexpr int D = 4;
+  static_assert(DH == 128, "the K swizzle spans 16 chunks per key row");
+  static_assert(LPT * 256 * 8 == STAGE, "stage is a whole number of loads");
+  __shared__ __attribute__((aligned(16))) uint16_t st0[STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t st1[STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t st2[STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t st3[STAGE];
+  auto stage_ptr = [&](int b) -> uint16_t* { return b == 0 ? st0 : b == 1 ? st1 : b == 2 ? st2 : st3; };
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int c16 = lane & 15, q4 = lane >> 4;
+  const int g = blockIdx.x, item_id = items[blockIdx.y].order;
+  const AttnItem it = items[item_id];
+  const AttnQBlock qb = qblocks[it.qblock];
+  const int G = n_q_heads / n_kv_heads;
+
+  // This lane's query row.  Waves without rows still take part in the
+  // stage loads and barriers; their results are not written.
+  const int row = wave * 16 + c16;
+  const int jq = row / G;
+  const int head = g * G + (row % G);
+  const bool row_valid = jq < qb.n_q;
+  bf16x8 qf[KC];
+  if (row_valid) {
+    const uint16_t* qrow = q + ((int64_t)(qb.q_row0 + jq) * n_q_heads + head) * DH;
+#pragma unroll
+    for (int c = 0; c < KC; ++c) qf[c] = *(const bf16x8*)(qrow + c * 32 + q4 * 8);
+  } else {
+#pragma unroll
+    for (int c = 0; c < KC; ++c) qf[c] = bf16x8{};
+  }
+
+  const int key0 = it.page_begin * kPage;
+  const int key_end = (it.page_begin + it.n_pages) * kPage;
+  const int kv_lim = min(qb.pos0 + qb.n_q, key_end);  // keys at or past it hold no data
+  const int row_lim = row_valid ? min(qb.pos0 + jq + 1, key_end) : key0;
+  const int32_t* btrow = bt + (int64_t)qb.slot * bt_stride + it.page_begin;
+  const int64_t head_off = (int64_t)g * BLK;
+  const int n_st = (it.n_pages + 1) >> 1;
+  const int last = n_st - 1;
+
+  // DMA: load j of a stage fills chunks j*256 + tid (block b = chunk / (2*CPK*... )).
+  int src_off[LPT];
+  int src_blk[LPT];
+#pragma unroll
+  for (int j = 0; j < LPT; ++j) {
+    const int x = j * 256 + tid;
+    const int b = x / (BLK / 8), cc = x % (BLK / 8);
+    src_blk[j] = b;
+    if (b < 2) {
+      const int k = cc / CPK, slot = cc % CPK;
+      src_off[j] = k * DH + ((slot ^ kswz(k, b)) * 8);
+    } else {
+      src_off[j] = cc * 8;
+    }
+  }
+  // The stage's two page numbers are read with uniform indices (scalar
+  // loads): a per-lane page-table read would be a vector load, and waiting
+  // for it would also wait for every stage in flight (loads retire in order).
+  auto issue = [&](int st, int buf) {
+    uint16_t* base = stage_ptr(buf) + wave * 64 * 8;
+    const int page_a = btrow[2 * st];
+    const int page_b = btrow[min(2 * st + 1, it.n_pages - 1)];  // missing: a valid page, masked
+    const int64_t base_a = (int64_t)page_a * page_stride + head_off;
+    const int64_t base_b = (int64_t)page_b * page_stride + head_off;
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) {
+      const int b = src_blk[j];
+      const uint16_t* src = (b < 2 ? kpool : vpool) + ((b & 1) ? base_b : base_a) + src_off[j];
+      dma16(src, base + j * 256 * 8);
+    }
+  };
+
+  // Lane-constant fragment offsets (as in the split kernel).
+  const int k_tok = 8 * ((c16 >> 2) & 1) + (c16 & 3);  // + 4u
+  const int k_page_sel = c16 >> 3;
+  const int v_page_sel = q4 >> 1;
+  const int v_tok0 = 8 * (q4 & 1);
+
+  float m = -INFINITY, l = 0.f;
+  f32x4 acc[DT];
+#pragma unroll
+  for (int t = 0; t < DT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](int st, int buf) {
+    const uint16_t* sb = stage_ptr(buf);
+    bf16x8 kf[2][KC];
+    u16x8 vf[DT];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int k = k_tok + 4 * u;
+      const uint16_t* kr = sb + k_page_sel * BLK + k * DH;
+#pragma unroll
+      for (int c = 0; c < KC; ++c)
+        kf[u][c] = *(const bf16x8*)(kr + (((4 * c + q4) ^ kswz(k, k_page_sel)) * 8));
+    }
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+      vf[t] = *(const u16x8*)(sb + (2 + v_page_sel) * BLK + (t * 16 + c16) * kPage + v_tok0);
+
+    f32x4 s[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      s[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < KC; ++c)
+        s[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[u][c], qf[c], s[u], 0, 0, 0);
+    }
+    const int kbase = key0 + (2 * st + v_page_sel) * kPage + v_tok0;
+    float sv[8];
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int e = 4 * u + rr;
+        const float x = (kbase + e < row_lim) ? s[u][rr] * scale_log2 : -INFINITY;
+        sv[e] = x;
+        mloc = fmaxf(mloc, x);
+      }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+    const float m_new = fmaxf(m, mloc);
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    if (__any(m_new != m)) {
+      const float alpha = __builtin_amdgcn_exp2f(m - m_use);
+      l *= alpha;
+#pragma unroll
+      for (int t = 0; t < DT; ++t) acc[t] *= alpha;
+    }
+    m = m_new;
+    uint32_t pw4[4];
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const f32x2 pv = {__builtin_amdgcn_exp2f(sv[e] - m_use),
+                        __builtin_amdgcn_exp2f(sv[e + 1] - m_use)};
+      const uint32_t bits = __builtin_bit_cast(uint32_t, __builtin_convertvector(pv, bf16x2));
+      pw4[e / 2] = bits;
+      l += __uint_as_float(bits << 16) + __uint_as_float(bits & 0xFFFF0000u);
+    }
+    const bf16x8 pf = __builtin_bit_cast(bf16x8, u32x4{pw4[0], pw4[1], pw4[2], pw4[3]});
+    if (__builtin_expect(key0 + (2 * st + 2) * kPage > kv_lim, 0)) {  // the block's last keys
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (kbase + e >= kv_lim)
+#pragma unroll
+          for (int t = 0; t < DT; ++t) vf[t][e] = 0;
+    }
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[t]), pf,
+                                                       acc[t], 0, 0, 0);
+  };
+
+  // Ring of D stages, two in flight while one is used (stage indices
+  // clamped to the last, so every step issues one stage and the count of
+  // loads in flight is fixed).  After the barrier of step st every wave has
+  // finished step st-1, whose stage then takes step st+3.
+#pragma unroll
+  for (int b = 0; b < D - 1; ++b) issue(min(b, last), b);
+  int st = 0;
+  for (; st + D <= n_st; st += D) {
+#pragma unroll
+    for (int b = 0; b < D; ++b) {
+      wait_vmem<(D - 2) * LPT>();
+      wg_barrier();
+      issue(min(st + b + D - 1, last), (b + D - 1) % D);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(st + b, b);
+    }
+  }
+  const int tail = n_st - st;  // uniform over the work group
+#pragma unroll
+  for (int b = 0; b < D; ++b)
+    if (b < tail) {
+      wait_vmem<(D - 2) * LPT>();
+      wg_barrier();
+      issue(min(st + b + D - 1, last), (b + D - 1) % D);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(st + b, b);
+    }
+  wait_vmem<0>();  // no LDS write may still be in flight when the group ends
+
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  if (row_valid) {
+    const int64_t prow = ((int64_t)item_id * n_kv_heads + g) * R + row;
+    if (q4 == 0) {
+      part_ml[prow * 2] = m;
+      part_ml[prow * 2 + 1] = l;
+    }
+    float* pa = part_acc + prow * DH;
+#pragma unroll
+    for (int t = 0; t < DT; ++t) *(f32x4*)(pa + t * 16 + 4 * q4) = acc[t];
+  }
+}
+
+// ---------------------------------------------------------------------------
 // fp32, VALU.  One wave per work group; lane = head dimension (DH/64 per
 // lane).  Rows and keys are walked one at a time: this path serves the small
 // fp32 decoder, where launches, not bytes, set the step time.
@@ -493,8 +724,15 @@ hipError_t launch_attention_split(int dtype, int kv_fp8, float k_scale, float v_
   } else {                                                                                   \
     if (rows_per_item == 64) PDEC_ATTN_BF16(64, 4, 1, KT_); else PDEC_ATTN_BF16(64, 1, 4, KT_); \
   }
-    // 64-row items (prefill): waves split rows.  16-row items (decode): waves
-    // split pages.
+    // 64-row items (prefill) with bf16 pages and 128-dim heads: the
+    // LDS-staged prefill kernel.
+    if (rows_per_item == 64 && !kv_fp8 && head_dim == 128)
+      return launch_timed(attn_prefill_bf16<128>, grid, dim3(256), stream, ev_start, ev_stop,
+                          items, qblocks, qq, (const uint16_t*)k_pages, (const uint16_t*)v_pages,
+                          page_stride_elems, block_table, bt_stride, n_q_heads, n_kv_heads,
+                          scale_log2, part_ml, part_acc);
+    // Other prefill (fp8 pages, 64-dim heads): waves split rows.  16-row
+    // items (decode): waves split pages.
     if (kv_fp8) {
       PDEC_ATTN_KT(uint8_t)
     } else {

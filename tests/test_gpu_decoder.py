@@ -168,12 +168,12 @@ def test_batch_order_is_bitwise_invariant(bf16):
     np.testing.assert_array_equal(a[order], b)
 
 
-def _bf16_parity(shape, seed, prefix_lens, n_steps, chunk, kv_fp8=None):
+def _bf16_parity(shape, seed, prefix_lens, n_steps, chunk, kv_fp8=None, **engine_kw):
     tol = FP8_KV_TOL if kv_fp8 is not None else BF16_TOL
     closer = []
     arrays = make_weights(shape, seed=seed, bf16=True)
     w64 = od.ModelWeights.from_arrays(shape, arrays)
-    E = _engine(shape, arrays, bf16=True, max_chunk=max(chunk, 16), kv_fp8=kv_fp8)
+    E = _engine(shape, arrays, bf16=True, max_chunk=max(chunk, 16), kv_fp8=kv_fp8, **engine_kw)
     seqs, toks = [], []
     gpu = [[] for _ in prefix_lens]
     buf = _logits_buf(1, shape.vocab)
@@ -217,6 +217,19 @@ def test_bf16_8b_geometry_two_layers_parity():
                        n_kv_heads=EIGHT_B.n_kv_heads, head_dim=EIGHT_B.head_dim,
                        ffn_dim=EIGHT_B.ffn_dim, vocab=4096)
     _bf16_parity(shape, seed=6, prefix_lens=[9, 33, 48, 20], n_steps=4, chunk=32)
+
+
+@pytest.mark.parametrize("n_kv_heads", [16, 4])
+def test_bf16_long_prefill_items(n_kv_heads):
+    """Prefill attention over long items: with 16 query heads of 128 dims and
+    many KV heads the planner cuts each query block's keys into items of ~32
+    pages (16 two-page stages), so the prefill kernel's four-stage LDS ring
+    wraps several times; chunks of 1000 tokens start mid-page and the last
+    item of a block has an odd page count.  G = 1 and G = 4."""
+    shape = ModelShape(n_layers=1, d_model=256, n_q_heads=16, n_kv_heads=n_kv_heads,
+                       head_dim=128, ffn_dim=256, vocab=512)
+    _bf16_parity(shape, seed=12, prefix_lens=[4000, 1531], n_steps=2, chunk=1000,
+                 pool_tokens=6144, max_seq_len=4096)
 
 
 def test_fp8_kv_decoder_parity():
