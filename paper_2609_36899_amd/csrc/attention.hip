@@ -328,13 +328,16 @@ __attribute__((amdgpu_waves_per_eu(sizeof(KT) == 1 ? 2 : 3))) void attn_split_bf
 
 // ---------------------------------------------------------------------------
 // Prefill, bf16 pages.  A work group of 4 waves takes one (item, KV head) of
-// a 64-row query block (16/G queries x G heads per 16 rows); wave w owns rows
-// 16w .. 16w+15.  All four waves need every key of the item, so the pages
-// pass through LDS two at a time (a stage: K of both pages, then V^T of
-// both), fetched by LDS-DMA into a ring of four stages and read from there by
-// every wave: each page crosses L2 once per work group rather than once per
-// wave, and two stages stay in flight while one is used.  The math per page
-// pair is the split kernel's (S^T = K Q^T, online softmax, O^T = V^T P^T).
+// a 128-row query block (128/G queries x G heads); wave w owns rows
+// 32w .. 32w+31 as two 16-row tiles.  All four waves need every key of the
+// item, so the pages pass through LDS two at a time (a stage: K of both
+// pages, then V^T of both), fetched by LDS-DMA into a ring of four stages and
+// read from there by every wave: each page crosses L2 once per work group
+// rather than once per wave, and two stages stay in flight while one is
+// used.  Each K and V fragment a wave reads from LDS serves both of its row
+// tiles, which halves LDS traffic per MFMA against one tile per wave.  The
+// math per page pair and row tile is the split kernel's (S^T = K Q^T,
+// online softmax, O^T = V^T P^T).
 //
 // K rows in LDS: the 16-byte chunk j of key k of page p sits in slot
 // j ^ kswz(k, p), so that the lanes of one fragment read (8 or 16 keys of the
@@ -347,7 +350,7 @@ __device__ __forceinline__ int kswz(int k, int p) {
 }
 
 template <int DH>  // 128
-__global__ __launch_bounds__(256) void attn_prefill_bf16(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_prefill_bf16(
     const AttnItem* __restrict__ items, const AttnQBlock* __restrict__ qblocks,
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
     const uint16_t* __restrict__ vpool, int64_t page_stride, const int32_t* __restrict__ bt,
@@ -355,7 +358,8 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(
     float* __restrict__ part_ml, float* __restrict__ part_acc) {
   constexpr int KC = DH / 32;   // k-steps of QK^T
   constexpr int DT = DH / 16;   // 16-wide dim tiles of PV
-  constexpr int R = 64;         // query rows per item
+  constexpr int RT = 2;         // 16-row tiles per wave
+  constexpr int R = 64 * RT;    // query rows per item
   constexpr int BLK = kPage * DH;          // elements of one page's K (or V^T) block
   constexpr int STAGE = 4 * BLK;           // K0 K1 V0 V1
   constexpr int CPK = DH / 8;              // 16-byte chunks per K row
@@ -376,44 +380,46 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(
   const AttnQBlock qb = qblocks[it.qblock];
   const int G = n_q_heads / n_kv_heads;
 
-  // This lane's query row.  Waves without rows still take part in the
-  // stage loads and barriers; their results are not written.
-  const int row = wave * 16 + c16;
-  const int jq = row / G;
-  const int head = g * G + (row % G);
-  const bool row_valid = jq < qb.n_q;
-  bf16x8 qf[KC];
-  if (row_valid) {
-    const uint16_t* qrow = q + ((int64_t)(qb.q_row0 + jq) * n_q_heads + head) * DH;
-#pragma unroll
-    for (int c = 0; c < KC; ++c) qf[c] = *(const bf16x8*)(qrow + c * 32 + q4 * 8);
-  } else {
-#pragma unroll
-    for (int c = 0; c < KC; ++c) qf[c] = bf16x8{};
-  }
-
   const int key0 = it.page_begin * kPage;
   const int key_end = (it.page_begin + it.n_pages) * kPage;
   const int kv_lim = min(qb.pos0 + qb.n_q, key_end);  // keys at or past it hold no data
-  const int row_lim = row_valid ? min(qb.pos0 + jq + 1, key_end) : key0;
+
+  // This lane's query row in tile r.  Waves without rows still take part in
+  // the stage loads and barriers; their results are not written.
+  int row[RT], row_lim[RT];
+  bool row_valid[RT];
+  bf16x8 qf[RT][KC];
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+    row[r] = wave * 16 * RT + 16 * r + c16;
+    const int jq = row[r] / G, head = g * G + (row[r] % G);
+    row_valid[r] = jq < qb.n_q;
+    row_lim[r] = row_valid[r] ? min(qb.pos0 + jq + 1, key_end) : key0;
+    if (row_valid[r]) {
+      const uint16_t* qrow = q + ((int64_t)(qb.q_row0 + jq) * n_q_heads + head) * DH;
+#pragma unroll
+      for (int c = 0; c < KC; ++c) qf[r][c] = *(const bf16x8*)(qrow + c * 32 + q4 * 8);
+    } else {
+#pragma unroll
+      for (int c = 0; c < KC; ++c) qf[r][c] = bf16x8{};
+    }
+  }
+
   const int32_t* btrow = bt + (int64_t)qb.slot * bt_stride + it.page_begin;
   const int64_t head_off = (int64_t)g * BLK;
   const int n_st = (it.n_pages + 1) >> 1;
   const int last = n_st - 1;
 
-  // DMA: load j of a stage fills chunks j*256 + tid (block b = chunk / (2*CPK*... )).
+  // DMA: load j of a stage fills chunks j*256 + tid: block j (K page 0,
+  // K page 1, V page 0, V page 1), chunk tid.
   int src_off[LPT];
-  int src_blk[LPT];
 #pragma unroll
   for (int j = 0; j < LPT; ++j) {
-    const int x = j * 256 + tid;
-    const int b = x / (BLK / 8), cc = x % (BLK / 8);
-    src_blk[j] = b;
-    if (b < 2) {
-      const int k = cc / CPK, slot = cc % CPK;
-      src_off[j] = k * DH + ((slot ^ kswz(k, b)) * 8);
+    if (j < 2) {
+      const int k = tid / CPK, slot = tid % CPK;
+      src_off[j] = k * DH + ((slot ^ kswz(k, j)) * 8);
     } else {
-      src_off[j] = cc * 8;
+      src_off[j] = tid * 8;
     }
   }
   // The stage's two page numbers are read with uniform indices (scalar
@@ -426,11 +432,9 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(
     const int64_t base_a = (int64_t)page_a * page_stride + head_off;
     const int64_t base_b = (int64_t)page_b * page_stride + head_off;
 #pragma unroll
-    for (int j = 0; j < LPT; ++j) {
-      const int b = src_blk[j];
-      const uint16_t* src = (b < 2 ? kpool : vpool) + ((b & 1) ? base_b : base_a) + src_off[j];
-      dma16(src, base + j * 256 * 8);
-    }
+    for (int j = 0; j < LPT; ++j)
+      dma16((j < 2 ? kpool : vpool) + ((j & 1) ? base_b : base_a) + src_off[j],
+            base + j * 256 * 8);
   };
 
   // Lane-constant fragment offsets (as in the split kernel).
@@ -439,15 +443,29 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(
   const int v_page_sel = q4 >> 1;
   const int v_tok0 = 8 * (q4 & 1);
 
-  float m = -INFINITY, l = 0.f;
-  f32x4 acc[DT];
+  float m[RT];  // running max of scaled scores (log2 units), row-uniform
+  // The normaliser comes out of one more MFMA per tile: an all-ones A
+  // operand times P^T sums each row's rounded weights (element 0 of every
+  // lane is its row's sum; the other elements are not used).
+  f32x4 lacc[RT];
+  f32x4 acc[RT][DT];
 #pragma unroll
-  for (int t = 0; t < DT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int r = 0; r < RT; ++r) {
+    m[r] = -INFINITY;
+    lacc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < DT; ++t) acc[r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const bf16x8 ones = __builtin_bit_cast(bf16x8, u16x8{0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80,
+                                                       0x3F80, 0x3F80, 0x3F80});
+  // Stages wholly below every row's causal limit need no mask (keys below
+  // pos0 + 1 are visible to all rows of the block; rows past the block's
+  // queries are computed too and never written).
+  const int open_end = min(qb.pos0 + 1, key_end);
 
   auto compute = [&](int st, int buf) {
     const uint16_t* sb = stage_ptr(buf);
     bf16x8 kf[2][KC];
-    u16x8 vf[DT];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int k = k_tok + 4 * u;
@@ -456,51 +474,53 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(
       for (int c = 0; c < KC; ++c)
         kf[u][c] = *(const bf16x8*)(kr + (((4 * c + q4) ^ kswz(k, k_page_sel)) * 8));
     }
+    const int kbase = key0 + (2 * st + v_page_sel) * kPage + v_tok0;
+    const bool open = key0 + (2 * st + 2) * kPage <= open_end;  // uniform
+    bf16x8 pf[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      f32x4 s[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        s[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < KC; ++c)
+          s[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[u][c], qf[r][c], s[u], 0, 0, 0);
+      }
+      // Raw scores; the scale (> 0) is applied to the max and inside the
+      // exponent's FMA.  Masked keys are -inf, whose weight is exactly 0.
+      float sv[8];
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr)
+          sv[4 * u + rr] = (open || kbase + 4 * u + rr < row_lim[r]) ? s[u][rr] : -INFINITY;
+      float mloc = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
+                         fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+      const float m_new = fmaxf(m[r], mloc * scale_log2);
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      if (__any(m_new != m[r])) {
+        const float alpha = __builtin_amdgcn_exp2f(m[r] - m_use);
+        lacc[r][0] *= alpha;
+#pragma unroll
+        for (int t = 0; t < DT; ++t) acc[r][t] *= alpha;
+      }
+      m[r] = m_new;
+      uint32_t pw4[4];
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const f32x2 pv = {__builtin_amdgcn_exp2f(__builtin_fmaf(sv[e], scale_log2, -m_use)),
+                          __builtin_amdgcn_exp2f(__builtin_fmaf(sv[e + 1], scale_log2, -m_use))};
+        pw4[e / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pv, bf16x2));
+      }
+      pf[r] = __builtin_bit_cast(bf16x8, u32x4{pw4[0], pw4[1], pw4[2], pw4[3]});
+    }
+    u16x8 vf[DT];
 #pragma unroll
     for (int t = 0; t < DT; ++t)
       vf[t] = *(const u16x8*)(sb + (2 + v_page_sel) * BLK + (t * 16 + c16) * kPage + v_tok0);
-
-    f32x4 s[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      s[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int c = 0; c < KC; ++c)
-        s[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[u][c], qf[c], s[u], 0, 0, 0);
-    }
-    const int kbase = key0 + (2 * st + v_page_sel) * kPage + v_tok0;
-    float sv[8];
-    float mloc = -INFINITY;
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int e = 4 * u + rr;
-        const float x = (kbase + e < row_lim) ? s[u][rr] * scale_log2 : -INFINITY;
-        sv[e] = x;
-        mloc = fmaxf(mloc, x);
-      }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m, mloc);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    if (__any(m_new != m)) {
-      const float alpha = __builtin_amdgcn_exp2f(m - m_use);
-      l *= alpha;
-#pragma unroll
-      for (int t = 0; t < DT; ++t) acc[t] *= alpha;
-    }
-    m = m_new;
-    uint32_t pw4[4];
-#pragma unroll
-    for (int e = 0; e < 8; e += 2) {
-      const f32x2 pv = {__builtin_amdgcn_exp2f(sv[e] - m_use),
-                        __builtin_amdgcn_exp2f(sv[e + 1] - m_use)};
-      const uint32_t bits = __builtin_bit_cast(uint32_t, __builtin_convertvector(pv, bf16x2));
-      pw4[e / 2] = bits;
-      l += __uint_as_float(bits << 16) + __uint_as_float(bits & 0xFFFF0000u);
-    }
-    const bf16x8 pf = __builtin_bit_cast(bf16x8, u32x4{pw4[0], pw4[1], pw4[2], pw4[3]});
     if (__builtin_expect(key0 + (2 * st + 2) * kPage > kv_lim, 0)) {  // the block's last keys
 #pragma unroll
       for (int e = 0; e < 8; ++e)
@@ -509,9 +529,13 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(
           for (int t = 0; t < DT; ++t) vf[t][e] = 0;
     }
 #pragma unroll
-    for (int t = 0; t < DT; ++t)
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[t]), pf,
-                                                       acc[t], 0, 0, 0);
+    for (int r = 0; r < RT; ++r) {
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+        acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[t]),
+                                                            pf[r], acc[r][t], 0, 0, 0);
+      lacc[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[r], lacc[r], 0, 0, 0);
+    }
   };
 
   // Ring of D stages, two in flight while one is used (stage indices
@@ -543,17 +567,17 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16(
     }
   wait_vmem<0>();  // no LDS write may still be in flight when the group ends
 
-  l += __shfl_xor(l, 16, 64);
-  l += __shfl_xor(l, 32, 64);
-  if (row_valid) {
-    const int64_t prow = ((int64_t)item_id * n_kv_heads + g) * R + row;
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+    if (!row_valid[r]) continue;
+    const int64_t prow = ((int64_t)item_id * n_kv_heads + g) * R + row[r];
     if (q4 == 0) {
-      part_ml[prow * 2] = m;
-      part_ml[prow * 2 + 1] = l;
+      part_ml[prow * 2] = m[r];
+      part_ml[prow * 2 + 1] = lacc[r][0];
     }
     float* pa = part_acc + prow * DH;
 #pragma unroll
-    for (int t = 0; t < DT; ++t) *(f32x4*)(pa + t * 16 + 4 * q4) = acc[t];
+    for (int t = 0; t < DT; ++t) *(f32x4*)(pa + t * 16 + 4 * q4) = acc[r][t];
   }
 }
 
@@ -724,9 +748,9 @@ hipError_t launch_attention_split(int dtype, int kv_fp8, float k_scale, float v_
   } else {                                                                                   \
     if (rows_per_item == 64) PDEC_ATTN_BF16(64, 4, 1, KT_); else PDEC_ATTN_BF16(64, 1, 4, KT_); \
   }
-    // 64-row items (prefill) with bf16 pages and 128-dim heads: the
+    // 128-row items: prefill with bf16 pages and 128-dim heads, the
     // LDS-staged prefill kernel.
-    if (rows_per_item == 64 && !kv_fp8 && head_dim == 128)
+    if (rows_per_item == 128 && !kv_fp8 && head_dim == 128)
       return launch_timed(attn_prefill_bf16<128>, grid, dim3(256), stream, ev_start, ev_stop,
                           items, qblocks, qq, (const uint16_t*)k_pages, (const uint16_t*)v_pages,
                           page_stride_elems, block_table, bt_stride, n_q_heads, n_kv_heads,

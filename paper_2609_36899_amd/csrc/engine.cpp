@@ -205,7 +205,11 @@ struct WsLayout {
 constexpr size_t kDeltaCap = 65536;
 // Query rows per attention work item: decode (one wave) and prefill (four).
 constexpr int kDecodeRows = 16;
-constexpr int kPrefillRows = 64;
+// Query rows per prefill block: 128 for the LDS-staged prefill kernel (bf16
+// pages, 128-dim heads), 64 for the others.
+int prefill_rows(const pdec_model_cfg& c) {
+  return (c.dtype == PDEC_BF16 && !c.kv_fp8 && c.head_dim == 128) ? 128 : 64;
+}
 
 int check_cfg(const pdec_model_cfg* c) {
   if (!c) return fail(PDEC_INVALID_ARG, "null cfg");
@@ -261,14 +265,15 @@ int make_layout(const pdec_model_cfg* c, int32_t max_seqs, int32_t max_seq_len,
   const int64_t ab = elem_bytes(c->dtype);
   const int64_t qd = (int64_t)c->n_q_heads * c->head_dim;
   L->rows_cap = std::max(max_batch, max_chunk);
-  // Decode: one query per block, 16-row items.  Prefill: kPrefillRows / G
-  // queries per block, 64-row items.
-  const int64_t pre_blocks = (max_chunk + (kPrefillRows / G) - 1) / (kPrefillRows / G);
+  // Decode: one query per block, 16-row items.  Prefill: prefill_rows / G
+  // queries per block, prefill_rows-row items.
+  const int pre_rows = prefill_rows(*c);
+  const int64_t pre_blocks = (max_chunk + (pre_rows / G) - 1) / (pre_rows / G);
   L->qblocks_cap = std::max<int64_t>(max_batch, pre_blocks);
   const int64_t items_dec = attn_target_items(c->n_kv_heads, kDecodeTargetGroups) + max_batch + 16;
   const int64_t items_pre = attn_target_items(c->n_kv_heads, kPrefillTargetGroups) + pre_blocks + 16;
   L->items_cap = std::max(items_dec, items_pre);
-  L->part_row_slots = std::max(items_dec * kDecodeRows, items_pre * kPrefillRows);
+  L->part_row_slots = std::max(items_dec * kDecodeRows, items_pre * pre_rows);
   L->bt_stride = PagePool::pages_for(max_seq_len);
   L->meta_bytes = align_up(L->rows_cap * sizeof(RowMeta)) +
                   align_up(L->qblocks_cap * sizeof(AttnQBlock)) +
@@ -728,7 +733,8 @@ int kv_append_prefix(pdec_engine* E, int32_t seq, const int32_t* tokens_host, in
   st = E->pool->grow(&slot, 1, n, &undo);
   if (!st.good()) return fail(st.code, st.msg);
 
-  const int QB = kPrefillRows / (E->cfg.n_q_heads / E->cfg.n_kv_heads);
+  const int pre_rows = prefill_rows(E->cfg);
+  const int QB = pre_rows / (E->cfg.n_q_heads / E->cfg.n_kv_heads);
   std::vector<RowMeta> rows;
   std::vector<QBlockSpec> specs;
   std::vector<AttnQBlock> qblocks;
@@ -745,7 +751,7 @@ int kv_append_prefix(pdec_engine* E, int32_t seq, const int32_t* tokens_host, in
                                       kPrefillTargetGroups),
                    &qblocks, &items);
     const bool last = c0 + C >= n;
-    int rc = enqueue_forward(E, C, rows, qblocks, items, kPrefillRows, nullptr, tokens_host + c0,
+    int rc = enqueue_forward(E, C, rows, qblocks, items, pre_rows, nullptr, tokens_host + c0,
                              last ? last_logits_dev : nullptr, true);
     if (rc != PDEC_OK) {
       E->pool->undo(undo);
