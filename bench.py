@@ -432,6 +432,8 @@ def run_multiturn(workload, segments, seg_steps, warmup):
         "departed": departed, "final_batch": len(live),
         "append": {"tokens": int(app_tokens), "ms": round(app_ms, 1),
                    "prefill_tokens_per_s": round(app_tokens / (app_ms / 1e3), 1) if app_ms else None},
+        # decoded tokens over decode and append time together
+        "end_to_end_tokens_per_s": round(dec_tokens / ((dec_ms + app_ms) / 1e3), 2),
         "cpu_baseline": None,
     }
     return out
