@@ -7,8 +7,9 @@
 // streams its pages once, applies them to every query head of the GQA group,
 // and leaves an online-softmax partial (max, sum, unnormalised output) that
 // the combine pass merges.  Query rows of a block = (query, head-in-group)
-// pairs, at most 16: one in-group head set per decode row, 16/G queries in
-// prefill.
+// pairs: one query (G rows) per decode block; 128/G queries per prefill
+// block for the LDS-staged prefill kernel (bf16 pages, 128-dim heads) and
+// 64/G for the row-wave form of the split kernel (fp8 pages, 64-dim heads).
 //
 // bf16 path: both products run on MFMA (v_mfma_f32_16x16x32_bf16).  Scores are
 // computed transposed, S^T = K Q^T, so that each lane's output column is one

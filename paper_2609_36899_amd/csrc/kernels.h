@@ -23,8 +23,9 @@ struct WSegs {
 };
 
 // ---- attention --------------------------------------------------------------
-// Split pass: one work group per (item, KV head) of rows_per_item / 16
-// waves (rows_per_item = 16 or 64).  Writes per-row partial softmax
+// Split pass: one work group per (item, KV head).  rows_per_item = 16
+// (decode), 64 (prefill, fp8 pages or 64-dim heads) or 128 (prefill, bf16
+// pages and 128-dim heads: the LDS-staged prefill kernel).  Writes per-row partial softmax
 // statistics part_ml [items][Hkv][rows_per_item][2] = (max in log2 units,
 // sum) and unnormalised outputs part_acc [items][Hkv][rows_per_item][head_dim].
 // kv_fp8: K/V pages hold E4M3 codes read back as code * k_scale / v_scale.
