@@ -111,6 +111,96 @@ def weight_bytes_per_step(shape, batch, elem=2):
                    + batch * shape.d_model)
 
 
+class ClockSampler:
+    """Samples the GPU's current graphics and memory clocks (MHz) through
+    amd-smi while a timed region runs; clocks are not pinned, so they are
+    reported beside the timings.  Sampling failures leave the record empty
+    with the reason."""
+
+    def __init__(self, device=0, period_s=0.2):
+        import threading
+        self.device, self.period_s = device, period_s
+        self.gfx, self.mem, self.error = [], [], None
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+        self.bdf = None
+        try:
+            import amdsmi
+            import torch
+            props = torch.cuda.get_device_properties(device)
+            amdsmi.amdsmi_init()
+            # The processor whose PCI domain:bus:device matches this device's.
+            for h in amdsmi.amdsmi_get_processor_handles():
+                bdf = amdsmi.amdsmi_get_gpu_device_bdf(h)
+                dom, bus, dev = bdf.split(".")[0].split(":")
+                if (int(dom, 16), int(bus, 16), int(dev, 16)) == (
+                        props.pci_domain_id, props.pci_bus_id, props.pci_device_id):
+                    self._handle, self.bdf = h, bdf
+                    break
+            else:
+                raise RuntimeError("no amd-smi processor has this device's PCI address")
+            self._smi = amdsmi
+        except Exception as e:  # no amd-smi on this host: report why
+            self._smi, self.error = None, f"{type(e).__name__}: {e}"
+
+    def _read(self):
+        t = self._smi.AmdSmiClkType
+        for kind, dst in ((t.GFX, self.gfx), (t.MEM, self.mem)):
+            info = self._smi.amdsmi_get_clock_info(self._handle, kind)
+            v = info.get("clk", info.get("cur_clk"))
+            if isinstance(v, (int, float)):
+                dst.append(float(v))
+
+    def _run(self):
+        while not self._stop.is_set():
+            try:
+                self._read()
+            except Exception as e:
+                self.error = f"{type(e).__name__}: {e}"
+                return
+            self._stop.wait(self.period_s)
+
+    def __enter__(self):
+        if self._smi is not None:
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self._smi is not None:
+            self._thread.join()
+
+    def summary(self):
+        def stats(v):
+            return ({"min": min(v), "median": float(np.median(v)), "max": max(v)}
+                    if v else None)
+        return {"pinned": False, "source": "amd-smi current clock, sampled every "
+                f"{self.period_s:g} s over the timed steps", "pci": self.bdf,
+                "samples": len(self.gfx),
+                "gfx_mhz": stats(self.gfx), "mem_mhz": stats(self.mem), "error": self.error}
+
+
+def stream_copy_gbs(n=1 << 30, iters=10):
+    """Practical HBM ceiling: a device-to-device copy of n bytes (torch copy_),
+    counted as n read + n written per copy, averaged over iters copies."""
+    import torch
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(iters):
+        b.copy_(a)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / iters
+    del a, b
+    return {"bytes_per_copy": 2 * n, "avg_ms": round(ms, 4),
+            "gbps": round(2 * n / (ms / 1e3) / 1e9, 1), "kernel": "torch copy_ (uint8, 1 GiB)"}
+
+
 def file_hash(path):
     with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
@@ -259,7 +349,8 @@ def run_decode(workload, steps, warmup, with_cpu):
         step()
     torch.cuda.synchronize()
     log(f"warmup done ({warmup} steps); timing {steps} steps")
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # One event after every step: per-step times for the median and P95.
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     # Only attention launches (the roofline kernel) are timed in the timed
     # region, and only one in every n_layers + 1 of them: a timed launch
     # leaves the GPU idle for a few microseconds around it, and all layers of
@@ -268,15 +359,17 @@ def run_decode(workload, steps, warmup, with_cpu):
     attn_every = shape.n_layers + 1
     E.profile([N.TIMER_ATTENTION], every=attn_every)
     torch.cuda.synchronize()
-    w0 = time.perf_counter()
-    start.record()
-    for _ in range(steps):
-        step()
-    end.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
+    with ClockSampler() as clocks:
+        w0 = time.perf_counter()
+        marks[0].record()
+        for i in range(steps):
+            step()
+            marks[i + 1].record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
     E.profile([])
-    gpu_ms = start.elapsed_time(end)
+    gpu_ms = marks[0].elapsed_time(marks[-1])
+    step_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(steps)])
     attn_ms, attn_n = E.profile_read(N.TIMER_ATTENTION)
     # Projection / LM-head breakdown from a few further steps, outside the
     # timed region (their event pairs would lengthen the timed steps).
@@ -320,6 +413,11 @@ def run_decode(workload, steps, warmup, with_cpu):
                    "kv_pages": "fp8 e4m3, scales 1" if kv_fp8 is not None else "bf16"},
         "hbm_gbps": round(hbm, 1), "hbm_frac_of_peak": round(hbm / HBM_PEAK_GBS, 4),
         "step_bytes": int(step_bytes), "wall_s": round(wall, 3),
+        "step_ms": {"median": round(float(np.median(step_ms)), 4),
+                    "p95": round(float(np.percentile(step_ms, 95)), 4),
+                    "min": round(float(step_ms.min()), 4),
+                    "max": round(float(step_ms.max()), 4)},
+        "clocks": clocks.summary(),
         "breakdown_ms_per_step": {"attention": round(attn_avg_ms * shape.n_layers, 3),
                                   "projections": round(gemm_ms / bsteps, 3),
                                   "lm_head": round(lm_ms / bsteps, 3)},
@@ -334,6 +432,7 @@ def run_decode(workload, steps, warmup, with_cpu):
     }
     del E, weights, logits, pool
     torch.cuda.empty_cache()
+    out["stream_copy"] = stream_copy_gbs()
     if with_cpu:
         log("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(shape, lens)

@@ -21,8 +21,8 @@ BUILD = os.path.join(PKG, "_build")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
-HIP_SOURCES = ["attention.hip", "gemm.hip", "pointwise.hip", "kvcopy.hip", "sample.hip",
-               "engine.cpp", "pagepool.cpp", "pacing.cpp"]
+HIP_SOURCES = ["attention.hip", "attention_prefill.hip", "gemm.hip", "pointwise.hip", "kvcopy.hip",
+               "sample.hip", "engine.cpp", "pagepool.cpp", "pacing.cpp"]
 HIP_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
     # Packed fp32 VALU ops are kept out of the device code.

@@ -1,0 +1,288 @@
+// LDS-staged prefill attention for gfx950 (bf16 pages, 128-dim heads).
+//
+// Chunked prefill (the re-prefill path that rebuilds a trajectory's KV from
+// its tokens, paper: KV Preparation for Late-Bound Placement) presents 128-row query
+// blocks: 128/G queries of one chunk times the G query heads of a GQA group.
+// Such blocks are MFMA-bound rather than HBM-bound, so this kernel shares each
+// page between four waves through LDS instead of letting every wave stream it.
+// It writes the same partials as the decode split kernel and is merged by the
+// same combine pass.
+#include "hip_common.h"
+#include "kernels.h"
+
+namespace pdec {
+
+namespace {
+// ---------------------------------------------------------------------------
+// Prefill, bf16 pages.  A work group of 4 waves takes one (item, KV head) of
+// a 128-row query block (128/G queries x G heads); wave w owns rows
+// 32w .. 32w+31 as two 16-row tiles.  All four waves need every key of the
+// item, so the pages pass through LDS two at a time (a stage: K of both
+// pages, then V^T of both), fetched by LDS-DMA into a ring of four stages and
+// read from there by every wave: each page crosses L2 once per work group
+// rather than once per wave, and two stages stay in flight while one is
+// used.  Each K and V fragment a wave reads from LDS serves both of its row
+// tiles, which halves LDS traffic per MFMA against one tile per wave.  The
+// math per page pair and row tile is the split kernel's (S^T = K Q^T,
+// online softmax, O^T = V^T P^T).
+//
+// K rows in LDS: the 16-byte chunk j of key k of page p sits in slot
+// j ^ kswz(k, p), so that the lanes of one fragment read (8 or 16 keys of the
+// same chunk column) hit distinct banks; the swizzle goes on the DMA's source
+// address.  V^T blocks are copied as they are (a fragment read covers 16
+// dims x 32 bytes, already conflict-free).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int kswz(int k, int p) {
+  return (k & 3) | (((k >> 3) & 1) << 2) | (p << 3);  // < 16 chunks per 128-dim key row
+}
+
+template <int DH>  // 128
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_prefill_bf16(
+    const AttnItem* __restrict__ items, const AttnQBlock* __restrict__ qblocks,
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
+    const uint16_t* __restrict__ vpool, int64_t page_stride, const int32_t* __restrict__ bt,
+    int32_t bt_stride, int32_t n_q_heads, int32_t n_kv_heads, float scale_log2,
+    float* __restrict__ part_ml, float* __restrict__ part_acc) {
+  constexpr int KC = DH / 32;   // k-steps of QK^T
+  constexpr int DT = DH / 16;   // 16-wide dim tiles of PV
+  constexpr int RT = 2;         // 16-row tiles per wave
+  constexpr int R = 64 * RT;    // query rows per item
+  constexpr int BLK = kPage * DH;          // elements of one page's K (or V^T) block
+  constexpr int STAGE = 4 * BLK;           // K0 K1 V0 V1
+  constexpr int CPK = DH / 8;              // 16-byte chunks per K row
+  constexpr int LPT = STAGE * 2 / 16 / 256;  // DMA loads per thread per stage
+  constexpr int D = 4;
+  static_assert(DH == 128, "the K swizzle spans 16 chunks per key row");
+  static_assert(LPT * 256 * 8 == STAGE, "stage is a whole number of loads");
+  __shared__ __attribute__((aligned(16))) uint16_t st0[STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t st1[STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t st2[STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t st3[STAGE];
+  auto stage_ptr = [&](int b) -> uint16_t* { return b == 0 ? st0 : b == 1 ? st1 : b == 2 ? st2 : st3; };
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int c16 = lane & 15, q4 = lane >> 4;
+  const int g = blockIdx.x, item_id = items[blockIdx.y].order;
+  const AttnItem it = items[item_id];
+  const AttnQBlock qb = qblocks[it.qblock];
+  const int G = n_q_heads / n_kv_heads;
+
+  const int key0 = it.page_begin * kPage;
+  const int key_end = (it.page_begin + it.n_pages) * kPage;
+  const int kv_lim = min(qb.pos0 + qb.n_q, key_end);  // keys at or past it hold no data
+
+  // This lane's query row in tile r.  Waves without rows still take part in
+  // the stage loads and barriers; their results are not written.
+  int row[RT], row_lim[RT];
+  bool row_valid[RT];
+  bf16x8 qf[RT][KC];
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+    row[r] = wave * 16 * RT + 16 * r + c16;
+    const int jq = row[r] / G, head = g * G + (row[r] % G);
+    row_valid[r] = jq < qb.n_q;
+    row_lim[r] = row_valid[r] ? min(qb.pos0 + jq + 1, key_end) : key0;
+    if (row_valid[r]) {
+      const uint16_t* qrow = q + ((int64_t)(qb.q_row0 + jq) * n_q_heads + head) * DH;
+#pragma unroll
+      for (int c = 0; c < KC; ++c) qf[r][c] = *(const bf16x8*)(qrow + c * 32 + q4 * 8);
+    } else {
+#pragma unroll
+      for (int c = 0; c < KC; ++c) qf[r][c] = bf16x8{};
+    }
+  }
+
+  const int32_t* btrow = bt + (int64_t)qb.slot * bt_stride + it.page_begin;
+  const int64_t head_off = (int64_t)g * BLK;
+  const int n_st = (it.n_pages + 1) >> 1;
+  const int last = n_st - 1;
+
+  // DMA: load j of a stage fills chunks j*256 + tid: block j (K page 0,
+  // K page 1, V page 0, V page 1), chunk tid.
+  int src_off[LPT];
+#pragma unroll
+  for (int j = 0; j < LPT; ++j) {
+    if (j < 2) {
+      const int k = tid / CPK, slot = tid % CPK;
+      src_off[j] = k * DH + ((slot ^ kswz(k, j)) * 8);
+    } else {
+      src_off[j] = tid * 8;
+    }
+  }
+  // The stage's two page numbers are read with uniform indices (scalar
+  // loads): a per-lane page-table read would be a vector load, and waiting
+  // for it would also wait for every stage in flight (loads retire in order).
+  auto issue = [&](int st, int buf) {
+    uint16_t* base = stage_ptr(buf) + wave * 64 * 8;
+    const int page_a = btrow[2 * st];
+    const int page_b = btrow[min(2 * st + 1, it.n_pages - 1)];  // missing: a valid page, masked
+    const int64_t base_a = (int64_t)page_a * page_stride + head_off;
+    const int64_t base_b = (int64_t)page_b * page_stride + head_off;
+#pragma unroll
+    for (int j = 0; j < LPT; ++j)
+      dma16((j < 2 ? kpool : vpool) + ((j & 1) ? base_b : base_a) + src_off[j],
+            base + j * 256 * 8);
+  };
+
+  // Lane-constant fragment offsets (as in the split kernel).
+  const int k_tok = 8 * ((c16 >> 2) & 1) + (c16 & 3);  // + 4u
+  const int k_page_sel = c16 >> 3;
+  const int v_page_sel = q4 >> 1;
+  const int v_tok0 = 8 * (q4 & 1);
+
+  float m[RT];  // running max of scaled scores (log2 units), row-uniform
+  // The normaliser comes out of one more MFMA per tile: an all-ones A
+  // operand times P^T sums each row's rounded weights (element 0 of every
+  // lane is its row's sum; the other elements are not used).
+  f32x4 lacc[RT];
+  f32x4 acc[RT][DT];
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+    m[r] = -INFINITY;
+    lacc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < DT; ++t) acc[r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const bf16x8 ones = __builtin_bit_cast(bf16x8, u16x8{0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80,
+                                                       0x3F80, 0x3F80, 0x3F80});
+  // Stages wholly below every row's causal limit need no mask (keys below
+  // pos0 + 1 are visible to all rows of the block; rows past the block's
+  // queries are computed too and never written).
+  const int open_end = min(qb.pos0 + 1, key_end);
+
+  auto compute = [&](int st, int buf) {
+    const uint16_t* sb = stage_ptr(buf);
+    bf16x8 kf[2][KC];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int k = k_tok + 4 * u;
+      const uint16_t* kr = sb + k_page_sel * BLK + k * DH;
+#pragma unroll
+      for (int c = 0; c < KC; ++c)
+        kf[u][c] = *(const bf16x8*)(kr + (((4 * c + q4) ^ kswz(k, k_page_sel)) * 8));
+    }
+    const int kbase = key0 + (2 * st + v_page_sel) * kPage + v_tok0;
+    const bool open = key0 + (2 * st + 2) * kPage <= open_end;  // uniform
+    bf16x8 pf[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      f32x4 s[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        s[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < KC; ++c)
+          s[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[u][c], qf[r][c], s[u], 0, 0, 0);
+      }
+      // Raw scores; the scale (> 0) is applied to the max and inside the
+      // exponent's FMA.  Masked keys are -inf, whose weight is exactly 0.
+      float sv[8];
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr)
+          sv[4 * u + rr] = (open || kbase + 4 * u + rr < row_lim[r]) ? s[u][rr] : -INFINITY;
+      float mloc = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
+                         fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+      const float m_new = fmaxf(m[r], mloc * scale_log2);
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      if (__any(m_new != m[r])) {
+        const float alpha = __builtin_amdgcn_exp2f(m[r] - m_use);
+        lacc[r][0] *= alpha;
+#pragma unroll
+        for (int t = 0; t < DT; ++t) acc[r][t] *= alpha;
+      }
+      m[r] = m_new;
+      uint32_t pw4[4];
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const f32x2 pv = {__builtin_amdgcn_exp2f(__builtin_fmaf(sv[e], scale_log2, -m_use)),
+                          __builtin_amdgcn_exp2f(__builtin_fmaf(sv[e + 1], scale_log2, -m_use))};
+        pw4[e / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pv, bf16x2));
+      }
+      pf[r] = __builtin_bit_cast(bf16x8, u32x4{pw4[0], pw4[1], pw4[2], pw4[3]});
+    }
+    u16x8 vf[DT];
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+      vf[t] = *(const u16x8*)(sb + (2 + v_page_sel) * BLK + (t * 16 + c16) * kPage + v_tok0);
+    if (__builtin_expect(key0 + (2 * st + 2) * kPage > kv_lim, 0)) {  // the block's last keys
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (kbase + e >= kv_lim)
+#pragma unroll
+          for (int t = 0; t < DT; ++t) vf[t][e] = 0;
+    }
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+#pragma unroll
+      for (int t = 0; t < DT; ++t)
+        acc[r][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[t]),
+                                                            pf[r], acc[r][t], 0, 0, 0);
+      lacc[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[r], lacc[r], 0, 0, 0);
+    }
+  };
+
+  // Ring of D stages, two in flight while one is used (stage indices
+  // clamped to the last, so every step issues one stage and the count of
+  // loads in flight is fixed).  After the barrier of step st every wave has
+  // finished step st-1, whose stage then takes step st+3.
+#pragma unroll
+  for (int b = 0; b < D - 1; ++b) issue(min(b, last), b);
+  int st = 0;
+  for (; st + D <= n_st; st += D) {
+#pragma unroll
+    for (int b = 0; b < D; ++b) {
+      wait_vmem<(D - 2) * LPT>();
+      wg_barrier();
+      issue(min(st + b + D - 1, last), (b + D - 1) % D);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(st + b, b);
+    }
+  }
+  const int tail = n_st - st;  // uniform over the work group
+#pragma unroll
+  for (int b = 0; b < D; ++b)
+    if (b < tail) {
+      wait_vmem<(D - 2) * LPT>();
+      wg_barrier();
+      issue(min(st + b + D - 1, last), (b + D - 1) % D);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(st + b, b);
+    }
+  wait_vmem<0>();  // no LDS write may still be in flight when the group ends
+
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+    if (!row_valid[r]) continue;
+    const int64_t prow = ((int64_t)item_id * n_kv_heads + g) * R + row[r];
+    if (q4 == 0) {
+      part_ml[prow * 2] = m[r];
+      part_ml[prow * 2 + 1] = lacc[r][0];
+    }
+    float* pa = part_acc + prow * DH;
+#pragma unroll
+    for (int t = 0; t < DT; ++t) *(f32x4*)(pa + t * 16 + 4 * q4) = acc[r][t];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attention_prefill_bf16(int n_items, int n_q_heads, int n_kv_heads,
+                                         const AttnItem* items, const AttnQBlock* qblocks,
+                                         const void* q, const void* k_pages, const void* v_pages,
+                                         int64_t page_stride_elems, const int32_t* block_table,
+                                         int32_t bt_stride, float scale_log2, float* part_ml,
+                                         float* part_acc, hipStream_t stream, hipEvent_t ev_start,
+                                         hipEvent_t ev_stop) {
+  if (n_items == 0) return hipSuccess;
+  return launch_timed(attn_prefill_bf16<128>, dim3(n_kv_heads, n_items), dim3(256), stream,
+                      ev_start, ev_stop, items, qblocks, (const uint16_t*)q,
+                      (const uint16_t*)k_pages, (const uint16_t*)v_pages, page_stride_elems,
+                      block_table, bt_stride, n_q_heads, n_kv_heads, scale_log2, part_ml,
+                      part_acc);
+}
+
+}  // namespace pdec
