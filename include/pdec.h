@@ -371,6 +371,29 @@ int weight_projection(int32_t dtype, int32_t M, int32_t N, int32_t K, const void
                       const void* w, float* out, void* workspace, int64_t workspace_bytes,
                       void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Isolated gate/up projection with SwiGLU, the first half of the decoder
+ * block's feed-forward layer as decode_step and kv_append_prefix run it:
+ *   u[m][n] = silu(g) * up,  g = x[m] . w_gate[n],  up = x[m] . w_up[n],
+ *   silu(z) = z / (1 + exp(-z)),  n < F.
+ * When one work group per column group covers K (bf16 whenever the planner
+ * chooses no K split, as for every 8B-shaped batch), the product and the
+ * SwiGLU run in one kernel and the fp32 gate/up values never reach memory;
+ * otherwise the split-K partials go to the workspace and a second kernel sums
+ * them and applies SwiGLU with the same fp32 arithmetic.
+ *   x: device [M][K] in dtype; w_gate, w_up: [F][K] weights as produced by
+ *   pack_weight; u: device [M][F] in dtype (bf16 rounded to nearest even);
+ *   workspace: device, at least swiglu_projection_workspace_bytes(...) bytes
+ *   (may be 0).
+ * Errors: PDEC_UNSUPPORTED (bf16 with K % 64 != 0, F % 4 != 0),
+ * PDEC_INVALID_ARG.
+ * ------------------------------------------------------------------------- */
+int64_t swiglu_projection_workspace_bytes(int32_t dtype, int32_t M, int32_t F, int32_t K);
+
+int swiglu_projection(int32_t dtype, int32_t M, int32_t F, int32_t K, const void* x,
+                      const void* w_gate, const void* w_up, void* u, void* workspace,
+                      int64_t workspace_bytes, void* stream);
+
 int64_t paged_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
                                         int32_t head_dim, int64_t max_total_tokens);
 

@@ -92,6 +92,9 @@ SIGNATURES = {
     "weight_projection_workspace_bytes": (c_int64, [c_int32, c_int32, c_int32, c_int32]),
     "weight_projection": (c_int32, [c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                     c_void_p, c_void_p, c_int64, c_void_p]),
+    "swiglu_projection_workspace_bytes": (c_int64, [c_int32, c_int32, c_int32, c_int32]),
+    "swiglu_projection": (c_int32, [c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
+                                    c_void_p, c_void_p, c_void_p, c_int64, c_void_p]),
     "paged_attention_workspace_bytes": (c_int64, [c_int32, c_int32, c_int32, c_int32, c_int64]),
     "paged_decode_attention": (c_int32, [c_int32, c_int32, c_int32, c_int32, c_int32, c_void_p,
                                          c_void_p, c_void_p, c_void_p, c_int32, POINTER(c_int32),

@@ -434,8 +434,13 @@ int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
     HIP_OR_FAIL(launch_resid_norm(dt, M, d, E->part, S, E->x, E->ffn_norm[l], c.rms_eps, E->h, s));
     S = gemm_plan_splits(dt, M, 2 * F, d, &ks);
     HIP_OR_FAIL(E->timer.pair(PDEC_TIMER_GEMM, &ea, &eb));
-    HIP_OR_FAIL(launch_gemm(dt, M, 2 * F, d, E->h, d, E->w_gu[l], E->part, S, ks, s, ea, eb));
-    HIP_OR_FAIL(launch_swiglu(dt, M, F, E->part, S, E->u, s));
+    if (dt == PDEC_BF16 && S == 1) {  // one work group per column: SwiGLU in the epilogue
+      HIP_OR_FAIL(launch_gemm_swiglu(M, F, d, E->h, d, E->w_gu[l].ptr[0], E->w_gu[l].ptr[1],
+                                     E->u, s, ea, eb));
+    } else {
+      HIP_OR_FAIL(launch_gemm(dt, M, 2 * F, d, E->h, d, E->w_gu[l], E->part, S, ks, s, ea, eb));
+      HIP_OR_FAIL(launch_swiglu(dt, M, F, E->part, S, E->u, s));
+    }
     S = gemm_plan_splits(dt, M, d, F, &ks);
     HIP_OR_FAIL(E->timer.pair(PDEC_TIMER_GEMM, &ea, &eb));
     HIP_OR_FAIL(launch_gemm(dt, M, d, F, E->u, F, E->w_down[l], E->part, S, ks, s, ea, eb));
@@ -929,6 +934,44 @@ int weight_projection(int32_t dtype, int32_t M, int32_t N, int32_t K, const void
   float* dst = S > 1 ? (float*)workspace : out;
   HIP_OR_FAIL(launch_gemm(dtype, M, N, K, x, K, ws, dst, S, ks, s));
   if (S > 1) HIP_OR_FAIL(launch_sum_splits((int64_t)M * N, dst, S, out, s));
+  return PDEC_OK;
+}
+
+int64_t swiglu_projection_workspace_bytes(int32_t dtype, int32_t M, int32_t F, int32_t K) {
+  if ((dtype != PDEC_F32 && dtype != PDEC_BF16) || M < 1 || F < 1 || K < 1 || F > INT32_MAX / 2)
+    return fail(PDEC_INVALID_ARG, "bad projection arguments");
+  int ks;
+  const int S = gemm_plan_splits(dtype, M, 2 * F, K, &ks);
+  return (dtype == PDEC_BF16 && S == 1) ? 0 : (int64_t)S * M * 2 * F * 4;
+}
+
+int swiglu_projection(int32_t dtype, int32_t M, int32_t F, int32_t K, const void* x,
+                      const void* w_gate, const void* w_up, void* u, void* workspace,
+                      int64_t ws_bytes, void* stream) {
+  if (!x || !w_gate || !w_up || !u) return fail(PDEC_INVALID_ARG, "null argument");
+  const int64_t need = swiglu_projection_workspace_bytes(dtype, M, F, K);
+  if (need < 0) return (int)need;
+  if (dtype == PDEC_BF16 && K % 64)
+    return fail(PDEC_UNSUPPORTED, "bf16 projections need K % 64 == 0");
+  if (F % 4) return fail(PDEC_UNSUPPORTED, "SwiGLU needs F % 4 == 0");
+  if (ws_bytes < need || (need > 0 && !workspace))
+    return fail(PDEC_INVALID_ARG, "workspace too small: need " + std::to_string(need));
+  int ks;
+  const int S = gemm_plan_splits(dtype, M, 2 * F, K, &ks);
+  hipStream_t s = (hipStream_t)stream;
+  // The same choice as the decoder layer.
+  if (dtype == PDEC_BF16 && S == 1) {
+    HIP_OR_FAIL(launch_gemm_swiglu(M, F, K, x, K, w_gate, w_up, u, s));
+    return PDEC_OK;
+  }
+  WSegs ws{};
+  ws.ptr[0] = w_gate;
+  ws.ptr[1] = w_up;
+  ws.row_end[0] = F;
+  ws.row_end[1] = 2 * F;
+  ws.n_seg = 2;
+  HIP_OR_FAIL(launch_gemm(dtype, M, 2 * F, K, x, K, ws, (float*)workspace, S, ks, s));
+  HIP_OR_FAIL(launch_swiglu(dtype, M, F, (const float*)workspace, S, u, s));
   return PDEC_OK;
 }
 

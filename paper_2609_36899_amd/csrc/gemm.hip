@@ -63,6 +63,14 @@ __global__ __launch_bounds__(256) void pack_weight_kernel(const uint16_t* __rest
   *(u32x4*)(P + chunk * 8) = v;
 }
 
+// SwiGLU-fused form (GLU = true, gate and up given as the two segments of
+// w, N = the FFN width F, no K split): work group v takes half h = v % 2 of
+// group G = v / 2 of both matrices, and each wave the same 16 columns of the
+// gate and of the up matrix.  The two results of a column then sit in one
+// lane, and the epilogue writes silu(gate) * up as bf16 to u [M][F]: the
+// fp32 gate/up products never reach memory.
+__device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.f + expf(-g)) * u; }
+
 // Small batches (M <= 32): a work group owns one 128-column group, each of
 // its four waves two strips of it and every row of the batch (MT tiles of 16
 // rows), so no two waves share weight bytes and no LDS or barrier is needed.
@@ -71,21 +79,41 @@ __global__ __launch_bounds__(256) void pack_weight_kernel(const uint16_t* __rest
 // loop is branch-free (the prefetch index is clamped to the last step) and
 // pinned to consume-then-refill order per slot, so the compiler keeps all NS
 // slots in flight instead of draining the ring.
-template <int MT, int NS>
+template <int MT, int NS, bool GLU>
 __global__ __launch_bounds__(256) void gemm_bf16_stream(int M, int N, int K, int k_split,
                                                         const uint16_t* __restrict__ A,
                                                         int64_t lda, WSegs w,
-                                                        float* __restrict__ out) {
+                                                        float* __restrict__ out,
+                                                        uint16_t* __restrict__ glu_out) {
   constexpr int WS = 2;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int c16 = lane & 15, q4 = lane >> 4;
   const int kbeg = blockIdx.z * k_split;
   const int n_iter = (min(K, kbeg + k_split) - kbeg) / 64;
   if (n_iter <= 0) return;  // no barriers in this kernel
-  const GroupRef gr = group_ref(w, blockIdx.x, K);
 
-  // Strip 2 wave + s, k-block kb of the group: gr.base + (kb * 8 + 2 wave + s) * 512.
-  const uint16_t* wp = gr.base + ((int64_t)(kbeg / 32) * 8 + 2 * wave) * 512 + lane * 8;
+  // Strip s of this wave, k-block kb: wp[s] + kb * 4096 (a k-block of a
+  // group is 8 strips of 512 elements).  Plain: strips 2 wave and 2 wave + 1
+  // of group blockIdx.x.  GLU: strip 4 h + wave of the gate and of the up
+  // matrix's group G.
+  const uint16_t* wp[WS];
+  int col_s[WS], col_end;
+  if constexpr (GLU) {
+    const int G = blockIdx.x >> 1, h = blockIdx.x & 1;
+    const int64_t off =
+        (int64_t)G * kGroupCols * K + ((int64_t)(kbeg / 32) * 8 + 4 * h + wave) * 512 + lane * 8;
+    wp[0] = (const uint16_t*)w.ptr[0] + off;
+    wp[1] = (const uint16_t*)w.ptr[1] + off;
+    col_s[0] = col_s[1] = G * kGroupCols + (4 * h + wave) * 16 + c16;
+    col_end = N;
+  } else {
+    const GroupRef gr = group_ref(w, blockIdx.x, K);
+    wp[0] = gr.base + ((int64_t)(kbeg / 32) * 8 + 2 * wave) * 512 + lane * 8;
+    wp[1] = wp[0] + 512;
+    col_s[0] = gr.col0 + 2 * wave * 16 + c16;
+    col_s[1] = col_s[0] + 16;
+    col_end = gr.col_end;
+  }
   const uint16_t* ap[MT];
 #pragma unroll
   for (int t = 0; t < MT; ++t)
@@ -100,8 +128,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(int M, int N, int K, int
   auto load = [&](int i, bf16x8(&wr)[WS][2], bf16x8(&ar)[MT][2]) {
 #pragma unroll
     for (int s = 0; s < WS; ++s) {
-      wr[s][0] = load_stream<bf16x8>(wp + (int64_t)(2 * i) * 4096 + s * 512);
-      wr[s][1] = load_stream<bf16x8>(wp + (int64_t)(2 * i + 1) * 4096 + s * 512);
+      wr[s][0] = load_stream<bf16x8>(wp[s] + (int64_t)(2 * i) * 4096);
+      wr[s][1] = load_stream<bf16x8>(wp[s] + (int64_t)(2 * i + 1) * 4096);
     }
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
@@ -135,18 +163,27 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(int M, int N, int K, int
   for (int s = 0; s < NS; ++s)
     if (s < rem) mma(rw[s], ra[s]);
 
-  float* o = out + (int64_t)blockIdx.z * M * N;
+  if constexpr (GLU) {
 #pragma unroll
-  for (int t = 0; t < MT; ++t)
-#pragma unroll
-    for (int s = 0; s < WS; ++s) {
-      const int col = gr.col0 + (2 * wave + s) * 16 + c16;
+    for (int t = 0; t < MT; ++t)
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int row = t * 16 + 4 * q4 + rr;
-        if (row < M && col < gr.col_end) o[(int64_t)row * N + col] = acc[t][s][rr];
+        if (row < M && col_s[0] < col_end)
+          glu_out[(int64_t)row * N + col_s[0]] = f32_to_bf16(silu_mul(acc[t][0][rr], acc[t][1][rr]));
       }
-    }
+  } else {
+    float* o = out + (int64_t)blockIdx.z * M * N;
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+      for (int s = 0; s < WS; ++s)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const int row = t * 16 + 4 * q4 + rr;
+          if (row < M && col_s[s] < col_end) o[(int64_t)row * N + col_s[s]] = acc[t][s][rr];
+        }
+  }
 }
 
 // Larger batches (M > 32): (64 WM) x 128 output tiles, 2 WM waves in a WM x 2
@@ -165,12 +202,18 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(int M, int N, int K, int
 // batch size W is read from HBM exactly once per step.  Larger batches take
 // several M-blocks, laid out so the M-blocks of one column tile are
 // dispatched back to back (ids L and L+8 share an XCD).
-template <int WM>
+// GLU (gate and up as the two segments of w, N = F, no K split): column tile
+// v holds half v % 2 of group v / 2 of both matrices, its eight strips
+// staged as gate, up, gate, up, ... so that each wave's four strips are two
+// (gate, up) pairs of the same columns; the epilogue writes silu(gate) * up
+// as bf16 to u [M][F].
+template <int WM, bool GLU>
 __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, int k_split,
                                                           int n_mb, int n_nb,
                                                           const uint16_t* __restrict__ A,
                                                           int64_t lda, WSegs w,
-                                                          float* __restrict__ out) {
+                                                          float* __restrict__ out,
+                                                          uint16_t* __restrict__ glu_out) {
   constexpr int MT = 4, NT = 4, D = 3;
   constexpr int THREADS = 128 * WM, ROWS = 64 * WM;
   constexpr int ACH = ROWS * 8 / THREADS;  // A chunks per thread per stage (4)
@@ -194,7 +237,9 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
   if (n_iter <= 0) return;
   const int m_blk = mb * ROWS;
   const int wm = wave >> 1, wn = wave & 1;
-  const GroupRef gr = group_ref(w, nb, K);
+  GroupRef gr;
+  if constexpr (GLU) gr = {nullptr, (nb >> 1) * kGroupCols + (nb & 1) * 64, N};
+  else gr = group_ref(w, nb, K);
 
   // Chunk id = j * THREADS + tid lands at LDS chunk id of the stage (the DMA
   // of wave w, load j, fills chunks j * THREADS + 64 w .. +63).  A: chunk id
@@ -209,8 +254,16 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
   // 2i + (id >> 9), strip (id >> 6) & 7, lane id & 63).
   const uint16_t* wsrc[WCH];
 #pragma unroll
-  for (int j = 0; j < WCH; ++j)
-    wsrc[j] = gr.base + (int64_t)(kbeg / 32) * 4096 + (j * THREADS + tid) * 8;
+  for (int j = 0; j < WCH; ++j) {
+    const int id = j * THREADS + tid;
+    if constexpr (GLU) {  // staged strip sp: strip 4 h + sp / 2 of gate (sp even) or up
+      const int kb = id >> 9, sp = (id >> 6) & 7, ln = id & 63;
+      wsrc[j] = (const uint16_t*)w.ptr[sp & 1] + (int64_t)(nb >> 1) * kGroupCols * K +
+                ((int64_t)(kbeg / 32 + kb) * 8 + 4 * (nb & 1) + (sp >> 1)) * 512 + ln * 8;
+    } else {
+      wsrc[j] = gr.base + (int64_t)(kbeg / 32) * 4096 + id * 8;
+    }
+  }
   int aoff[MT][2];
 #pragma unroll
   for (int t = 0; t < MT; ++t)
@@ -282,18 +335,34 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
     }
   wait_vmem<0>();  // no LDS write may still be in flight when the group ends
 
-  float* o = out + (int64_t)blockIdx.z * M * N;
+  if constexpr (GLU) {
 #pragma unroll
-  for (int i = 0; i < MT; ++i)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      const int col = gr.col0 + wn * 64 + j * 16 + c16;
+      for (int p = 0; p < NT / 2; ++p) {
+        const int col = gr.col0 + (2 * wn + p) * 16 + c16;
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int row = m_blk + wm * 64 + i * 16 + 4 * q4 + rr;
-        if (row < M && col < gr.col_end) o[(int64_t)row * N + col] = acc[i][j][rr];
+        for (int rr = 0; rr < 4; ++rr) {
+          const int row = m_blk + wm * 64 + i * 16 + 4 * q4 + rr;
+          if (row < M && col < gr.col_end)
+            glu_out[(int64_t)row * N + col] =
+                f32_to_bf16(silu_mul(acc[i][2 * p][rr], acc[i][2 * p + 1][rr]));
+        }
       }
-    }
+  } else {
+    float* o = out + (int64_t)blockIdx.z * M * N;
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        const int col = gr.col0 + wn * 64 + j * 16 + c16;
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const int row = m_blk + wm * 64 + i * 16 + 4 * q4 + rr;
+          if (row < M && col < gr.col_end) o[(int64_t)row * N + col] = acc[i][j][rr];
+        }
+      }
+  }
 }
 
 // fp32 weights are row-major [N][K] (the packed layout is for bf16 only).
@@ -396,6 +465,48 @@ hipError_t launch_pack_weight(int dtype, int N, int K, const void* w, void* pack
   return hipGetLastError();
 }
 
+namespace {
+
+// The bf16 kernels over n_groups column groups (GLU: half-groups).
+template <bool GLU>
+hipError_t launch_gemm_bf16(int M, int N, int K, const uint16_t* a, int64_t lda, const WSegs& w,
+                            int n_groups, float* out, uint16_t* glu_out, int splits, int k_split,
+                            hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
+  if (M <= kStreamMaxRows) {
+    const dim3 grid(n_groups, 1, splits);
+    if (M <= 16)
+      return launch_timed(gemm_bf16_stream<1, 2, GLU>, grid, dim3(256), stream, ev_start,
+                          ev_stop, M, N, K, k_split, a, lda, w, out, glu_out);
+    return launch_timed(gemm_bf16_stream<2, 2, GLU>, grid, dim3(256), stream, ev_start, ev_stop,
+                        M, N, K, k_split, a, lda, w, out, glu_out);
+  }
+  const int rows = tile_rows(M);
+  const int n_mb = (M + rows - 1) / rows, n_nb = n_groups;
+  const dim3 grid(((n_nb + 7) / 8) * 8 * n_mb, 1, splits);
+  if (rows == 128)
+    return launch_timed(gemm_bf16_tile<2, GLU>, grid, dim3(256), stream, ev_start, ev_stop, M, N,
+                        K, k_split, n_mb, n_nb, a, lda, w, out, glu_out);
+  return launch_timed(gemm_bf16_tile<4, GLU>, grid, dim3(512), stream, ev_start, ev_stop, M, N, K,
+                      k_split, n_mb, n_nb, a, lda, w, out, glu_out);
+}
+
+}  // namespace
+
+hipError_t launch_gemm_swiglu(int M, int F, int K, const void* A, int64_t lda, const void* w_gate,
+                              const void* w_up, void* u, hipStream_t stream, hipEvent_t ev_start,
+                              hipEvent_t ev_stop) {
+  if (M <= 0 || F <= 0) return hipSuccess;
+  WSegs w{};
+  w.ptr[0] = w_gate;
+  w.ptr[1] = w_up;
+  w.row_end[0] = F;
+  w.row_end[1] = 2 * F;
+  w.n_seg = 2;
+  const int halves = 2 * ((F + kGroupCols - 1) / kGroupCols);
+  return launch_gemm_bf16<true>(M, F, K, (const uint16_t*)A, lda, w, halves, nullptr,
+                                (uint16_t*)u, 1, K, stream, ev_start, ev_stop);
+}
+
 hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t lda,
                        const WSegs& w_in, float* out, int splits, int k_split, hipStream_t stream,
                        hipEvent_t ev_start, hipEvent_t ev_stop) {
@@ -410,24 +521,8 @@ hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t ld
       w.grp_end[s] = n_groups;
       start = w.row_end[s];
     }
-    const uint16_t* a = (const uint16_t*)A;
-    if (M <= kStreamMaxRows) {
-      const dim3 grid(n_groups, 1, splits);
-      if (M <= 16)
-        return launch_timed(gemm_bf16_stream<1, 2>, grid, block, stream, ev_start, ev_stop, M, N,
-                            K, k_split, a, lda, w, out);
-      return launch_timed(gemm_bf16_stream<2, 2>, grid, block, stream, ev_start, ev_stop, M, N,
-                          K, k_split, a, lda, w, out);
-    } else {
-      const int rows = tile_rows(M);
-      const int n_mb = (M + rows - 1) / rows, n_nb = n_groups;
-      const dim3 grid(((n_nb + 7) / 8) * 8 * n_mb, 1, splits);
-      if (rows == 128)
-        return launch_timed(gemm_bf16_tile<2>, grid, dim3(256), stream, ev_start, ev_stop, M, N,
-                            K, k_split, n_mb, n_nb, a, lda, w, out);
-      return launch_timed(gemm_bf16_tile<4>, grid, dim3(512), stream, ev_start, ev_stop, M, N, K,
-                          k_split, n_mb, n_nb, a, lda, w, out);
-    }
+    return launch_gemm_bf16<false>(M, N, K, (const uint16_t*)A, lda, w, n_groups, out, nullptr,
+                                   splits, k_split, stream, ev_start, ev_stop);
   } else {
     const dim3 grid((N + 63) / 64, (M + 31) / 32, splits);
     return launch_timed(gemm_f32_tiled, grid, block, stream, ev_start, ev_stop, M, N, K, k_split,

@@ -67,6 +67,13 @@ hipError_t launch_attention_combine(int head_dim, int rows_per_item, int n_qbloc
 hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t lda,
                        const WSegs& w, float* out, int splits, int k_split, hipStream_t stream,
                        hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+// bf16 gate/up projection with the SwiGLU epilogue, no K split:
+// u[m][n] = bf16(silu(g) * up), g and up the products of row m of A with
+// column n of the packed gate and up matrices ([F][K] each), n < F.  Equals
+// launch_gemm over the two segments (splits = 1) followed by launch_swiglu.
+hipError_t launch_gemm_swiglu(int M, int F, int K, const void* A, int64_t lda, const void* w_gate,
+                              const void* w_up, void* u, hipStream_t stream,
+                              hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 // Temperature / top-p sampling (sample.hip).
 hipError_t launch_sample_top_p(int B, int V, const float* logits, float temperature, float top_p,
                                const float* uniforms, int32_t* tokens, hipStream_t stream);

@@ -274,6 +274,27 @@ class Engine:
                                 int(mode)))
 
 
+def swiglu_projection(x: torch.Tensor, w_gate: PackedWeight, w_up: PackedWeight,
+                      u: torch.Tensor, workspace: Optional[torch.Tensor] = None,
+                      stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """u = silu(x Wg^T) * (x Wu^T) through the library's kernels; see include/pdec.h."""
+    rows, k = x.shape
+    ffn = w_gate.n
+    assert isinstance(w_gate, PackedWeight) and isinstance(w_up, PackedWeight)
+    assert w_up.n == ffn and w_gate.k == k and w_up.k == k and x.is_contiguous()
+    assert w_gate.dtype == w_up.dtype and x.dtype == _TORCH_DTYPE[w_gate.dtype]
+    assert u.dtype == x.dtype and tuple(u.shape) == (rows, ffn) and u.is_contiguous()
+    lib = N.load()
+    need = N.check(lib.swiglu_projection_workspace_bytes(w_gate.dtype, rows, ffn, k))
+    if need and (workspace is None or workspace.numel() < need):
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    N.check(lib.swiglu_projection(w_gate.dtype, rows, ffn, k, x.data_ptr(), w_gate.data_ptr(),
+                                  w_up.data_ptr(), u.data_ptr(),
+                                  workspace.data_ptr() if need else None,
+                                  workspace.numel() if need else 0, _stream_handle(stream)))
+    return u
+
+
 def weight_projection_workspace_bytes(dtype: int, rows: int, cols: int, k: int) -> int:
     """Scratch bytes weight_projection needs for split-K partials (0 if none)."""
     return N.check(N.load().weight_projection_workspace_bytes(dtype, rows, cols, k))

@@ -70,3 +70,9 @@ def test_host_only_calls_without_gpu():
     assert lib.packed_weight_bytes(N.F32, 100, 96) == 100 * 96 * 4
     assert lib.packed_weight_bytes(N.BF16, 100, 96) == N.UNSUPPORTED  # K % 64
     assert lib.packed_weight_bytes(N.BF16, 0, 64) == N.INVALID_ARG
+    # SwiGLU projection scratch: none where the bf16 plan has no K split (the
+    # fused epilogue), the split-K partials of gate|up otherwise
+    assert lib.swiglu_projection_workspace_bytes(N.BF16, 256, 14336, 4096) == 0
+    assert lib.swiglu_projection_workspace_bytes(N.BF16, 4, 256, 256) > 0
+    assert lib.swiglu_projection_workspace_bytes(N.F32, 4, 688, 256) > 0
+    assert lib.swiglu_projection_workspace_bytes(N.BF16, 0, 256, 256) == N.INVALID_ARG

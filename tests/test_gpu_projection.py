@@ -79,3 +79,59 @@ def test_pack_layout(N, K):
             q, e = divmod(r2, 8)
             expect[(((G * (K // 32) + b) * 8 + s) * 64 + q * 16 + c) * 8 + e] = w[n, k] % 65536
     np.testing.assert_array_equal(got, expect)
+
+
+def _swiglu_run(M, F, K, bf16=True, seed=0):
+    """u = silu(x Wg^T) * (x Wu^T) through swiglu_projection against the
+    oracle's silu on float64 products of the same (bf16-representable)
+    inputs.  bf16 u is rounded to nearest even: per row,
+    max|gpu - ref| <= 2^-8 * max|ref| (half an ulp is 2^-9 of the element,
+    fp32 accumulation adds < 1e-5); fp32 u: 1e-4 * max|ref|."""
+    import paper_2609_36899_amd as P
+    from oracle import decoder as od
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((M, K), dtype=np.float32) * np.float32(3.0)
+    wg = rng.standard_normal((F, K), dtype=np.float32) * np.float32(0.02)
+    wu = rng.standard_normal((F, K), dtype=np.float32) * np.float32(0.02)
+    if bf16:
+        x, wg, wu = round_to_bf16(x), round_to_bf16(wg), round_to_bf16(wu)
+    td = torch.bfloat16 if bf16 else torch.float32
+    xd = torch.from_numpy(x).cuda().to(td).contiguous()
+    pg = P.pack_weight(torch.from_numpy(wg).cuda().to(td).contiguous())
+    pu = P.pack_weight(torch.from_numpy(wu).cuda().to(td).contiguous())
+    u = torch.full((M, F), float("nan"), dtype=td, device="cuda")
+    P.swiglu_projection(xd, pg, pu, u)
+    got = u.float().cpu().numpy()
+    x64 = x.astype(np.float64)
+    ref = od.silu(x64 @ wg.astype(np.float64).T) * (x64 @ wu.astype(np.float64).T)
+    tol = 2.0 ** -8 if bf16 else 1e-4
+    assert np.isfinite(got).all()
+    for r in range(M):
+        err = np.max(np.abs(got[r] - ref[r]))
+        assert err <= tol * np.max(np.abs(ref[r])), (M, F, K, r, err)
+
+
+@pytest.mark.parametrize("M", [1, 16, 17, 32, 33, 128, 129, 256, 300])
+@pytest.mark.parametrize("F,K", [(8256, 320), (16320, 256)])
+def test_swiglu_fused_epilogue(M, F, K):
+    """Shapes whose bf16 plan has no K split: the SwiGLU runs in the GEMM's
+    epilogue (streaming kernel up to 32 rows, 128- and 256-row tiles above,
+    two M-blocks at 300 rows).  F = 8256 and 16320 end in a half-filled
+    column group, whose empty half writes nothing."""
+    import paper_2609_36899_amd as P
+    from paper_2609_36899_amd import _native as N
+    assert N.load().swiglu_projection_workspace_bytes(N.BF16, M, F, K) == 0
+    _swiglu_run(M, F, K, seed=M + F)
+
+
+@pytest.mark.parametrize("M", [4, 64])
+def test_swiglu_split_k(M):
+    """A narrow FFN (F = 256): the plan splits K, the partials go through the
+    workspace and the separate SwiGLU kernel."""
+    from paper_2609_36899_amd import _native as N
+    assert N.load().swiglu_projection_workspace_bytes(N.BF16, M, 256, 512) > 0
+    _swiglu_run(M, 256, 512, seed=M)
+
+
+def test_swiglu_f32():
+    _swiglu_run(4, 688, 256, bf16=False, seed=9)
