@@ -195,7 +195,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_stream(int M, int N, int K, int
 // it, every wave has finished step it-1, whose stage then takes step it+2.
 // The W tile (one packed group, 2 k-blocks x 8 strips) is one contiguous
 // 16 KiB run in HBM, copied in packed order (fragment reads from LDS are
-// linear, hence free of bank conflicts); the A tile is row-major with its
+// linear, hence free of bank conflicts) with the non-temporal hint, so the
+// weight stream does not push the re-read A tiles out of L2; the A tile is row-major with its
 // 16-byte chunks XOR-swizzled by
 // row (the swizzle is applied to the source address, as the DMA writes each
 // wave's 64 chunks contiguously).  WM = 4 covers 256 rows, so up to that
@@ -284,7 +285,8 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
 #pragma unroll
     for (int j = 0; j < ACH; ++j) dma16(asrc[j] + i * 64, base + j * THREADS * 8);
 #pragma unroll
-    for (int j = 0; j < WCH; ++j) dma16(wsrc[j] + (int64_t)i * 8192, base + SA + j * THREADS * 8);
+    for (int j = 0; j < WCH; ++j)
+      dma16_stream(wsrc[j] + (int64_t)i * 8192, base + SA + j * THREADS * 8);
   };
   auto compute = [&](int b) {
     const uint16_t* la = stage_ptr(b);

@@ -34,6 +34,12 @@ __device__ __forceinline__ void dma16(const void* src, void* lds) {
   __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
                                    (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
 }
+// The same with the non-temporal hint (nt), for data read once per launch
+// (streamed weights): it leaves the L2 to the operands that are re-read.
+__device__ __forceinline__ void dma16_stream(const void* src, void* lds) {
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                   (__attribute__((address_space(3))) void*)lds, 16, 0, 2);
+}
 
 // Wait until at most N vector-memory operations of this wave are outstanding
 // (loads retire in issue order), leaving the other counters alone.

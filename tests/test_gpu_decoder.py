@@ -243,6 +243,50 @@ def test_bf16_wide_ffn_fused_swiglu_parity():
                  pool_tokens=2048, max_seq_len=1024)
 
 
+LONG_G4 = dict(n_layers=1, d_model=256, n_q_heads=8, n_kv_heads=2, head_dim=128, ffn_dim=256,
+               vocab=512)
+
+
+@pytest.mark.parametrize("kv_fp8", [None, (0.5, 0.25)])
+def test_decode_many_items_per_sequence(kv_fp8):
+    """Decode attention over many split items per sequence: contexts of 3000
+    and 700 tokens give 24 and 6 items of 8 pages (several items per wave of
+    the merge pass), 17 tokens a single item; GQA groups of 4 as in the 8B
+    shape, bf16 and fp8 pages."""
+    _bf16_parity(ModelShape(**LONG_G4), seed=14, prefix_lens=[3000, 700, 17], n_steps=3,
+                 chunk=1024, kv_fp8=kv_fp8, pool_tokens=4096, max_seq_len=4096)
+
+
+def test_decode_many_items_batch_order_is_bitwise_invariant():
+    """Sequences of many split items decoded in three batch orders (and so
+    with different item ids, dispatch slots and physical pages): the merge
+    reads each block's partials in item order, so the logits are bitwise
+    the same."""
+    shape = ModelShape(**LONG_G4)
+    arrays = make_weights(shape, seed=15, bf16=True)
+    E = _engine(shape, arrays, bf16=True, pool_tokens=4096, max_seq_len=2048, max_chunk=512)
+    lens = [900, 40, 300, 1500]
+    prefixes = [random_tokens(n, shape.vocab, seed=50 + i) for i, n in enumerate(lens)]
+    tok = random_tokens(len(lens), shape.vocab, seed=60)
+    outs = []
+    for order in ([0, 1, 2, 3], [3, 1, 0, 2], [2, 3, 1, 0]):
+        seqs = []
+        for i in order:
+            s = E.kv_alloc(0)
+            E.kv_append_prefix(s, prefixes[i], chunk_tokens=512)
+            seqs.append(s)
+        lb = _logits_buf(len(seqs), shape.vocab)
+        E.decode_step(seqs, torch.from_numpy(tok[order]).cuda(), lb)
+        got = lb.cpu().numpy()
+        res = np.empty_like(got)
+        res[order] = got
+        outs.append(res)
+        for s in seqs:
+            E.kv_free(s)
+    for o in outs[1:]:
+        np.testing.assert_array_equal(outs[0], o)
+
+
 def test_fp8_kv_decoder_parity():
     """KV pages as E4M3 codes: the oracle quantises its own float64 k and v
     with the same rule; a code can differ where the GPU's float32 value sits
