@@ -345,8 +345,11 @@ hipError_t launch_qkv_rope_kv(int dtype, int kv_fp8, float k_scale, float v_scal
                               const float* q_gain, const float* k_gain, float eps,
                               hipStream_t stream) {
   if (M == 0) return hipSuccess;
-  // Enough groups per row that small batches still fill the GPU.
-  const dim3 grid(M, M >= 64 ? 2 : 8);
+  // Enough groups per row that every thread has at most one (q or k) quad,
+  // so no group runs a second, mostly idle pass; small batches take more
+  // groups per row to fill the GPU.
+  const int n_quads = (n_q_heads + n_kv_heads) * (head_dim / 8);
+  const dim3 grid(M, std::max(M >= 64 ? 2 : 8, (n_quads + kRowThreads - 1) / kRowThreads));
 #define PDEC_QKV(T_, KVT_)                                                                   \
   qkv_rope_kv_kernel<T_, KVT_><<<grid, kRowThreads, 0, stream>>>(                             \
       M, head_dim, n_q_heads, n_kv_heads, part, splits, rows, rope_cs, block_table, bt_stride, \
