@@ -5,8 +5,8 @@
 // blocks: 128/G queries of one chunk times the G query heads of a GQA group.
 // Such blocks are MFMA-bound rather than HBM-bound, so this kernel shares each
 // page between four waves through LDS instead of letting every wave stream it.
-// It writes the same partials as the decode split kernel and is merged by the
-// same combine pass.
+// It writes the same partials as the decode split kernel; they are merged by
+// the row-split merge pass below.
 #include "hip_common.h"
 #include "kernels.h"
 
@@ -268,7 +268,100 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   }
 }
 
+// ---------------------------------------------------------------------------
+// Merge of prefill partials.  A prefill query block has up to 128 rows and a
+// handful of items, so the work is split by rows, not by items: a work group
+// of 4 waves takes 16 rows (4 per wave, 16 lanes x DH/16 dims per row) and
+// each row merges all of its block's items in item order with the
+// online-softmax rule (m = max(m, m_i); l = l 2^(m_old-m) + l_i 2^(m_i-m);
+// o likewise; output o / l), four items' loads in flight at a time.  No
+// LDS and no barriers; the result does not depend on which work group runs
+// when.
+// ---------------------------------------------------------------------------
+template <int DPL>
+__device__ __forceinline__ void merge_row(float& m, float& l, float* o, float mi, float li,
+                                          const float* oi) {
+  const float mn = fmaxf(m, mi);
+  const float mu = (mn == -INFINITY) ? 0.f : mn;  // both empty: keep zeros
+  const float so = exp2f(m - mu), si = exp2f(mi - mu);
+  l = l * so + li * si;
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) o[e] = o[e] * so + oi[e] * si;
+  m = mn;
+}
+
+template <int DH, typename OutT>
+__global__ __launch_bounds__(256) void attn_combine_rows(const AttnQBlock* __restrict__ qblocks,
+                                                         const float* __restrict__ part_ml,
+                                                         const float* __restrict__ part_acc,
+                                                         int32_t n_q_heads, int32_t n_kv_heads,
+                                                         int32_t R, OutT* __restrict__ out) {
+  constexpr int DPL = DH / 16;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int d0 = (lane & 15) * DPL;
+  const AttnQBlock qb = qblocks[blockIdx.x];
+  const int g = blockIdx.y;
+  const int G = n_q_heads / n_kv_heads;
+  const int r = blockIdx.z * 16 + wave * 4 + (lane >> 4);
+  if (r >= qb.n_q * G) return;  // no barriers in this kernel
+  float m = -INFINITY, l = 0.f, o[DPL];
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) o[e] = 0.f;
+  for (int i0 = qb.item_begin; i0 < qb.item_end; i0 += 4) {
+    float2 ml[4];
+    float a[4][DPL];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = min(i0 + u, qb.item_end - 1);
+      const int64_t prow = ((int64_t)i * n_kv_heads + g) * R + r;
+      ml[u] = *(const float2*)(part_ml + prow * 2);
+#pragma unroll
+      for (int e = 0; e < DPL; e += 4) {
+        const float4 v = *(const float4*)(part_acc + prow * DH + d0 + e);
+        a[u][e] = v.x;
+        a[u][e + 1] = v.y;
+        a[u][e + 2] = v.z;
+        a[u][e + 3] = v.w;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (i0 + u >= qb.item_end) break;
+      merge_row<DPL>(m, l, o, ml[u].x, ml[u].y, a[u]);
+    }
+  }
+  const float inv = 1.f / l;
+  const int jq = r / G, head = g * G + r % G;
+  OutT* orow = out + ((int64_t)(qb.q_row0 + jq) * n_q_heads + head) * DH + d0;
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) orow[e] = Store<OutT>::from(o[e] * inv);
+}
+
 }  // namespace
+
+hipError_t launch_attention_combine_rows(int head_dim, int rows_per_item, int n_qblocks,
+                                         int n_q_heads, int n_kv_heads, const AttnQBlock* qblocks,
+                                         const float* part_ml, const float* part_acc, void* out,
+                                         int out_bf16, hipStream_t stream) {
+  if (n_qblocks == 0) return hipSuccess;
+  const dim3 grid(n_qblocks, n_kv_heads, (rows_per_item + 15) / 16);
+  if (head_dim == 128) {
+    if (out_bf16)
+      attn_combine_rows<128, uint16_t><<<grid, 256, 0, stream>>>(
+          qblocks, part_ml, part_acc, n_q_heads, n_kv_heads, rows_per_item, (uint16_t*)out);
+    else
+      attn_combine_rows<128, float><<<grid, 256, 0, stream>>>(
+          qblocks, part_ml, part_acc, n_q_heads, n_kv_heads, rows_per_item, (float*)out);
+  } else {
+    if (out_bf16)
+      attn_combine_rows<64, uint16_t><<<grid, 256, 0, stream>>>(
+          qblocks, part_ml, part_acc, n_q_heads, n_kv_heads, rows_per_item, (uint16_t*)out);
+    else
+      attn_combine_rows<64, float><<<grid, 256, 0, stream>>>(
+          qblocks, part_ml, part_acc, n_q_heads, n_kv_heads, rows_per_item, (float*)out);
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_attention_prefill_bf16(int n_items, int n_q_heads, int n_kv_heads,
                                          const AttnItem* items, const AttnQBlock* qblocks,

@@ -425,9 +425,14 @@ int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
                                        d_it, d_qb,
                                        E->q, E->k_layer(l), E->v_layer(l), E->page_stride, E->bt,
                                        E->ws.bt_stride, E->att_ml, E->att_acc, s, ea, eb));
-    HIP_OR_FAIL(launch_attention_combine(Dh, rows_per_item, n_qb, max_items, c.n_q_heads,
-                                         c.n_kv_heads, d_qb, E->att_ml, E->att_acc, E->o,
-                                         dt == PDEC_BF16, s));
+    if (rows_per_item == kDecodeRows)
+      HIP_OR_FAIL(launch_attention_combine(Dh, rows_per_item, n_qb, max_items, c.n_q_heads,
+                                           c.n_kv_heads, d_qb, E->att_ml, E->att_acc, E->o,
+                                           dt == PDEC_BF16, s));
+    else  // prefill: up to 128 rows and few items per block
+      HIP_OR_FAIL(launch_attention_combine_rows(Dh, rows_per_item, n_qb, c.n_q_heads,
+                                                c.n_kv_heads, d_qb, E->att_ml, E->att_acc, E->o,
+                                                dt == PDEC_BF16, s));
     S = gemm_plan_splits(dt, M, d, qd, &ks);
     HIP_OR_FAIL(E->timer.pair(PDEC_TIMER_GEMM, &ea, &eb));
     HIP_OR_FAIL(launch_gemm(dt, M, d, qd, E->o, qd, E->w_o[l], E->part, S, ks, s, ea, eb));

@@ -51,6 +51,14 @@ hipError_t launch_attention_prefill_bf16(int n_items, int n_q_heads, int n_kv_he
                                          hipEvent_t ev_start = nullptr,
                                          hipEvent_t ev_stop = nullptr);
 
+// Merge pass for prefill blocks (rows_per_item >= 64): one work group per
+// (query block, KV head, 16 rows), each row merging its block's items in
+// item order; same partial layout and output as launch_attention_combine.
+hipError_t launch_attention_combine_rows(int head_dim, int rows_per_item, int n_qblocks,
+                                         int n_q_heads, int n_kv_heads, const AttnQBlock* qblocks,
+                                         const float* part_ml, const float* part_acc, void* out,
+                                         int out_bf16, hipStream_t stream);
+
 // Merge pass: one work group per (query block, KV head); writes
 // out [rows][n_q_heads][head_dim] as fp32 (out_bf16 = 0) or bf16.
 hipError_t launch_attention_combine(int head_dim, int rows_per_item, int n_qblocks,
