@@ -367,6 +367,180 @@ __global__ __launch_bounds__(128 * WM) void gemm_bf16_tile(int M, int N, int K, 
   }
 }
 
+// Batches above 256 rows (prefill chunks, B = 512 decode): 256 x 256 output
+// tiles, 8 waves in a 4 x 2 grid of 64 x 128 sub-tiles (each wave's columns
+// are one packed group, NT = 8 strips).  Against the 256 x 128 tile this
+// halves the A bytes each output needs from L2 (the A tile is shared by two
+// column groups) and reads 12 fragments from LDS per 32 MFMAs instead of 16.
+// Stages hold one k-block (32): A 256 rows x 64 B (16-byte chunks swizzled
+// by row so that the 16 rows of a fragment read hit distinct banks) and W
+// 2 groups x 8 strips (two contiguous 8 KiB runs); a ring of four stages
+// keeps three k-blocks in flight.  Column tile v covers groups 2v and 2v + 1
+// (the second clamped to a valid group and its outputs dropped when the
+// group count is odd); GLU: column tile v is group v of both matrices, wave
+// column wn taking half wn of it with its strips staged as gate, up, gate,
+// up, ... (four (gate, up) pairs per wave), and the epilogue writes
+// silu(gate) * up as bf16.
+template <bool GLU>
+__global__ __launch_bounds__(512) void gemm_bf16_wide(int M, int N, int K, int k_split,
+                                                     int n_mb, int n_nb, int n_groups,
+                                                     const uint16_t* __restrict__ A,
+                                                     int64_t lda, WSegs w,
+                                                     float* __restrict__ out,
+                                                     uint16_t* __restrict__ glu_out) {
+  constexpr int MT = 4, NT = 8, D = 4, THREADS = 512, ROWS = 256;
+  constexpr int ACH = ROWS * 4 / THREADS;  // A chunks per thread per stage (2)
+  constexpr int WCH = 1024 / THREADS;      // W chunks per thread per stage (2)
+  constexpr int LPS = ACH + WCH;
+  constexpr int SA = ROWS * 32, STAGE = SA + 2 * 8 * 512;  // elements
+  __shared__ __attribute__((aligned(16))) uint16_t lds0[STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t lds1[STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t lds2[STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t lds3[STAGE];
+  auto stage_ptr = [&](int b) -> uint16_t* {
+    return b == 0 ? lds0 : b == 1 ? lds1 : b == 2 ? lds2 : lds3;
+  };
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int c16 = lane & 15, q4 = lane >> 4;
+  const int L = blockIdx.x;
+  const int grp = L / (8 * n_mb), rem = L % (8 * n_mb);
+  const int mb = rem / 8, nb = grp * 8 + rem % 8;
+  if (nb >= n_nb) return;  // padding of the id layout; uniform over the group
+  const int kbeg = blockIdx.z * k_split;
+  const int n_iter = (min(K, kbeg + k_split) - kbeg) / 32;
+  if (n_iter <= 0) return;
+  const int m_blk = mb * ROWS;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // This wave's output columns: strip t covers col0 + 16 t .. + 15 (plain) or
+  // the pair p = t / 2 covers col0 + 16 p .. + 15 (GLU).
+  int col0, col_end;
+  if constexpr (GLU) {
+    col0 = nb * kGroupCols + wn * 64;
+    col_end = N;
+  } else {
+    const int gw = 2 * nb + wn;
+    const GroupRef gr = group_ref(w, min(gw, n_groups - 1), K);
+    col0 = gr.col0;
+    col_end = gw < n_groups ? gr.col_end : 0;  // a clamped second group writes nothing
+  }
+
+  // A: chunk id = row * 4 + slot, holding source chunk slot ^ ((row >> 2) & 3).
+  const uint16_t* asrc[ACH];
+#pragma unroll
+  for (int j = 0; j < ACH; ++j) {
+    const int id = j * THREADS + tid, r = id >> 2, slot = id & 3;
+    asrc[j] = A + (int64_t)min(m_blk + r, M - 1) * lda + kbeg + ((slot ^ ((r >> 2) & 3)) * 8);
+  }
+  // W: chunk id = (g2 * 8 + sp) * 64 + lane of staged group g2 (the wave
+  // column that reads it), staged strip sp.
+  const uint16_t* wsrc[WCH];
+#pragma unroll
+  for (int j = 0; j < WCH; ++j) {
+    const int id = j * THREADS + tid, g2 = id >> 9, sp = (id >> 6) & 7, ln = id & 63;
+    if constexpr (GLU) {
+      wsrc[j] = (const uint16_t*)w.ptr[sp & 1] + (int64_t)nb * kGroupCols * K +
+                ((int64_t)(kbeg / 32) * 8 + 4 * g2 + (sp >> 1)) * 512 + ln * 8;
+    } else {
+      const GroupRef gs = group_ref(w, min(2 * nb + g2, n_groups - 1), K);
+      wsrc[j] = gs.base + ((int64_t)(kbeg / 32) * 8 + sp) * 512 + ln * 8;
+    }
+  }
+  int aoff[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+    const int ra = wm * 64 + t * 16 + c16;
+    aoff[t] = ra * 32 + ((q4 ^ ((ra >> 2) & 3)) * 8);
+  }
+
+  f32x4 acc[MT][NT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto issue = [&](int i, int b) {
+    uint16_t* base = stage_ptr(b) + wave * 64 * 8;
+#pragma unroll
+    for (int j = 0; j < ACH; ++j) dma16(asrc[j] + i * 32, base + j * THREADS * 8);
+#pragma unroll
+    for (int j = 0; j < WCH; ++j)
+      dma16_stream(wsrc[j] + (int64_t)i * 4096, base + SA + j * THREADS * 8);
+  };
+  auto compute = [&](int b) {
+    const uint16_t* la = stage_ptr(b);
+    const uint16_t* lw = la + SA + wn * 8 * 512;
+    bf16x8 af[MT], bf[NT];
+#pragma unroll
+    for (int t = 0; t < MT; ++t) af[t] = *(const bf16x8*)(la + aoff[t]);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) bf[t] = *(const bf16x8*)(lw + (t * 64 + lane) * 8);
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+  };
+  // As in the 256 x 128 tile: every step issues one stage (the prefetch index
+  // clamped to the last step), so waiting until D - 2 stages are outstanding
+  // means this wave's part of step it has landed; the barrier covers the
+  // other waves' parts and frees the stage that step it + D - 1 refills.
+  const int last = n_iter - 1;
+#pragma unroll
+  for (int s = 0; s < D - 1; ++s) issue(min(s, last), s);
+  int it = 0;
+  for (; it + D <= n_iter; it += D) {
+#pragma unroll
+    for (int s = 0; s < D; ++s) {
+      wait_vmem<(D - 2) * LPS>();
+      wg_barrier();
+      issue(min(it + s + D - 1, last), (s + D - 1) % D);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(s);
+    }
+  }
+  const int tail = n_iter - it;  // uniform over the work group
+#pragma unroll
+  for (int s = 0; s < D; ++s)
+    if (s < tail) {
+      wait_vmem<(D - 2) * LPS>();
+      wg_barrier();
+      issue(min(it + s + D - 1, last), (s + D - 1) % D);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(s);
+    }
+  wait_vmem<0>();  // no LDS write may still be in flight when the group ends
+
+  if constexpr (GLU) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int p = 0; p < NT / 2; ++p) {
+        const int col = col0 + p * 16 + c16;
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const int row = m_blk + wm * 64 + i * 16 + 4 * q4 + rr;
+          if (row < M && col < col_end)
+            glu_out[(int64_t)row * N + col] =
+                f32_to_bf16(silu_mul(acc[i][2 * p][rr], acc[i][2 * p + 1][rr]));
+        }
+      }
+  } else {
+    float* o = out + (int64_t)blockIdx.z * M * N;
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        const int col = col0 + j * 16 + c16;
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const int row = m_blk + wm * 64 + i * 16 + 4 * q4 + rr;
+          if (row < M && col < col_end) o[(int64_t)row * N + col] = acc[i][j][rr];
+        }
+      }
+  }
+}
+
 // fp32 weights are row-major [N][K] (the packed layout is for bf16 only).
 __device__ __forceinline__ const void* seg_row(const WSegs& w, int n, int64_t row_elems,
                                                int elem_bytes) {
@@ -430,8 +604,16 @@ __global__ __launch_bounds__(256) void gemm_f32_tiled(int M, int N, int K, int k
 constexpr int kStreamMaxRows = 32;
 
 // Rows per tile: 128 (4 waves) up to 128-row batches, 256 (8 waves) beyond,
-// so W is read once per step for batches up to 256.
+// so W is read once per step for batches up to 256.  Above 256 rows the
+// 256 x 256 tile (two column groups per work group).
 int tile_rows(int M) { return M <= 128 ? 128 : 256; }
+// The 256 x 256 tile is taken only where its grid alone fills the GPU
+// (gate/up and the LM head at any M > 256, qkv only past ~2300 rows): where
+// it would need more K splits than the 256 x 128 tile (o, down, qkv at
+// 384-1024 rows) the extra partial traffic made it 5-45% slower.
+bool wide_tiles(int M, int64_t groups) {
+  return M > 256 && ((groups + 1) / 2) * ((M + 255) / 256) >= 224;
+}
 
 int gemm_plan_splits(int dtype, int M, int N, int K, int* k_split) {
   const int kq = (dtype == 1) ? 64 : 16;
@@ -440,7 +622,8 @@ int gemm_plan_splits(int dtype, int M, int N, int K, int* k_split) {
   if (dtype == 1) {
     // Work groups per split: one per 128-column group (times the M-blocks).
     int64_t groups = (N + kGroupCols - 1) / kGroupCols;
-    if (M > kStreamMaxRows) groups *= (M + tile_rows(M) - 1) / tile_rows(M);
+    if (wide_tiles(M, groups)) groups = ((groups + 1) / 2) * ((M + 255) / 256);
+    else if (M > kStreamMaxRows) groups *= (M + tile_rows(M) - 1) / tile_rows(M);
     // Measured on the 8B shapes with weights streamed from HBM: the best
     // split count fills one round of work groups on the 256 CUs (a partial
     // second round costs 15-30%).
@@ -474,6 +657,8 @@ template <bool GLU>
 hipError_t launch_gemm_bf16(int M, int N, int K, const uint16_t* a, int64_t lda, const WSegs& w,
                             int n_groups, float* out, uint16_t* glu_out, int splits, int k_split,
                             hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
+  // Plain matrices given as several segments (q|k|v) keep the 256 x 128 tile.
+  const bool wide = wide_tiles(M, n_groups) && (GLU || w.n_seg == 1);
   if (M <= kStreamMaxRows) {
     const dim3 grid(n_groups, 1, splits);
     if (M <= 16)
@@ -481,6 +666,13 @@ hipError_t launch_gemm_bf16(int M, int N, int K, const uint16_t* a, int64_t lda,
                           ev_stop, M, N, K, k_split, a, lda, w, out, glu_out);
     return launch_timed(gemm_bf16_stream<2, 2, GLU>, grid, dim3(256), stream, ev_start, ev_stop,
                         M, N, K, k_split, a, lda, w, out, glu_out);
+  }
+  if (wide) {
+    // GLU: n_groups counts half-groups; a wide column tile is one whole group.
+    const int n_mb = (M + 255) / 256, n_nb = GLU ? n_groups / 2 : (n_groups + 1) / 2;
+    const dim3 grid(((n_nb + 7) / 8) * 8 * n_mb, 1, splits);
+    return launch_timed(gemm_bf16_wide<GLU>, grid, dim3(512), stream, ev_start, ev_stop, M, N, K,
+                        k_split, n_mb, n_nb, n_groups, a, lda, w, out, glu_out);
   }
   const int rows = tile_rows(M);
   const int n_mb = (M + rows - 1) / rows, n_nb = n_groups;

@@ -52,6 +52,16 @@ def test_bf16_8b_shapes_sampled_rows(M, N, K):
     _run(M, N, K, seed=N + M, rows=rows)
 
 
+@pytest.mark.parametrize("M", [257, 300, 520])
+def test_bf16_wide_tiles(M):
+    """256 x 256 tiles (two column groups per work group), taken above 256
+    rows when their grid fills the GPU: N = 28736 is 225 groups, so the last
+    work group's second group is clamped and writes nothing, the last group
+    is half-filled, and 520 rows end in a partial third M-block."""
+    rows = sorted(set([0, 1, M // 2, M - 2, M - 1]))
+    _run(M, 28736, 320, seed=M, rows=rows)
+
+
 @pytest.mark.parametrize("M", [1, 4, 33])
 def test_f32(M):
     _run(M, 688, 256, bf16=False, seed=M)
