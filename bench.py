@@ -773,7 +773,8 @@ PROJ_SHAPES = [("qkv", 6144, 4096), ("o", 4096, 4096), ("gate_up", 28672, 4096),
 
 
 def run_projections(batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), iters=24):
-    """The 8B projection shapes through weight_projection, swept over the batch.
+    """The 8B projection shapes through weight_projection, swept over the batch,
+    and the gate/up pair through swiglu_projection (the decode step's path).
 
     Per shape and batch: time per call (HIP events), weight-stream GB/s,
     TFLOP/s, and the roofline time max(weights / 8 TB/s, flops / 2.5 PF/s).
@@ -828,10 +829,35 @@ def run_projections(batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), iters=24):
         del raw, packed
         torch.cuda.empty_cache()
         log(f"projections {name} done")
+    # The decode step's own gate/up path: both matrices in one call with the
+    # SwiGLU applied in the GEMM epilogue where the plan has no K split.
+    from workload import EIGHT_B
+    F, d = EIGHT_B.ffn_dim, EIGHT_B.d_model
+    copies = max(1, -(-(768 << 20) // (4 * F * d)))
+    pairs = [[P.pack_weight(torch.empty((F, d), dtype=torch.bfloat16, device="cuda").normal_(
+        0, 0.02, generator=g)) for _ in range(2)] for _ in range(copies)]
+    for m in batches:
+        x = torch.empty((m, d), dtype=torch.bfloat16, device="cuda").normal_(generator=g)
+        u = torch.empty((m, F), dtype=torch.bfloat16, device="cuda")
+        ws = torch.empty(max(1, P.swiglu_projection_workspace_bytes(P.BF16, m, F, d)),
+                         dtype=torch.uint8, device="cuda")
+        us = timed(lambda i: P.swiglu_projection(x, pairs[i][0], pairs[i][1], u, ws), copies)
+        wbytes, flops = 4 * F * d, 4 * m * F * d
+        roof_us = max(wbytes / HBM_PEAK_GBS / 1e3, flops / 2.5e15 * 1e6)
+        rows.append({"shape": "gate_up_swiglu", "N": 2 * F, "K": d, "M": m, "us": round(us, 2),
+                     "weight_GBps": round(wbytes / us / 1e3, 1),
+                     "TFLOPs": round(flops / us / 1e6, 1),
+                     "roofline_us": round(roof_us, 2), "frac_of_roofline": round(roof_us / us, 3),
+                     "torch_matmul_us": None})
+    del pairs
+    torch.cuda.empty_cache()
+    log("projections gate_up_swiglu done")
     layer, layer_ref = {}, {}
+    # Per layer as the decode step runs it: qkv + o + fused gate/up + down.
     for r in rows:
-        if r["shape"] != "lm_head":
+        if r["shape"] in ("qkv", "o", "gate_up_swiglu", "down"):
             layer[r["M"]] = layer.get(r["M"], 0.0) + r["us"]
+        if r["shape"] in ("qkv", "o", "gate_up", "down"):
             layer_ref[r["M"]] = layer_ref.get(r["M"], 0.0) + r["torch_matmul_us"]
     return {"metric": "weight projection time per 8B layer, 1 MI355X", "value": layer.get(256),
             "unit": "us at batch 256", "n_gpus": 1, "higher_is_better": False,

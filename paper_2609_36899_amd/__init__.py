@@ -14,6 +14,7 @@ def __getattr__(name):
     if name in ("Engine", "paged_decode_attention", "paged_attention_workspace_bytes",
                 "kv_bytes_per_token", "weights_to_device", "model_cfg", "weight_projection",
                 "weight_projection_workspace_bytes", "pack_weight", "swiglu_projection",
+                "swiglu_projection_workspace_bytes",
                 "PackedWeight", "sample_top_p",
                 "paged_decode_attention_fp8"):
         from . import engine

@@ -274,6 +274,11 @@ class Engine:
                                 int(mode)))
 
 
+def swiglu_projection_workspace_bytes(dtype: int, rows: int, ffn: int, k: int) -> int:
+    """Scratch bytes swiglu_projection needs (0 when the SwiGLU is fused)."""
+    return N.check(N.load().swiglu_projection_workspace_bytes(dtype, rows, ffn, k))
+
+
 def swiglu_projection(x: torch.Tensor, w_gate: PackedWeight, w_up: PackedWeight,
                       u: torch.Tensor, workspace: Optional[torch.Tensor] = None,
                       stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
