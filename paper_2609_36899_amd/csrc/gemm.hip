@@ -4,19 +4,19 @@
 // Introduction; Design Principles, "Specialization in Heterogeneous Pools"),
 // so at decode batch sizes the weight stream from HBM is the bound.  bf16
 // weights are stored packed so that this stream is long contiguous runs:
+// columns form groups of 128 (8 strips of 16), a 16-column x 32-k block is
+// 1 KiB in the lane order of the v_mfma_f32_16x16x32_bf16 B operand (one
+// 16-byte load per lane at lane * 8 is exactly one fragment), and the eight
+// blocks of one k-block of a group are adjacent, so a group's weight tile for
+// a k-step of 64 is one contiguous 16 KiB run (layout at pack_weight_kernel).
+// Row-wise [N][K] weights give 128-byte runs in many rows at once and stream
+// 10-25% slower.
 //
-//   strip j = columns 16j .. 16j+15 (the last strip zero-padded), holding
-//   K/32 blocks of 16 columns x 32 k, each block 1 KiB in the lane order of
-//   the v_mfma_f32_16x16x32_bf16 B operand: element (n, k) of W sits at
-//       ((j * K/32 + b) * 64 + q * 16 + c) * 8 + e,
-//   n = 16j + c, k = 32b + 8q + e.
-//
-// One 16-byte load per lane at lane * 8 is then exactly one MFMA fragment,
-// and a strip's K range is a single contiguous run.  Row-wise [N][K] weights
-// give 128-byte runs in many rows at once and stream 10-25% slower.
-//
-// When the column tiles alone cannot fill 256 CUs the K axis is split and the
-// fp32 partial sums are reduced in a fixed order by the next kernel.
+// Kernels by batch rows: the streaming kernel (up to 32 rows, weights straight
+// into registers), the 128- and 256-row LDS tiles (up to 256 rows), and the
+// 256 x 256 tile above that.  When the column tiles alone cannot fill 256 CUs
+// the K axis is split and the fp32 partial sums are reduced in a fixed order
+// by the next kernel.
 #include "hip_common.h"
 #include "kernels.h"
 
@@ -600,7 +600,8 @@ __global__ __launch_bounds__(256) void gemm_f32_tiled(int M, int N, int K, int k
 // Kernel choice for bf16, from measurements on the 8B projection shapes:
 //  * M <= 32: the streaming kernel (two strips per wave, ring depth 2);
 //    6.0-6.6 TB/s of weights up to M = 16;
-//  * larger M: the 128 x 128 tile (M <= 128) or 256 x 128 tile.
+//  * larger M: the 128 x 128 tile (M <= 128) or 256 x 128 tile, and above
+//    256 rows the 256 x 256 tile where its grid fills the GPU.
 constexpr int kStreamMaxRows = 32;
 
 // Rows per tile: 128 (4 waves) up to 128-row batches, 256 (8 waves) beyond,
