@@ -694,6 +694,100 @@ def gpu_weights_f32_tiny(shape):
             "final_norm": ones(), "layers": layers}
 
 
+def run_attention_isolated(calls=50):
+    """The attention pass alone (paged_decode_attention) on the isolated
+    workload: B=64, 32/8 heads, Dh 128, contexts U[1024, 8192], block tables
+    from one random permutation of a 200k-page pool; K/V pages N(0,1) bf16.
+    Per call: host planning, one metadata upload, the split pass and the
+    merge, timed with HIP events over back-to-back calls."""
+    import torch
+
+    import paper_2609_36899_amd as P
+    from workload import lazy_paged_attention_case, lengths_uniform
+
+    B, HQ, HKV, DH, POOL = 64, 32, 8, 128, 200000
+    lens = lengths_uniform(B, 1024, 8192, seed=21)
+    case = lazy_paged_attention_case(B, HQ, HKV, DH, lens, POOL, seed=22)
+    torch.cuda.set_device(0)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    k = torch.empty((POOL, HKV, 16, DH), dtype=torch.bfloat16, device="cuda").normal_(generator=g)
+    v = torch.empty((POOL, HKV, DH, 16), dtype=torch.bfloat16, device="cuda").normal_(generator=g)
+    q = torch.empty((B, HQ, DH), dtype=torch.bfloat16, device="cuda").normal_(generator=g)
+    bt = torch.from_numpy(case.block_table).cuda()
+    out = torch.empty((B, HQ, DH), dtype=torch.float32, device="cuda")
+    ws = torch.empty(P.paged_attention_workspace_bytes(B, HQ, HKV, DH), dtype=torch.uint8,
+                     device="cuda")
+    P.paged_decode_attention(q, k, v, bt, lens, out, ws)  # checks the page ids once
+    for _ in range(3):
+        P.paged_decode_attention(q, k, v, bt, lens, out, ws, check_pages=False)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(calls):
+        P.paged_decode_attention(q, k, v, bt, lens, out, ws, check_pages=False)
+    ev1.record()
+    torch.cuda.synchronize()
+    us = ev0.elapsed_time(ev1) / calls * 1e3
+    kv_bytes = int(np.sum(lens)) * HKV * DH * 2 * 2
+    assert np.isfinite(out[:2].cpu().numpy()).all()
+    gbs = kv_bytes / (us * 1e-6) / 1e9
+    return {"metric": "isolated paged decode attention, 1 MI355X", "value": round(gbs, 1),
+            "unit": "GB/s (K+V bytes read once / call time)", "n_gpus": 1,
+            "higher_is_better": True, "data": "synthetic", "dtype": "bf16",
+            "config": {"workload": "attention-b64", "batch": B, "heads": [HQ, HKV], "head_dim": DH,
+                       "context": "U[1024, 8192]", "pool_pages": POOL,
+                       "context_mean": round(float(lens.mean()), 1)},
+            "us_per_call": round(us, 2), "kv_bytes": kv_bytes,
+            "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4), "calls": calls, "cpu_baseline": None}
+
+
+def run_tiny(steps=32, warmup=3):
+    """Decode-step latency of the tiny fp32 decoder (2 layers, d 256, 4/2
+    heads, Dh 64, FFN 688, vocab 1024) at B=4 after prefixes {17, 40, 96,
+    128}: a launch-bound shape, reported as time per step."""
+    import torch
+
+    import paper_2609_36899_amd as P
+    from workload import TINY, random_tokens
+
+    torch.cuda.set_device(0)
+    w = gpu_weights_f32_tiny(TINY)
+    prefixes = (17, 40, 96, 128)
+    per_tok = P.kv_bytes_per_token(TINY, P.F32)
+    E = P.Engine(TINY, w, P.F32, 4096 * per_tok, max_seqs=4, max_seq_len=512, max_batch=4,
+                 max_chunk=128)
+    ids = []
+    for i, n in enumerate(prefixes):
+        s_id = E.kv_alloc(0)
+        E.kv_append_prefix(s_id, random_tokens(n, TINY.vocab, seed=100 + i), chunk_tokens=128)
+        ids.append(s_id)
+    ids = np.array(ids, dtype=np.int32)
+    tok = torch.zeros(4, dtype=torch.int32, device="cuda")
+    logits = torch.empty((4, TINY.vocab), dtype=torch.float32, device="cuda")
+    for _ in range(warmup):
+        E.decode_step(ids, tok, logits)
+        E.sample(logits, tok)
+    torch.cuda.synchronize()
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    w0 = time.perf_counter()
+    marks[0].record()
+    for i in range(steps):
+        E.decode_step(ids, tok, logits)
+        E.sample(logits, tok)
+        marks[i + 1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    step_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(steps)])
+    return {"metric": "decode step latency, tiny fp32 decoder, 1 MI355X",
+            "value": round(float(np.median(step_ms)), 4), "unit": "ms per step (median)",
+            "n_gpus": 1, "higher_is_better": False, "data": "synthetic", "dtype": "f32",
+            "config": {"workload": "tiny-fp32", "batch": 4, "prefixes": list(prefixes)},
+            "steps": steps, "step_ms_p95": round(float(np.percentile(step_ms, 95)), 4),
+            "wall_ms_per_step": round(wall / steps * 1e3, 4),
+            "tokens_per_s": round(4 / (float(np.mean(step_ms)) / 1e3), 1), "cpu_baseline": None}
+
+
 def run_copy_calibration(n=1 << 30):
     """One device copy of n bytes (torch copy_): the reference kernel whose
     FETCH_SIZE / WRITE_SIZE counters calibrate the HBM traffic figures."""
@@ -939,7 +1033,7 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
                     choices=sorted(WORKLOADS) + sorted(FP8_KV) + sorted(MULTITURN)
                     + ["kv-transfer-8b", "projections-8b", "landscape-8b", "sampling-8b",
-                       "copy-1gib", "paced-rollout-8b"])
+                       "copy-1gib", "paced-rollout-8b", "attention-b64", "tiny-fp32"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -957,6 +1051,10 @@ def main():
         out = run_sampling()
     elif args.workload == "copy-1gib":
         out = run_copy_calibration()
+    elif args.workload == "attention-b64":
+        out = run_attention_isolated()
+    elif args.workload == "tiny-fp32":
+        out = run_tiny()
     elif args.workload == "paced-rollout-8b":
         out = run_paced_rollout()
     elif args.workload in MULTITURN:
