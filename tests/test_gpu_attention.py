@@ -158,3 +158,66 @@ def test_bf16_full_config2_sampled():
         for h in range(HQ):
             err = np.max(np.abs(got[b, h] - ref[h]))
             assert err <= BF16_TOL * np.max(np.abs(ref[h])), (b, h, err)
+
+
+def _full_size_sampled(lens, sampled, seed):
+    """The attention pass at a decode workload's full size, in the launch
+    configuration of the decode step (the same planner and kernels): every
+    sequence's pages are filled on the GPU (torch's seeded generator), then
+    the pages and query of the sampled sequences are overwritten with the
+    seeded host draws of the lazy case, and those sequences' outputs are
+    checked against the oracle row by row.  Attention is per sequence, so
+    the filler around them shapes only the work split, not their result."""
+    from workload import EIGHT_B
+    B, HQ, HKV, DH = len(lens), EIGHT_B.n_q_heads, EIGHT_B.n_kv_heads, EIGHT_B.head_dim
+    pages = int(np.sum((np.asarray(lens) + PAGE_TOKENS - 1) // PAGE_TOKENS))
+    pool = pages + 64
+    case = lazy_paged_attention_case(B, HQ, HKV, DH, lens, pool, seed=seed)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    k = torch.empty((pool, HKV, PAGE_TOKENS, DH), dtype=torch.bfloat16, device="cuda")
+    v = torch.empty((pool, HKV, DH, PAGE_TOKENS), dtype=torch.bfloat16, device="cuda")
+    k.normal_(generator=g)
+    v.normal_(generator=g)
+    q = torch.empty((B, HQ, DH), dtype=torch.bfloat16, device="cuda").normal_(generator=g)
+    for b in sampled:
+        qb, kb, vb = case.sequence(b)
+        idx = torch.from_numpy(case.block_table[b, :kb.shape[0]].astype(np.int64)).cuda()
+        k[idx] = torch.from_numpy(kb).cuda().to(torch.bfloat16)
+        v[idx] = torch.from_numpy(np.ascontiguousarray(vb.transpose(0, 1, 3, 2))).cuda().to(
+            torch.bfloat16)
+        q[b] = torch.from_numpy(qb).cuda().to(torch.bfloat16)
+    bt = torch.from_numpy(case.block_table).cuda()
+    out = torch.empty((B, HQ, DH), dtype=torch.float32, device="cuda")
+    _pdec().paged_decode_attention(q, k, v, bt, lens, out)
+    got = out.cpu().numpy()
+    for b in sampled:
+        qb, kb, vb = case.sequence(b)
+        n = int(lens[b])
+        keys = kb.transpose(0, 2, 1, 3).reshape(-1, HKV, DH)[:n].astype(np.float64)
+        vals = vb.transpose(0, 2, 1, 3).reshape(-1, HKV, DH)[:n].astype(np.float64)
+        ref = oracle.attention(qb.astype(np.float64), keys, vals)
+        assert np.isfinite(got[b]).all()
+        for h in range(HQ):
+            err = np.max(np.abs(got[b, h] - ref[h]))
+            assert err <= BF16_TOL * np.max(np.abs(ref[h])), (b, h, err)
+
+
+def test_bf16_full_size_b256_lognormal_sampled():
+    """B=256, contexts lognormal (median 4096, sigma 0.8, clipped to
+    [256, 32768]), the default decode workload's draw: 1.27 M keys, 5.2 GB of
+    K and V pages.  Sampled: the shortest, the longest and six others."""
+    from workload import lengths_lognormal
+    lens = lengths_lognormal(256, 4096, 0.8, 256, 32768, 1)
+    order = np.argsort(lens)
+    sampled = sorted({int(order[0]), int(order[-1]), 3, 64, 100, 128, 200, 255})
+    _full_size_sampled(lens, sampled, seed=31)
+
+
+def test_bf16_full_size_b8_long_sampled():
+    """B=8, contexts U[65536, 131072], the long-context decode workload's
+    draw: ~0.8 M keys, 3.2 GB of pages, each sequence cut into dozens of
+    items.  Sampled: three sequences, including the longest."""
+    lens = lengths_uniform(8, 65536, 131072, 1)
+    sampled = sorted({int(np.argmax(lens)), 0, 5})
+    _full_size_sampled(lens, sampled, seed=32)
