@@ -630,6 +630,21 @@ int gemm_plan_splits(int dtype, int M, int N, int K, int* k_split) {
     // second round costs 15-30%).
     s = (int)std::max<int64_t>(1, 256 / groups);
     s = std::min(s, 8);
+    // Above 256 rows (prefill chunks, large batches) with a long K (the down
+    // projection), a grid of 129-255 work groups fills one round poorly; up
+    // to 4 splits are weighed by rounds per unit of work,
+    // ceil(groups * s / 256) / s, ties to fewer splits.  Measured at 640-1536
+    // rows this picked the best count every time (1242 rows: 160 groups,
+    // 3 splits, 142 against 189 us).  With K = 4096 the shorter split loops
+    // and the partials cost more than the rounds save, so those keep the
+    // rule above.
+    if (M > 256 && groups < 256 && K >= 8192) {
+      double best = 1e30;
+      for (int c = 1; c <= 4; ++c) {
+        const double cost = (double)((groups * c + 255) / 256) / c;
+        if (cost < best - 1e-9) best = cost, s = c;
+      }
+    }
   } else {
     const int64_t groups = (int64_t)((N + 63) / 64) * ((M + 31) / 32);
     if (groups < 512) s = (int)std::min<int64_t>((512 + groups - 1) / groups, 8);
