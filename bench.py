@@ -394,6 +394,10 @@ def run_decode(workload, steps, warmup, with_cpu):
     logit_bytes = 2 * batch * shape.vocab * 4  # LM-head write + argmax read
     step_bytes = kv_read + kv_write + w_bytes + logit_bytes
     hbm = step_bytes / (ms_step / 1e3) / 1e9
+    # Per-trajectory effective bandwidth (the paper's bandwidth share): each
+    # trajectory's own KV bytes plus its 1/B share of the weights, per step.
+    traj_keys = lens + warmup + (steps + 1) / 2.0
+    share = (traj_keys * per_tok + w_bytes / batch) / (ms_step / 1e3) / 1e9
     kv_elem = 1 if kv_fp8 is not None else 2
     attn_bytes = mean_keys * shape.n_kv_heads * shape.head_dim * 2 * kv_elem  # per layer launch
     attn_avg_ms = attn_ms / max(attn_n, 1)
@@ -413,6 +417,10 @@ def run_decode(workload, steps, warmup, with_cpu):
                    "kv_pages": "fp8 e4m3, scales 1" if kv_fp8 is not None else "bf16"},
         "hbm_gbps": round(hbm, 1), "hbm_frac_of_peak": round(hbm / HBM_PEAK_GBS, 4),
         "step_bytes": int(step_bytes), "wall_s": round(wall, 3),
+        "per_trajectory_gbps": {"mean": round(float(share.mean()), 2),
+                                "min": round(float(share.min()), 2),
+                                "max": round(float(share.max()), 2),
+                                "definition": "(own KV bytes + weights / B) per step time"},
         "step_ms": {"median": round(float(np.median(step_ms)), 4),
                     "p95": round(float(np.percentile(step_ms, 95)), 4),
                     "min": round(float(step_ms.min()), 4),
