@@ -409,7 +409,7 @@ def run_decode(workload, steps, warmup, with_cpu):
         "steps": steps, "warmup": warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": workload, "model": "8B-shaped decoder (32x4096, 32/8 heads, "
+        "config": {"workload": workload, "decoder_shape": "8B-shaped decoder (32x4096, 32/8 heads, "
                    "Dh 128, FFN 14336, vocab 128256), random init",
                    "batch": int(batch), "context_mean": round(float(lens.mean()), 1),
                    "context_min": int(lens.min()), "context_max": int(lens.max()),
