@@ -233,13 +233,15 @@ def test_bf16_long_prefill_items(n_kv_heads):
                  pool_tokens=6144, max_seq_len=4096)
 
 
-def test_bf16_wide_ffn_fused_swiglu_parity():
-    """An FFN wide enough (F = 8256, a half-filled last column group) that
-    the gate/up projection runs unsplit with SwiGLU in its epilogue: prefill
-    chunks of 300 rows (256-row tiles, two M-blocks) and 77 rows (128-row
-    tile), then decode steps (the streaming kernel)."""
+@pytest.mark.parametrize("ffn", [8256, 14336])
+def test_bf16_wide_ffn_fused_swiglu_parity(ffn):
+    """An FFN wide enough that the gate/up projection runs unsplit with
+    SwiGLU in its epilogue: prefill chunks of 300 rows and 77 rows (128-row
+    tile), then decode steps (the streaming kernel).  At F = 8256 (a
+    half-filled last column group) the 300-row chunk takes 256-row tiles in
+    two M-blocks; at the 8B width F = 14336 it takes the 256 x 256 tile."""
     shape = ModelShape(n_layers=1, d_model=256, n_q_heads=4, n_kv_heads=2, head_dim=64,
-                       ffn_dim=8256, vocab=512)
+                       ffn_dim=ffn, vocab=512)
     _bf16_parity(shape, seed=13, prefix_lens=[377, 77], n_steps=3, chunk=300,
                  pool_tokens=2048, max_seq_len=1024)
 
