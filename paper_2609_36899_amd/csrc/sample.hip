@@ -32,6 +32,7 @@ namespace {
 
 constexpr int kThreads = 1024, kWaves = kThreads / 64;
 constexpr int kUnroll = 8;  // loads in flight per lane: index slabs of 64
+constexpr int kUnroll4 = 4;  // 16-byte loads in flight per lane (vectorised passes)
 constexpr int kRounds = 4, kMaxBins = 2048;
 // Radix digits of the 41-bit keys, most significant first: bits 40..30,
 // 29..19, 18..8, 7..0.
@@ -91,14 +92,43 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(
     }
   };
 
+  // The passes whose results are sums (max, histograms, tie counts) may see
+  // a wave's tokens in any order: with V % 4 == 0 (rows 16-byte aligned) they
+  // read 16 bytes per lane, four times the bytes in flight of the scalar
+  // blocks, which is what bounds one work group's pass over a long row.  Only
+  // the final walk needs index order and keeps the scalar blocks.
+  const bool vec4 = (V & 3) == 0;
+  auto for_each = [&](auto&& f) {
+    if (vec4) {
+      for (int base = w0; base < w1; base += 256 * kUnroll4) {
+        float4 zv[kUnroll4];
+#pragma unroll
+        for (int u = 0; u < kUnroll4; ++u) {
+          const int i = base + (u * 64 + lane) * 4;  // i < w1 implies i + 3 < w1
+          zv[u] = i < w1 ? *(const float4*)(z + i)
+                         : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll4; ++u) {
+          f(zv[u].x);
+          f(zv[u].y);
+          f(zv[u].z);
+          f(zv[u].w);
+        }
+      }
+    } else {
+      for (int base = w0; base < w1; base += 64 * kUnroll) {
+        float zv[kUnroll];
+        load_block(base, zv);
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) f(zv[u]);
+      }
+    }
+  };
+
   // Row max.
   float mx = -INFINITY;
-  for (int base = w0; base < w1; base += 64 * kUnroll) {
-    float zv[kUnroll];
-    load_block(base, zv);
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) mx = fmaxf(mx, zv[u]);
-  }
+  for_each([&](float v) { mx = fmaxf(mx, v); });
   mx = wave_max(mx);
   if (lane == 0) red_f[wave] = mx;
   __syncthreads();
@@ -125,25 +155,20 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(
     // keys of this round's range: [prefix << top, (prefix + 1) << top)
     const int top = shift + kWidth[r];
     const double xlo = x_floor(prefix << top), xhi = x_floor((prefix + 1) << top);
-    for (int base = w0; base < w1; base += 64 * kUnroll) {
-      float zv[kUnroll];
-      load_block(base, zv);
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const double x = ((double)zv[u] - m) * inv_t;
-        if (x < xlo || (r > 0 && x > xhi + 2e-9)) continue;
-        const uint64_t q = mass_of(zv[u], m, inv_t);
-        if (q != 0 && (q >> top) == prefix) {
-          const int d = (int)((q >> shift) & (uint64_t)(bins - 1));
-          if (d != run_bin) {
-            if (run_bin >= 0) atomicAdd((unsigned long long*)&hist[run_bin], run_sum);
-            run_bin = d;
-            run_sum = 0;
-          }
-          run_sum += q;
+    for_each([&](float zz) {
+      const double x = ((double)zz - m) * inv_t;
+      if (x < xlo || (r > 0 && x > xhi + 2e-9)) return;
+      const uint64_t q = mass_of(zz, m, inv_t);
+      if (q != 0 && (q >> top) == prefix) {
+        const int d = (int)((q >> shift) & (uint64_t)(bins - 1));
+        if (d != run_bin) {
+          if (run_bin >= 0) atomicAdd((unsigned long long*)&hist[run_bin], run_sum);
+          run_bin = d;
+          run_sum = 0;
         }
+        run_sum += q;
       }
-    }
+    });
     if (run_bin >= 0) atomicAdd((unsigned long long*)&hist[run_bin], run_sum);
     __syncthreads();
     if (r == 0) {  // S = total mass, T_p from it
@@ -200,17 +225,12 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(
   // can reach kappa).
   const double xk = x_floor(kappa);
   uint64_t ties = 0, strict = 0;
-  for (int base = w0; base < w1; base += 64 * kUnroll) {
-    float zv[kUnroll];
-    load_block(base, zv);
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      if (((double)zv[u] - m) * inv_t < xk) continue;
-      const uint64_t q = mass_of(zv[u], m, inv_t);
-      ties += q == kappa;
-      strict += q > kappa ? q : 0;
-    }
-  }
+  for_each([&](float zz) {
+    if (((double)zz - m) * inv_t < xk) return;
+    const uint64_t q = mass_of(zz, m, inv_t);
+    ties += q == kappa;
+    strict += q > kappa ? q : 0;
+  });
   ties = wave_sum_u64(ties);
   strict = wave_sum_u64(strict);
   if (lane == 0) {
