@@ -632,9 +632,11 @@ def run_landscape(steps=8, warmup=2):
             "cells": cells, "cpu_baseline": None}
 
 
-def run_sampling(batches=(1, 16, 256, 512), vocab=128256, iters=20):
+def run_sampling(batches=(1, 4, 16, 32, 64, 256, 512), vocab=128256, iters=20):
     """Greedy argmax and temperature/top-p sampling over 8B-sized logit rows:
-    time per call (HIP events) at each batch size."""
+    time per call (HIP events) at each batch size; top-p both in the form the
+    library picks for the batch (split over several groups per row for small
+    batches) and with one work group per row."""
     import torch
 
     import paper_2609_36899_amd as P
@@ -656,8 +658,13 @@ def run_sampling(batches=(1, 16, 256, 512), vocab=128256, iters=20):
         u = torch.rand(b, device="cuda", generator=g)
         out = torch.empty(b, dtype=torch.int32, device="cuda")
         res = {"batch": b}
+        need = P.sample_top_p_workspace_bytes(b)
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device="cuda")
         for name, fn in (("greedy_us", lambda: E.sample(logits, out, batch=b)),
-                         ("top_p_us", lambda: P.sample_top_p(logits, out, 0.8, 0.95, u))):
+                         ("top_p_us", lambda: P.sample_top_p(logits, out, 0.8, 0.95, u,
+                                                             workspace=ws)),
+                         ("top_p_one_group_us", lambda: P.sample_top_p(logits, out, 0.8, 0.95,
+                                                                       u, split=False))):
             for _ in range(3):
                 fn()
             torch.cuda.synchronize()

@@ -324,13 +324,21 @@ int pacing_plan(int64_t headroom_tokens, int64_t h_min_tokens, int64_t delta_tok
  *   token = first nucleus token in index order whose running mass > target.
  * A given (logits, T, top_p, u) always yields the same token.
  *   logits_dev: device fp32 [batch][vocab]; uniforms_dev: device fp32
- *   [batch]; tokens_dev_out: device int32 [batch].  No scratch memory.
+ *   [batch]; tokens_dev_out: device int32 [batch].
+ *   workspace: device scratch of at least sample_top_p_workspace_bytes(batch)
+ *   bytes, owned by the caller, contents ignored on entry; or null (0 bytes),
+ *   in which case one work group handles each row.  With it, rows of small
+ *   batches are split over several work groups per pass; the tokens are the
+ *   same either way.  Calls that share a workspace must not overlap.
  *   Asynchronous on stream.
  * Errors: PDEC_INVALID_ARG (temperature <= 0 or not finite, top_p outside
- * (0, 1], batch or vocab < 1, null pointer).
+ * (0, 1], batch or vocab < 1, null pointer, a non-null workspace smaller than
+ * required).
  * ------------------------------------------------------------------------- */
+int64_t sample_top_p_workspace_bytes(int32_t batch);
 int sample_top_p(int32_t batch, int32_t vocab, const float* logits_dev, float temperature,
-                 float top_p, const float* uniforms_dev, int32_t* tokens_dev_out, void* stream);
+                 float top_p, const float* uniforms_dev, int32_t* tokens_dev_out,
+                 void* workspace, int64_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Weight packing.  Each decode step streams every projection matrix from HBM

@@ -15,7 +15,7 @@ def __getattr__(name):
                 "kv_bytes_per_token", "weights_to_device", "model_cfg", "weight_projection",
                 "weight_projection_workspace_bytes", "pack_weight", "swiglu_projection",
                 "swiglu_projection_workspace_bytes",
-                "PackedWeight", "sample_top_p",
+                "PackedWeight", "sample_top_p", "sample_top_p_workspace_bytes",
                 "paged_decode_attention_fp8"):
         from . import engine
         return getattr(engine, name)

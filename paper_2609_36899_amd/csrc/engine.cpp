@@ -879,16 +879,27 @@ int pacing_plan(int64_t headroom_tokens, int64_t h_min_tokens, int64_t delta_tok
   return PDEC_OK;
 }
 
+int64_t sample_top_p_workspace_bytes(int32_t batch) {
+  if (batch < 1) return fail(PDEC_INVALID_ARG, "batch must be positive");
+  return sample_workspace_bytes(batch);
+}
+
 int sample_top_p(int32_t batch, int32_t vocab, const float* logits_dev, float temperature,
-                 float top_p, const float* uniforms_dev, int32_t* tokens_dev_out, void* stream) {
+                 float top_p, const float* uniforms_dev, int32_t* tokens_dev_out,
+                 void* workspace, int64_t workspace_bytes, void* stream) {
   if (batch < 1 || vocab < 1) return fail(PDEC_INVALID_ARG, "batch and vocab must be positive");
   if (!logits_dev || !uniforms_dev || !tokens_dev_out)
     return fail(PDEC_INVALID_ARG, "null argument");
   if (!(temperature > 0.f) || !std::isfinite(temperature))
     return fail(PDEC_INVALID_ARG, "temperature must be positive and finite");
   if (!(top_p > 0.f && top_p <= 1.f)) return fail(PDEC_INVALID_ARG, "top_p must be in (0, 1]");
+  if (workspace_bytes < 0 || (workspace && workspace_bytes == 0))
+    return fail(PDEC_INVALID_ARG, "bad workspace size");
+  if (workspace && workspace_bytes < sample_workspace_bytes(batch))
+    return fail(PDEC_INVALID_ARG, "workspace smaller than sample_top_p_workspace_bytes");
   HIP_OR_FAIL(launch_sample_top_p(batch, vocab, logits_dev, temperature, top_p, uniforms_dev,
-                                  tokens_dev_out, (hipStream_t)stream));
+                                  tokens_dev_out, workspace, workspace_bytes,
+                                  (hipStream_t)stream));
   return PDEC_OK;
 }
 

@@ -83,8 +83,12 @@ hipError_t launch_gemm_swiglu(int M, int F, int K, const void* A, int64_t lda, c
                               const void* w_up, void* u, hipStream_t stream,
                               hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 // Temperature / top-p sampling (sample.hip).
+// With a workspace of sample_workspace_bytes(B) (> 0 only for small batches)
+// every pass is split over several work groups per row; same tokens.
+int64_t sample_workspace_bytes(int B);
 hipError_t launch_sample_top_p(int B, int V, const float* logits, float temperature, float top_p,
-                               const float* uniforms, int32_t* tokens, hipStream_t stream);
+                               const float* uniforms, int32_t* tokens, void* workspace,
+                               int64_t ws_bytes, hipStream_t stream);
 // bf16: pack a row-major [N][K] weight into the group-major layout the GEMM
 // kernels read (((N + 127) / 128) * 128 * K elements); fp32: plain copy.
 hipError_t launch_pack_weight(int dtype, int N, int K, const void* w, void* packed,

@@ -26,6 +26,8 @@
 #include "hip_common.h"
 #include "kernels.h"
 
+#include <climits>
+
 namespace pdec {
 
 namespace {
@@ -288,15 +290,360 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Split form for batches below the CU count.  One work group per row leaves
+// most CUs idle and each pass over a 513 KB row runs at one CU's bandwidth;
+// here every pass is spread over C work groups per row, each owning a
+// contiguous chunk of the row, and the per-row decisions run in small
+// one-group kernels between them:
+//   chunk_max -> (chunk_hist(r) -> select(r)) x 4 -> chunk_ties -> walk.
+// All cross-chunk results are integer sums (or a max), so the token is the
+// one-group form's.  Workspace per row: the row state, C chunk maxima, C
+// partial histograms of 2048 bins and C (ties, strict mass) pairs.
+// ---------------------------------------------------------------------------
+constexpr int kST = 256, kSW = kST / 64;  // threads / waves of the split kernels
+
+struct RowState {
+  uint64_t prefix, above, t_p;
+  float m;
+  int32_t pad;
+};
+
+struct SplitWs {
+  RowState* st;       // [B]
+  float* cmax;        // [B][C]
+  uint64_t* hist;     // [B][C][kMaxBins]
+  uint64_t* ties;     // [B][C][2]: tie count, strict-member mass
+};
+
+// Chunk c of a row: [i0, i1), the chunk length a multiple of 4 so that with
+// V % 4 == 0 every chunk start is 16-byte aligned.
+__device__ __forceinline__ void chunk_range(int V, int C, int c, int& i0, int& i1) {
+  const int span = (((V + C - 1) / C) + 3) & ~3;
+  i0 = min(V, c * span);
+  i1 = min(V, i0 + span);
+}
+
+// Calls f(z) for every token of [i0, i1) in some order, 16-byte loads when
+// the row length allows.
+template <typename F>
+__device__ __forceinline__ void chunk_for_each(const float* z, int V, int i0, int i1, F&& f) {
+  const int t = threadIdx.x;
+  if ((V & 3) == 0) {
+    for (int base = i0 + 4 * t; base < i1; base += 4 * kST * kUnroll4) {
+      float4 zv[kUnroll4];
+#pragma unroll
+      for (int u = 0; u < kUnroll4; ++u) {
+        const int i = base + 4 * kST * u;  // i < i1 implies i + 3 < i1
+        zv[u] = i < i1 ? *(const float4*)(z + i)
+                       : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll4; ++u) {
+        f(zv[u].x);
+        f(zv[u].y);
+        f(zv[u].z);
+        f(zv[u].w);
+      }
+    }
+  } else {
+    for (int i = i0 + t; i < i1; i += kST) f(z[i]);
+  }
+}
+
+__device__ __forceinline__ uint64_t block_sum_u64(uint64_t v, uint64_t* red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  v = wave_sum_u64(v);
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  uint64_t total = 0;
+  for (int w = 0; w < kSW; ++w) total += red[w];
+  return total;
+}
+
+__global__ __launch_bounds__(kST) void split_chunk_max(int V, int C, const float* __restrict__ logits,
+                                                       SplitWs ws) {
+  __shared__ float red[kSW];
+  const int c = blockIdx.x, b = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int i0, i1;
+  chunk_range(V, C, c, i0, i1);
+  float mx = -INFINITY;
+  chunk_for_each(logits + (int64_t)b * V, V, i0, i1, [&](float v) { mx = fmaxf(mx, v); });
+  mx = wave_max(mx);
+  if (lane == 0) red[wave] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float bm = red[0];
+    for (int w = 1; w < kSW; ++w) bm = fmaxf(bm, red[w]);
+    ws.cmax[(int64_t)b * C + c] = bm;
+  }
+}
+
+// Row max from the chunk maxima (the same float max as one pass).
+__device__ __forceinline__ double row_max(const SplitWs& ws, int b, int C) {
+  float m = -INFINITY;
+  for (int c = 0; c < C; ++c) m = fmaxf(m, ws.cmax[(int64_t)b * C + c]);
+  return (double)m;
+}
+
+// Round r's histogram of one chunk: the tokens whose key lies in the
+// current prefix range, by their round-r digit, as in the one-group form.
+__global__ __launch_bounds__(kST) void split_chunk_hist(int V, int C, int r,
+                                                        const float* __restrict__ logits,
+                                                        double inv_t, SplitWs ws) {
+  __shared__ uint64_t hist[kMaxBins];
+  const int c = blockIdx.x, b = blockIdx.y;
+  const int shift = kShift[r], bins = 1 << kWidth[r], top = shift + kWidth[r];
+  const double m = row_max(ws, b, C);
+  const uint64_t prefix = r ? ws.st[b].prefix : 0;
+  for (int bin = threadIdx.x; bin < bins; bin += kST) hist[bin] = 0;
+  __syncthreads();
+  const double xlo = x_floor(prefix << top), xhi = x_floor((prefix + 1) << top);
+  int i0, i1;
+  chunk_range(V, C, c, i0, i1);
+  int run_bin = -1;
+  uint64_t run_sum = 0;
+  chunk_for_each(logits + (int64_t)b * V, V, i0, i1, [&](float zz) {
+    const double x = ((double)zz - m) * inv_t;
+    if (x < xlo || (r > 0 && x > xhi + 2e-9)) return;
+    const uint64_t q = mass_of(zz, m, inv_t);
+    if (q != 0 && (q >> top) == prefix) {
+      const int d = (int)((q >> shift) & (uint64_t)(bins - 1));
+      if (d != run_bin) {
+        if (run_bin >= 0) atomicAdd((unsigned long long*)&hist[run_bin], run_sum);
+        run_bin = d;
+        run_sum = 0;
+      }
+      run_sum += q;
+    }
+  });
+  if (run_bin >= 0) atomicAdd((unsigned long long*)&hist[run_bin], run_sum);
+  __syncthreads();
+  uint64_t* dst = ws.hist + ((int64_t)b * C + c) * kMaxBins;
+  for (int bin = threadIdx.x; bin < bins; bin += kST) dst[bin] = hist[bin];
+}
+
+// Round r's decision for one row: sum the chunk histograms, then pick the
+// digit exactly as the one-group form (walking bins from the top, the first
+// whose cumulative mass from `above` reaches T_p).
+__global__ __launch_bounds__(kThreads) void split_select(int C, int r, uint32_t p24,
+                                                         SplitWs ws) {
+  __shared__ uint64_t hist[kMaxBins];
+  __shared__ uint64_t wave_a[kWaves], wave_b[kWaves];
+  __shared__ uint64_t sel[2];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, b = blockIdx.x;
+  const int bins = 1 << kWidth[r];
+  const uint64_t* h0 = ws.hist + (int64_t)b * C * kMaxBins;
+  for (int bin = t; bin < bins; bin += kThreads) {
+    uint64_t v = 0;
+    for (int c = 0; c < C; ++c) v += h0[(int64_t)c * kMaxBins + bin];
+    hist[bin] = v;
+  }
+  __syncthreads();
+  RowState st = ws.st[b];
+  if (r == 0) {
+    st.prefix = 0;
+    st.above = 0;
+    uint64_t part = 0;
+    for (int bin = t; bin < bins; bin += kThreads) part += hist[bin];
+    part = wave_sum_u64(part);
+    if (lane == 0) wave_a[wave] = part;
+    __syncthreads();
+    uint64_t total = 0;
+    for (int w = 0; w < kWaves; ++w) total += wave_a[w];
+    st.t_p = (uint64_t)(((u128)p24 * total + ((u128)1 << 24) - 1) >> 24);
+  }
+  const int per = (bins + kThreads - 1) / kThreads;
+  uint64_t mine = 0;
+  for (int j = 0; j < per; ++j) {
+    const int rank = t * per + j;
+    if (rank < bins) mine += hist[bins - 1 - rank];
+  }
+  const uint64_t incl_w = wave_scan_incl(mine, lane);
+  if (lane == 63) wave_b[wave] = incl_w;
+  __syncthreads();
+  uint64_t before = st.above + incl_w - mine;
+  for (int w = 0; w < wave; ++w) before += wave_b[w];
+  for (int j = 0; j < per; ++j) {
+    const int rank = t * per + j;
+    if (rank >= bins) break;
+    const uint64_t h = hist[bins - 1 - rank];
+    if (before < st.t_p && (before + h >= st.t_p || rank == bins - 1)) {
+      sel[0] = (uint64_t)(bins - 1 - rank);
+      sel[1] = before;
+    }
+    before += h;
+  }
+  __syncthreads();
+  if (t == 0) {
+    st.prefix = (st.prefix << kWidth[r]) | sel[0];
+    st.above = sel[1];
+    ws.st[b] = st;
+  }
+}
+
+// Per chunk: the number of keys equal to kappa and the mass of keys above it.
+__global__ __launch_bounds__(kST) void split_chunk_ties(int V, int C,
+                                                        const float* __restrict__ logits,
+                                                        double inv_t, SplitWs ws) {
+  __shared__ uint64_t red[kSW];
+  const int c = blockIdx.x, b = blockIdx.y;
+  const double m = row_max(ws, b, C);
+  const uint64_t kappa = ws.st[b].prefix;
+  const double xk = x_floor(kappa);
+  int i0, i1;
+  chunk_range(V, C, c, i0, i1);
+  uint64_t ties = 0, strict = 0;
+  chunk_for_each(logits + (int64_t)b * V, V, i0, i1, [&](float zz) {
+    if (((double)zz - m) * inv_t < xk) return;
+    const uint64_t q = mass_of(zz, m, inv_t);
+    ties += q == kappa;
+    strict += q > kappa ? q : 0;
+  });
+  ties = block_sum_u64(ties, red);
+  strict = block_sum_u64(strict, red);
+  if (threadIdx.x == 0) {
+    ws.ties[((int64_t)b * C + c) * 2] = ties;
+    ws.ties[((int64_t)b * C + c) * 2 + 1] = strict;
+  }
+}
+
+// The row's token: the chunk whose nucleus mass range holds the target is
+// walked in index order, 256 tokens at a time, with a work-group scan.
+__global__ __launch_bounds__(kST) void split_walk(int V, int C, const float* __restrict__ logits,
+                                                  double inv_t,
+                                                  const float* __restrict__ uniforms,
+                                                  int32_t* __restrict__ tokens, SplitWs ws) {
+  __shared__ uint64_t wsum[kSW], wtie[kSW];
+  __shared__ int found_at;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, b = blockIdx.x;
+  const RowState st = ws.st[b];
+  const uint64_t kappa = st.prefix;
+  const uint64_t n_tie = (st.t_p - st.above + kappa - 1) / kappa;
+  const uint64_t* tc = ws.ties + (int64_t)b * C * 2;
+  // Nucleus mass of every chunk (its strict members plus its member ties,
+  // ties ranked in index order across chunks).
+  uint64_t Z = 0, tb = 0;
+  for (int c = 0; c < C; ++c) {
+    const uint64_t nt = tc[2 * c];
+    const uint64_t mt = n_tie > tb ? min(nt, n_tie - tb) : 0;
+    Z += tc[2 * c + 1] + mt * kappa;
+    tb += nt;
+  }
+  float u = uniforms[b];
+  u = fminf(fmaxf(u, 0.f), 0x1.fffffep-1f);
+  const uint64_t u24 = (uint64_t)(u * 0x1p24f);
+  const uint64_t target = (uint64_t)(((u128)u24 * Z) >> 24);
+  uint64_t mass_base = 0, tie_base = 0;
+  int cs = -1;
+  tb = 0;
+  for (int c = 0; c < C; ++c) {
+    const uint64_t nt = tc[2 * c];
+    const uint64_t mt = n_tie > tb ? min(nt, n_tie - tb) : 0;
+    const uint64_t own = tc[2 * c + 1] + mt * kappa;
+    if (own > 0 && mass_base <= target && target < mass_base + own) {
+      cs = c;
+      tie_base = tb;
+      break;
+    }
+    mass_base += own;
+    tb += nt;
+  }
+  if (cs < 0) return;  // cannot happen: Z > 0 (the max token has mass 2^40)
+  const double m = row_max(ws, b, C);
+  const double xk = x_floor(kappa);
+  const float* z = logits + (int64_t)b * V;
+  int i0, i1;
+  chunk_range(V, C, cs, i0, i1);
+  if (t == 0) found_at = INT_MAX;
+  uint64_t run = mass_base, rank = tie_base;
+  for (int base = i0; base < i1; base += kST) {
+    const int i = base + t;
+    uint64_t q = 0;
+    if (i < i1) {
+      const float zz = z[i];
+      if (((double)zz - m) * inv_t >= xk) q = mass_of(zz, m, inv_t);
+    }
+    const bool tie = q == kappa;  // out-of-range slots have q = 0 < kappa
+    // Tie ranks and member masses in index order: wave scans, then the
+    // waves before this one.
+    const uint64_t tie_mask = __ballot(tie);
+    const uint64_t tie_before_w = __popcll(tie_mask & ((1ull << lane) - 1));
+    if (lane == 0) wtie[wave] = __popcll(tie_mask);
+    __syncthreads();
+    uint64_t tie_before = rank + tie_before_w;
+    for (int w = 0; w < wave; ++w) tie_before += wtie[w];
+    const uint64_t mass = (q > kappa || (tie && tie_before < n_tie)) ? q : 0;
+    const uint64_t incl_w = wave_scan_incl(mass, lane);
+    if (lane == 63) wsum[wave] = incl_w;
+    __syncthreads();
+    uint64_t incl = run + incl_w;
+    for (int w = 0; w < wave; ++w) incl += wsum[w];
+    // The first token (lowest index) whose running mass passes the target.
+    const uint64_t hit = __ballot(mass > 0 && incl > target);
+    if (hit && lane == __ffsll((unsigned long long)hit) - 1) atomicMin(&found_at, i);
+    __syncthreads();
+    if (found_at != INT_MAX) {
+      if (t == 0) tokens[b] = found_at;
+      return;  // uniform: found_at is shared
+    }
+    for (int w = 0; w < kSW; ++w) {
+      run += wsum[w];
+      rank += wtie[w];
+    }
+    __syncthreads();
+  }
+}
+
 }  // namespace
 
+int sample_split_chunks(int B) {
+  // About 256 work groups per pass: 16 chunks per row up to 16 rows, 8 up
+  // to 32, none above (at 64 rows the split form's eleven launches already
+  // cost more than its wider passes save).
+  const int c = B > 0 ? 256 / B : 1;
+  return c >= 16 ? 16 : c >= 8 ? 8 : 1;
+}
+
+int64_t sample_workspace_bytes(int B) {
+  const int C = sample_split_chunks(B);
+  if (C == 1) return 0;
+  return (int64_t)B * (sizeof(RowState) + C * 4 + C * kMaxBins * 8 + C * 16) + 1024;
+}
+
 hipError_t launch_sample_top_p(int B, int V, const float* logits, float temperature, float top_p,
-                               const float* uniforms, int32_t* tokens, hipStream_t stream) {
+                               const float* uniforms, int32_t* tokens, void* workspace,
+                               int64_t ws_bytes, hipStream_t stream) {
   if (B == 0) return hipSuccess;
   const double inv_t = 1.0 / (double)temperature;
   uint32_t p24 = (uint32_t)rint((double)top_p * 16777216.0);
   p24 = p24 < 1 ? 1 : (p24 > (1u << 24) ? (1u << 24) : p24);
-  sample_top_p_kernel<<<B, kThreads, 0, stream>>>(V, logits, inv_t, p24, uniforms, tokens);
+  const int C = sample_split_chunks(B);
+  if (C == 1 || !workspace || ws_bytes < sample_workspace_bytes(B)) {
+    sample_top_p_kernel<<<B, kThreads, 0, stream>>>(V, logits, inv_t, p24, uniforms, tokens);
+    return hipGetLastError();
+  }
+  // Workspace layout (256-byte aligned pieces): row states, chunk maxima,
+  // histograms, tie pairs.
+  auto al = [](int64_t x) { return (x + 255) & ~(int64_t)255; };
+  char* p = (char*)workspace;
+  SplitWs ws;
+  ws.st = (RowState*)p;
+  p += al((int64_t)B * sizeof(RowState));
+  ws.cmax = (float*)p;
+  p += al((int64_t)B * C * 4);
+  ws.hist = (uint64_t*)p;
+  p += al((int64_t)B * C * kMaxBins * 8);
+  ws.ties = (uint64_t*)p;
+  const dim3 grid(C, B);
+  split_chunk_max<<<grid, kST, 0, stream>>>(V, C, logits, ws);
+  for (int r = 0; r < kRounds; ++r) {
+    split_chunk_hist<<<grid, kST, 0, stream>>>(V, C, r, logits, inv_t, ws);
+    split_select<<<B, kThreads, 0, stream>>>(C, r, p24, ws);
+  }
+  split_chunk_ties<<<grid, kST, 0, stream>>>(V, C, logits, inv_t, ws);
+  split_walk<<<B, kST, 0, stream>>>(V, C, logits, inv_t, uniforms, tokens, ws);
   return hipGetLastError();
 }
 

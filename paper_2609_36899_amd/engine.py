@@ -325,18 +325,30 @@ def weight_projection(x: torch.Tensor, w: PackedWeight, out: torch.Tensor,
     return out
 
 
+def sample_top_p_workspace_bytes(batch: int) -> int:
+    """Scratch bytes for the split form of sample_top_p (0: one group per row)."""
+    return N.check(N.load().sample_top_p_workspace_bytes(batch))
+
+
 def sample_top_p(logits: torch.Tensor, tokens_out: torch.Tensor, temperature: float,
                  top_p: float, uniforms: torch.Tensor,
+                 workspace: Optional[torch.Tensor] = None, split: bool = True,
                  stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """Temperature / top-p sampling of each row of logits [B, V] with the
-    given uniforms [B] (see sample_top_p in include/pdec.h)."""
+    given uniforms [B] (see sample_top_p in include/pdec.h).  split=False
+    passes no workspace (one work group per row)."""
     assert logits.dim() == 2 and logits.dtype == torch.float32 and logits.is_contiguous()
     B, V = logits.shape
     assert uniforms.dtype == torch.float32 and uniforms.numel() >= B and uniforms.is_cuda
     assert tokens_out.dtype == torch.int32 and tokens_out.numel() >= B
-    N.check(N.load().sample_top_p(B, V, logits.data_ptr(), float(temperature), float(top_p),
-                                  uniforms.data_ptr(), tokens_out.data_ptr(),
-                                  _stream_handle(stream)))
+    lib = N.load()
+    need = N.check(lib.sample_top_p_workspace_bytes(B)) if split else 0
+    if need and (workspace is None or workspace.numel() < need):
+        workspace = torch.empty(need, dtype=torch.uint8, device=logits.device)
+    N.check(lib.sample_top_p(B, V, logits.data_ptr(), float(temperature), float(top_p),
+                             uniforms.data_ptr(), tokens_out.data_ptr(),
+                             workspace.data_ptr() if need else None,
+                             workspace.numel() if need else 0, _stream_handle(stream)))
     return tokens_out
 
 

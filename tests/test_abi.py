@@ -76,3 +76,7 @@ def test_host_only_calls_without_gpu():
     assert lib.swiglu_projection_workspace_bytes(N.BF16, 4, 256, 256) > 0
     assert lib.swiglu_projection_workspace_bytes(N.F32, 4, 688, 256) > 0
     assert lib.swiglu_projection_workspace_bytes(N.BF16, 0, 256, 256) == N.INVALID_ARG
+    assert lib.sample_top_p_workspace_bytes(1) > 0
+    assert lib.sample_top_p_workspace_bytes(32) > 0
+    assert lib.sample_top_p_workspace_bytes(33) == 0
+    assert lib.sample_top_p_workspace_bytes(0) == N.INVALID_ARG
