@@ -977,6 +977,21 @@ def run_projections(batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), iters=24):
             "rows": rows, "cpu_baseline": None}
 
 
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+
+
+def prefill_flops(shape, n):
+    """Algorithmic flops of prefilling n tokens from an empty context: the
+    layer projections for every token (2 flops per weight) plus causal
+    attention, 4 Dh flops per (query, visible key) pair and query head.
+    No LM head (the append computes no logits here)."""
+    per_layer_w = (shape.d_model * (shape.q_dim + 2 * shape.kv_dim) + shape.q_dim * shape.d_model
+                   + 3 * shape.d_model * shape.ffn_dim)
+    gemm = 2.0 * n * shape.n_layers * per_layer_w
+    attn = 4.0 * shape.head_dim * (n * (n + 1) / 2) * shape.n_q_heads * shape.n_layers
+    return gemm + attn
+
+
 def run_kv_transfer(lengths=(4096, 16384, 65536)):
     """Prepared KV versus re-prefill for one departing trajectory.
 
@@ -1029,7 +1044,10 @@ def run_kv_transfer(lengths=(4096, 16384, 65536)):
                      "import_ms": round(import_ms, 2),
                      "import_GBps": round(nbytes / import_ms / 1e6, 1),
                      "reprefill_ms": round(prefill_ms, 1),
-                     "reprefill_tokens_per_s": round(n / prefill_ms * 1e3, 1)})
+                     "reprefill_tokens_per_s": round(n / prefill_ms * 1e3, 1),
+                     "reprefill_tflops_per_s": round(prefill_flops(shape, n) / prefill_ms / 1e9, 1),
+                     "reprefill_mfma_frac": round(prefill_flops(shape, n) / prefill_ms / 1e9
+                                                  / PEAK_BF16_TFLOPS, 3)})
         log(f"kv transfer {n}: export {export_ms:.1f} ms, import {import_ms:.1f} ms, "
             f"re-prefill {prefill_ms:.0f} ms")
         del snap
