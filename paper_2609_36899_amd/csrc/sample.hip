@@ -303,10 +303,10 @@ __global__ __launch_bounds__(kThreads) void sample_top_p_kernel(
 // ---------------------------------------------------------------------------
 constexpr int kST = 256, kSW = kST / 64;  // threads / waves of the split kernels
 
+// Per row, after the rounds so far: the key prefix, the mass of keys above
+// its range, and T_p.
 struct RowState {
   uint64_t prefix, above, t_p;
-  float m;
-  int32_t pad;
 };
 
 struct SplitWs {
