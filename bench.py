@@ -49,6 +49,8 @@ WORKLOADS = {
 # The same workloads with KV pages stored as fp8 (E4M3) codes, scales 1.
 FP8_KV = {f"{name}-fp8kv": name for name in ("decode-8b-b256-lognormal", "decode-8b-b8-long",
                                                "decode-8b-b16-pareto", "decode-8b-b64-pareto")}
+# The same workloads with the Qwen3-style per-head q/k RMSNorm (gains 1 + 0.1 N(0, 1)).
+QK_NORM = {f"{name}-qknorm": name for name in ("decode-8b-b256-lognormal", "decode-8b-b16-pareto")}
 DEFAULT_WORKLOAD = "decode-8b-b256-lognormal"
 # Multi-turn rollouts: decode segments of 128 steps separated by tool-output
 # appends of U[512, 2048] tokens per trajectory through kv_append_prefix.
@@ -97,6 +99,11 @@ def gpu_weights(shape, seed=0, std=0.02):
             "w_gate": proj(shape.ffn_dim, shape.d_model),
             "w_up": proj(shape.ffn_dim, shape.d_model),
             "w_down": proj(shape.d_model, shape.ffn_dim), "attn_norm": ones(), "ffn_norm": ones()})
+    if getattr(shape, "qk_norm", False):
+        for lay in out["layers"]:
+            for k in ("q_norm", "k_norm"):
+                gain = torch.empty(shape.head_dim, dtype=torch.float32, device="cuda")
+                lay[k] = gain.normal_(0.0, 0.1, generator=g).add_(1.0)
     out["lm_head"] = proj(shape.vocab, shape.d_model)
     out["final_norm"] = ones()
     return out
@@ -296,16 +303,18 @@ def cpu_baseline(shape, lens, budget_s=15.0, seed=7):
 # ---------------------------------------------------------------------------
 
 def run_decode(workload, steps, warmup, with_cpu):
-    """One decode workload; names in FP8_KV run the same batch with fp8 KV pages."""
+    """One decode workload; names in FP8_KV run the same batch with fp8 KV pages,
+    names in QK_NORM with per-head q/k RMSNorm."""
     import torch
 
     import paper_2609_36899_amd as P
     from paper_2609_36899_amd import _native as N
     from workload import EIGHT_B
 
-    shape = EIGHT_B
+    qk = workload in QK_NORM
+    shape = dataclasses.replace(EIGHT_B, qk_norm=True) if qk else EIGHT_B
     kv_fp8 = (1.0, 1.0) if workload in FP8_KV else None
-    batch, spec = WORKLOADS[FP8_KV.get(workload, workload)]
+    batch, spec = WORKLOADS[FP8_KV.get(workload, QK_NORM.get(workload, workload))]
     lens = draw_lengths(batch, spec)
     grow = warmup + steps + min(steps, 8) + 1  # warmup, timed and breakdown steps
     pages = int(np.sum((lens + grow + 15) // 16)) + 64
@@ -414,7 +423,8 @@ def run_decode(workload, steps, warmup, with_cpu):
                    "batch": int(batch), "context_mean": round(float(lens.mean()), 1),
                    "context_min": int(lens.min()), "context_max": int(lens.max()),
                    "length_distribution": list(spec), "page_tokens": 16,
-                   "kv_pages": "fp8 e4m3, scales 1" if kv_fp8 is not None else "bf16"},
+                   "kv_pages": "fp8 e4m3, scales 1" if kv_fp8 is not None else "bf16",
+                   "qk_norm": qk},
         "hbm_gbps": round(hbm, 1), "hbm_frac_of_peak": round(hbm / HBM_PEAK_GBS, 4),
         "step_bytes": int(step_bytes), "wall_s": round(wall, 3),
         "per_trajectory_gbps": {"mean": round(float(share.mean()), 2),
@@ -441,7 +451,7 @@ def run_decode(workload, steps, warmup, with_cpu):
     del E, weights, logits, pool
     torch.cuda.empty_cache()
     out["stream_copy"] = stream_copy_gbs()
-    if with_cpu:
+    if with_cpu and not qk:
         log("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(shape, lens)
     else:
@@ -1064,7 +1074,8 @@ def main():
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
-                    choices=sorted(WORKLOADS) + sorted(FP8_KV) + sorted(MULTITURN)
+                    choices=sorted(WORKLOADS) + sorted(FP8_KV) + sorted(QK_NORM)
+                    + sorted(MULTITURN)
                     + ["kv-transfer-8b", "projections-8b", "landscape-8b", "sampling-8b",
                        "copy-1gib", "paced-rollout-8b", "attention-b64", "tiny-fp32"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
