@@ -14,7 +14,19 @@
  *     stated otherwise.  last_error() returns a per-thread message for the
  *     last failure.
  *   - On any error no device work has been enqueued and the host-side state
- *     (sequence lengths, block tables, free pages) is unchanged.
+ *     (sequence lengths, block tables, free pages) is unchanged.  The one
+ *     exception is PDEC_HIP_ERROR from the runtime in the middle of a call
+ *     that enqueues several launches: the host state is still restored, but
+ *     launches before the failing one may have run (e.g. KV writes of the
+ *     first chunks of a prefill).  Every check that can fail on the
+ *     arguments runs before the first launch.
+ *   - Setting the environment variable PDEC_VALIDATE=1 before engine_create
+ *     makes that engine bounds-check every forward pass on the host before
+ *     enqueueing it: row slots and positions, query blocks and their work
+ *     items against the block-table row and the sequence's pages, page ids
+ *     against the pool, and pending block-table entries (range, and no entry
+ *     written twice).  A failed check returns PDEC_INVALID_ARG ("validate:
+ *     ...") with nothing enqueued.  Off by default (host cost per call).
  *   - Device memory (weights, KV pool, workspace, tokens, logits) is owned by
  *     the caller and must outlive the engine.  The library owns host metadata
  *     and a small pinned staging ring only.
@@ -223,6 +235,22 @@ int kv_extend_uninit(pdec_engine* engine, int32_t seq, int32_t n_tokens);
 int kv_append_prefix(pdec_engine* engine, int32_t seq, const int32_t* tokens_host, int32_t n,
                      int32_t chunk_tokens, float* last_logits_dev);
 
+/* The same for several sequences in one call (the backend's token batching of
+ * prefill work; Design, "Separating Departure from Placement").  Sequence
+ * seq_ids_host[i] receives n_tokens_host[i] tokens, taken in order from the
+ * concatenation tokens_host (sum of n_tokens_host ids).  The tokens of all
+ * sequences, in this order, are packed into forward passes of at most
+ * chunk_tokens rows (a pass holds pieces of up to 64 sequences); each
+ * sequence's result is the one kv_append_prefix would give, up to rounding.
+ * last_logits_dev (nullable): device fp32 [n_seqs][vocab]; row i receives
+ * the logits at sequence i's last new position.  Pages for every sequence
+ * are taken up front, all or nothing.
+ * Errors: as kv_append_prefix, and PDEC_INVALID_ARG for n_seqs outside
+ * [1, max_seqs], repeated ids or any n_tokens_host[i] < 1. */
+int kv_append_prefix_batch(pdec_engine* engine, int32_t n_seqs, const int32_t* seq_ids_host,
+                           const int32_t* n_tokens_host, const int32_t* tokens_host,
+                           int32_t chunk_tokens, float* last_logits_dev);
+
 /* One decode step for `batch` distinct resident sequences (iteration-level
  * token batching; Design, "Separating Departure from Placement").
  * seq_ids_host: host [batch] ids, any order; tokens_dev: device int32 [batch],
@@ -268,23 +296,6 @@ int kv_import(pdec_engine* engine, int32_t seq, const void* host_src, int64_t sr
 int sample(pdec_engine* engine, int32_t batch, const float* logits_dev, int32_t* tokens_dev_out,
            int32_t mode);
 
-/* ---------------------------------------------------------------------------
- * Isolated paged decode attention (one layer, no engine).
- *
- * For each sequence b and query head h (KV head g = h / (n_q_heads /
- * n_kv_heads)): out[b][h] = softmax(q[b][h] . K_g^T / sqrt(head_dim)) V_g over
- * the lens[b] cached positions of b.  Long-context decode attention is the
- * memory-bandwidth-bound part of the step (Design Principles,
- * "Specialization in Heterogeneous Pools").
- *   q: device [batch][n_q_heads][head_dim] in dtype;
- *   k_pages: device [n_pages][n_kv_heads][16][head_dim];
- *   v_pages: device [n_pages][n_kv_heads][head_dim][16];
- *   block_table_dev: device int32 [batch][bt_stride], logical page order;
- *   lens_host: host int32 [batch], each in [1, bt_stride * 16];
- *   out: device fp32 [batch][n_q_heads][head_dim];
- *   workspace: device, at least paged_attention_workspace_bytes(...).
- * Slots past lens[b] in the last page are never read.
- * ------------------------------------------------------------------------- */
 /* ---------------------------------------------------------------------------
  * Headroom pacing on this worker (Design, "Separating Departure from
  * Placement": pacing thresholds; Alg. pacing restricted to one worker, the
@@ -402,6 +413,34 @@ int swiglu_projection(int32_t dtype, int32_t M, int32_t F, int32_t K, const void
                       const void* w_gate, const void* w_up, void* u, void* workspace,
                       int64_t workspace_bytes, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Isolated paged decode attention (one layer, no engine).
+ *
+ * For each sequence b and query head h (KV head g = h / (n_q_heads /
+ * n_kv_heads)): out[b][h] = softmax(q[b][h] . K_g^T / sqrt(head_dim)) V_g over
+ * the lens[b] cached positions of b.  Long-context decode attention is the
+ * memory-bandwidth-bound part of the step (Design Principles,
+ * "Specialization in Heterogeneous Pools").
+ *   q: device [batch][n_q_heads][head_dim] in dtype;
+ *   k_pages: device [n_pages][n_kv_heads][16][head_dim];
+ *   v_pages: device [n_pages][n_kv_heads][head_dim][16];
+ *   block_table_dev: device int32 [batch][bt_stride], logical page order;
+ *   lens_host: host int32 [batch], each in [1, bt_stride * 16];
+ *   out: device fp32 [batch][n_q_heads][head_dim];
+ *   workspace: device, at least paged_attention_workspace_bytes(...) bytes
+ *     (max_total_tokens is accepted for compatibility and ignored: the work
+ *     list is bounded by the batch alone), owned by the caller; it holds the
+ *     work list and the per-item partial results.  Calls that share a
+ *     workspace must not overlap.
+ * The work list is planned on the host and copied through a small pinned
+ * staging ring that the library allocates on the first call and keeps.
+ * Slots past lens[b] in the last page are never read.  Asynchronous on
+ * stream.
+ * Errors: PDEC_INVALID_ARG (null pointers, sizes < 1, n_q_heads not a
+ * multiple of n_kv_heads, lens[b] outside [1, bt_stride * 16], workspace too
+ * small), PDEC_UNSUPPORTED (head_dim other than 64 / 128, GQA group size not
+ * dividing 16), PDEC_HIP_ERROR.
+ * ------------------------------------------------------------------------- */
 int64_t paged_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
                                         int32_t head_dim, int64_t max_total_tokens);
 

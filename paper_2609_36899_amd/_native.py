@@ -77,6 +77,8 @@ SIGNATURES = {
     "kv_extend_uninit": (c_int32, [c_void_p, c_int32, c_int32]),
     "kv_append_prefix": (c_int32, [c_void_p, c_int32, POINTER(c_int32), c_int32, c_int32,
                                    c_void_p]),
+    "kv_append_prefix_batch": (c_int32, [c_void_p, c_int32, POINTER(c_int32), POINTER(c_int32),
+                                         POINTER(c_int32), c_int32, c_void_p]),
     "decode_step": (c_int32, [c_void_p, c_int32, POINTER(c_int32), c_void_p, c_void_p]),
     "sample": (c_int32, [c_void_p, c_int32, c_void_p, c_void_p, c_int32]),
     "kv_export": (c_int32, [c_void_p, c_int32, c_void_p, c_int64, POINTER(c_int32)]),

@@ -5,6 +5,11 @@
 produces, next to this file:
   libpdec.so       -- HIP kernels + C ABI (include/pdec.h), built by hipcc for gfx950
   libpdec_host.so  -- page pool, attention planner and pacing only, built by g++ (CPU tests)
+
+    python -m paper_2609_36899_amd.build --sanitize
+
+builds libpdec_host_san.so, the host library under AddressSanitizer and
+UndefinedBehaviorSanitizer (tests/test_sanitizers.py runs the host tests on it).
 """
 
 from __future__ import annotations
@@ -61,15 +66,36 @@ def build_device(verbose: bool = False) -> str:
     return lib
 
 
-def build_host() -> str:
-    lib = os.path.join(PKG, "libpdec_host.so")
+HOST_SOURCES = ["pagepool.cpp", "pacing.cpp", "host_capi.cpp"]
+# The sanitizer build of the host library: AddressSanitizer and
+# UndefinedBehaviorSanitizer, every finding fatal.  Load it with the two
+# runtimes preloaded (SANITIZER_RUNTIMES) and ASAN_OPTIONS=detect_leaks=0
+# (the interpreter's own allocations are not ours).
+SANITIZE_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                  "-fno-sanitize-recover=all"]
+SANITIZER_RUNTIMES = ("libasan.so", "libubsan.so")
+
+
+def build_host(sanitize: bool = False) -> str:
+    """libpdec_host.so (g++ -O2), or with sanitize=True libpdec_host_san.so."""
+    lib = os.path.join(PKG, "libpdec_host_san.so" if sanitize else "libpdec_host.so")
     tmp = lib + ".tmp"
-    _run(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-Wall",
+    flags = SANITIZE_FLAGS if sanitize else ["-O2"]
+    _run(["g++", *flags, "-std=c++17", "-fPIC", "-shared", "-Wall", "-Werror",
           f"-I{os.path.join(ROOT, 'include')}",
-          os.path.join(CSRC, "pagepool.cpp"), os.path.join(CSRC, "pacing.cpp"),
-          os.path.join(CSRC, "host_capi.cpp"), "-o", tmp])
+          *[os.path.join(CSRC, f) for f in HOST_SOURCES], "-o", tmp])
     os.replace(tmp, lib)
     return lib
+
+
+def sanitizer_preload() -> str:
+    """LD_PRELOAD value that loads the sanitizer runtimes of g++."""
+    paths = []
+    for name in SANITIZER_RUNTIMES:
+        r = subprocess.run(["g++", f"-print-file-name={name}"], stdout=subprocess.PIPE,
+                           text=True, check=True)
+        paths.append(r.stdout.strip())
+    return ":".join(paths)
 
 
 def build_all(verbose: bool = False):
@@ -77,5 +103,8 @@ def build_all(verbose: bool = False):
 
 
 if __name__ == "__main__":
-    for p in build_all(verbose="-v" in sys.argv):
-        print(p)
+    if "--sanitize" in sys.argv:
+        print(build_host(sanitize=True))
+    else:
+        for p in build_all(verbose="-v" in sys.argv):
+            print(p)

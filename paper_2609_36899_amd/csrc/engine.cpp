@@ -11,6 +11,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <string>
@@ -196,13 +197,17 @@ class LaunchTimer {
 // Workspace layout.
 // ---------------------------------------------------------------------------
 struct WsLayout {
-  size_t rope, bt, meta, delta, x, h, o, u, q, part, att_ml, att_acc, total;
+  size_t rope, bt, meta, delta, x, h, o, u, q, lmg, part, att_ml, att_acc, total;
   size_t meta_bytes, part_elems, delta_cap;
   int64_t items_cap, qblocks_cap, rows_cap, part_row_slots;
   int32_t bt_stride;
 };
 
 constexpr size_t kDeltaCap = 65536;
+// Sequence pieces one prefill pass may hold (kv_append_prefix_batch packs
+// several sequences' tokens into one pass); also the most LM-head rows a
+// prefill pass produces.
+constexpr int kMaxPiecesPerPass = 64;
 // Query rows per attention work item: decode (one wave) and prefill (four).
 constexpr int kDecodeRows = 16;
 // Query rows per prefill block: 128 for the LDS-staged prefill kernel (bf16
@@ -268,7 +273,9 @@ int make_layout(const pdec_model_cfg* c, int32_t max_seqs, int32_t max_seq_len,
   // Decode: one query per block, 16-row items.  Prefill: prefill_rows / G
   // queries per block, prefill_rows-row items.
   const int pre_rows = prefill_rows(*c);
-  const int64_t pre_blocks = (max_chunk + (pre_rows / G) - 1) / (pre_rows / G);
+  // Each piece of a packed pass may leave one partly filled query block.
+  const int64_t pre_blocks = (max_chunk + (pre_rows / G) - 1) / (pre_rows / G) +
+                             std::min(kMaxPiecesPerPass, max_chunk);
   L->qblocks_cap = std::max<int64_t>(max_batch, pre_blocks);
   const int64_t items_dec = attn_target_items(c->n_kv_heads, kDecodeTargetGroups) + max_batch + 16;
   const int64_t items_pre = attn_target_items(c->n_kv_heads, kPrefillTargetGroups) + pre_blocks + 16;
@@ -277,7 +284,8 @@ int make_layout(const pdec_model_cfg* c, int32_t max_seqs, int32_t max_seq_len,
   L->bt_stride = PagePool::pages_for(max_seq_len);
   L->meta_bytes = align_up(L->rows_cap * sizeof(RowMeta)) +
                   align_up(L->qblocks_cap * sizeof(AttnQBlock)) +
-                  align_up(L->items_cap * sizeof(AttnItem)) + align_up(L->rows_cap * 4);
+                  align_up(L->items_cap * sizeof(AttnItem)) + align_up(L->rows_cap * 4) +
+                  align_up(kMaxPiecesPerPass * 4);
   L->delta_cap = kDeltaCap;
   L->part_elems = part_elems_for(c, L->rows_cap);
   size_t off = 0;
@@ -295,6 +303,7 @@ int make_layout(const pdec_model_cfg* c, int32_t max_seqs, int32_t max_seq_len,
   L->o = take((size_t)L->rows_cap * qd * ab);
   L->u = take((size_t)L->rows_cap * c->ffn_dim * ab);
   L->q = take((size_t)L->rows_cap * qd * ab);
+  L->lmg = take((size_t)kMaxPiecesPerPass * c->d_model * ab);
   L->part = take(L->part_elems * 4);
   L->att_ml = take((size_t)L->part_row_slots * c->n_kv_heads * 2 * 4);
   L->att_acc = take((size_t)L->part_row_slots * c->n_kv_heads * c->head_dim * 4);
@@ -325,7 +334,7 @@ struct pdec_engine {
   char* meta = nullptr;
   BtDelta* delta = nullptr;
   float* x = nullptr;
-  char *h = nullptr, *o = nullptr, *u = nullptr, *q = nullptr;
+  char *h = nullptr, *o = nullptr, *u = nullptr, *q = nullptr, *lmg = nullptr;
   float* part = nullptr;
   float* att_ml = nullptr;
   float* att_acc = nullptr;
@@ -336,6 +345,10 @@ struct pdec_engine {
   std::vector<char> host_meta;
   std::vector<int32_t> mark;
   int32_t epoch = 0;
+  // PDEC_VALIDATE=1 at engine creation: every pass's rows, query blocks,
+  // items, pages and pending block-table entries are bounds-checked on the
+  // host before anything is enqueued.
+  bool validate = false;
 
   int64_t ab() const { return elem_bytes(cfg.dtype); }
   int64_t kvb() const { return kv_elem_bytes(&cfg); }
@@ -349,6 +362,10 @@ namespace {
 
 int flush_deltas(pdec_engine* E) {
   const auto& pend = E->pool->pending();
+  if (E->validate) {
+    Status st = validate_deltas(pend, E->pool->max_seqs(), E->ws.bt_stride, E->pool->n_pages());
+    if (!st.good()) return fail(st.code, st.msg);
+  }
   size_t off = 0;
   while (off < pend.size()) {
     const size_t n = std::min(E->ws.delta_cap, pend.size() - off);
@@ -366,44 +383,72 @@ int max_items_per_qblock(const std::vector<AttnQBlock>& qblocks) {
   return m;
 }
 
-// Runs the decoder over M rows whose metadata is given; writes the LM-head
-// logits of every row (lm_last_only = false) or of the last row only.
-int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
-                    const std::vector<AttnQBlock>& qblocks, const std::vector<AttnItem>& items,
-                    int rows_per_item, const int32_t* tokens_dev, const int32_t* tokens_host,
-                    float* logits, bool lm_last_only) {
-  const pdec_model_cfg& c = E->cfg;
-  if ((int64_t)items.size() > E->ws.items_cap || (int64_t)qblocks.size() > E->ws.qblocks_cap ||
-      (int64_t)rows.size() > E->ws.rows_cap ||
-      (int64_t)items.size() * rows_per_item > E->ws.part_row_slots)
+// One forward pass of the decoder over M = rows.size() rows.
+struct Pass {
+  std::vector<RowMeta> rows;
+  std::vector<AttnQBlock> qblocks;
+  std::vector<AttnItem> items;
+  std::vector<int32_t> tokens;   // host token ids (prefill); empty: ids on the device
+  bool lm_all = false;           // logits of every row (decode)
+  std::vector<int32_t> lm_rows;  // otherwise: the rows whose logits are wanted
+  int32_t lm_out0 = 0;           // output row of the first of them
+};
+
+// Workspace bounds of one pass; checked for every pass of a call before the
+// first launch, so that a call either enqueues all of its work or none.
+int check_pass(const pdec_engine* E, const Pass& p, int rows_per_item) {
+  if ((int64_t)p.items.size() > E->ws.items_cap ||
+      (int64_t)p.qblocks.size() > E->ws.qblocks_cap ||
+      (int64_t)p.rows.size() > E->ws.rows_cap ||
+      (int64_t)p.items.size() * rows_per_item > E->ws.part_row_slots ||
+      (int64_t)p.lm_rows.size() > kMaxPiecesPerPass)
     return fail(PDEC_INVALID_ARG, "attention work list exceeds the workspace bound");
+  if (E->validate) {
+    Status st = validate_pass(p.rows, p.qblocks, p.items, E->pool->max_seqs(),
+                              E->pool->max_seq_len(), E->ws.bt_stride, E->pool);
+    if (!st.good()) return fail(st.code, st.msg);
+    for (int32_t r : p.lm_rows)
+      if (r < 0 || r >= (int32_t)p.rows.size()) return fail(PDEC_INVALID_ARG, "validate: LM row");
+  }
+  return PDEC_OK;
+}
+
+// Enqueues one pass (its bounds already checked).  Logits of the selected
+// rows go to logits + lm_out0 * vocab (nullable logits: none).
+int enqueue_forward(pdec_engine* E, const Pass& p, int rows_per_item, const int32_t* tokens_dev,
+                    float* logits) {
+  const pdec_model_cfg& c = E->cfg;
+  const int M = (int)p.rows.size();
   int rc = flush_deltas(E);
   if (rc != PDEC_OK) return rc;
 
   // Pack the metadata into one host buffer and copy it in one go.
+  const bool gather = logits && !p.lm_all && p.lm_rows.size() > 1;
   const size_t o_rows = 0;
-  const size_t o_qb = align_up(rows.size() * sizeof(RowMeta));
-  const size_t o_it = o_qb + align_up(qblocks.size() * sizeof(AttnQBlock));
-  const size_t o_tok = o_it + align_up(items.size() * sizeof(AttnItem));
-  const size_t total = o_tok + (tokens_host ? (size_t)M * 4 : 0);
+  const size_t o_qb = align_up(p.rows.size() * sizeof(RowMeta));
+  const size_t o_it = o_qb + align_up(p.qblocks.size() * sizeof(AttnQBlock));
+  const size_t o_tok = o_it + align_up(p.items.size() * sizeof(AttnItem));
+  const size_t o_lm = o_tok + align_up(p.tokens.size() * 4);
+  const size_t total = o_lm + (gather ? p.lm_rows.size() * 4 : 0);
   E->host_meta.resize(std::max<size_t>(total, 1));
   char* hm = E->host_meta.data();
-  std::memcpy(hm + o_rows, rows.data(), rows.size() * sizeof(RowMeta));
-  std::memcpy(hm + o_qb, qblocks.data(), qblocks.size() * sizeof(AttnQBlock));
-  std::memcpy(hm + o_it, items.data(), items.size() * sizeof(AttnItem));
-  if (tokens_host) std::memcpy(hm + o_tok, tokens_host, (size_t)M * 4);
+  std::memcpy(hm + o_rows, p.rows.data(), p.rows.size() * sizeof(RowMeta));
+  std::memcpy(hm + o_qb, p.qblocks.data(), p.qblocks.size() * sizeof(AttnQBlock));
+  std::memcpy(hm + o_it, p.items.data(), p.items.size() * sizeof(AttnItem));
+  if (!p.tokens.empty()) std::memcpy(hm + o_tok, p.tokens.data(), p.tokens.size() * 4);
+  if (gather) std::memcpy(hm + o_lm, p.lm_rows.data(), p.lm_rows.size() * 4);
   HIP_OR_FAIL(E->staging.upload(E->meta, hm, total, E->stream));
   const RowMeta* d_rows = (const RowMeta*)(E->meta + o_rows);
   const AttnQBlock* d_qb = (const AttnQBlock*)(E->meta + o_qb);
   const AttnItem* d_it = (const AttnItem*)(E->meta + o_it);
-  const int32_t* d_tok = tokens_host ? (const int32_t*)(E->meta + o_tok) : tokens_dev;
-
+  const int32_t* d_tok = p.tokens.empty() ? tokens_dev : (const int32_t*)(E->meta + o_tok);
+  const int32_t* d_lm = (const int32_t*)(E->meta + o_lm);
   const int dt = c.dtype;
   const int d = c.d_model, F = c.ffn_dim, Dh = c.head_dim;
   const int qd = c.n_q_heads * Dh, nqkv = qd + 2 * c.n_kv_heads * Dh;
   hipStream_t s = E->stream;
-  const int n_items = (int)items.size(), n_qb = (int)qblocks.size();
-  const int max_items = max_items_per_qblock(qblocks);
+  const int n_items = (int)p.items.size(), n_qb = (int)p.qblocks.size();
+  const int max_items = max_items_per_qblock(p.qblocks);
 
   HIP_OR_FAIL(launch_embed_norm(dt, M, d, c.vocab, d_tok, E->embed, E->attn_norm[0], c.rms_eps, E->x,
                                 E->h, s));
@@ -452,16 +497,23 @@ int enqueue_forward(pdec_engine* E, int M, const std::vector<RowMeta>& rows,
     const float* next_gain = (l + 1 < c.n_layers) ? E->attn_norm[l + 1] : E->final_norm;
     HIP_OR_FAIL(launch_resid_norm(dt, M, d, E->part, S, E->x, next_gain, c.rms_eps, E->h, s));
   }
-  if (logits) {
+  if (logits && (p.lm_all || !p.lm_rows.empty())) {
     WSegs lm{};
     lm.ptr[0] = E->lm_head;
     lm.row_end[0] = c.vocab;
     lm.n_seg = 1;
-    const char* a = E->h + (lm_last_only ? (int64_t)(M - 1) * d * E->ab() : 0);
+    const int m_lm = p.lm_all ? M : (int)p.lm_rows.size();
+    const char* a = E->h;
+    if (gather) {
+      HIP_OR_FAIL(launch_gather_rows(m_lm, d_lm, E->h, (int64_t)d * E->ab(), E->lmg, s));
+      a = E->lmg;
+    } else if (!p.lm_all) {
+      a = E->h + (int64_t)p.lm_rows[0] * d * E->ab();
+    }
     hipEvent_t ea, eb;
     HIP_OR_FAIL(E->timer.pair(PDEC_TIMER_LM_HEAD, &ea, &eb));
-    HIP_OR_FAIL(launch_gemm(dt, lm_last_only ? 1 : M, c.vocab, d, a, d, lm, logits, 1, d, s, ea,
-                            eb));
+    HIP_OR_FAIL(launch_gemm(dt, m_lm, c.vocab, d, a, d, lm, logits + (int64_t)p.lm_out0 * c.vocab,
+                            1, d, s, ea, eb));
   }
   return PDEC_OK;
 }
@@ -579,11 +631,16 @@ int engine_create(const pdec_model_cfg* cfg, const pdec_weights* w, void* kv_poo
   E->o = E->base + L.o;
   E->u = E->base + L.u;
   E->q = E->base + L.q;
+  E->lmg = E->base + L.lmg;
   E->part = (float*)(E->base + L.part);
   E->att_ml = (float*)(E->base + L.att_ml);
   E->att_acc = (float*)(E->base + L.att_acc);
   E->stream = (hipStream_t)stream;
   E->mark.assign(max_seqs, 0);
+  {
+    const char* v = std::getenv("PDEC_VALIDATE");
+    E->validate = v && v[0] && std::strcmp(v, "0") != 0;
+  }
 
   auto cleanup = [&](int code, const std::string& msg) {
     delete E->pool;
@@ -709,66 +766,124 @@ int decode_step(pdec_engine* E, int32_t B, const int32_t* ids, const int32_t* to
   Status st = E->pool->grow(slots.data(), B, 1, &undo);
   if (!st.good()) return fail(st.code, st.msg);
 
-  std::vector<RowMeta> rows(B);
+  Pass p;
+  p.rows.resize(B);
   std::vector<QBlockSpec> specs(B);
   for (int b = 0; b < B; ++b) {
     const int32_t pos = E->pool->len(slots[b]) - 1;
-    rows[b] = {slots[b], pos};
+    p.rows[b] = {slots[b], pos};
     specs[b] = {b, 1, slots[b], pos};
   }
-  std::vector<AttnQBlock> qblocks;
-  std::vector<AttnItem> items;
-  plan_attention(specs, choose_split_pages(total_key_pages(specs), E->cfg.n_kv_heads), &qblocks,
-                 &items);
-  int rc = enqueue_forward(E, B, rows, qblocks, items, kDecodeRows, tokens_dev, nullptr, logits,
-                           false);
+  p.lm_all = true;
+  plan_attention(specs, choose_split_pages(total_key_pages(specs), E->cfg.n_kv_heads), &p.qblocks,
+                 &p.items);
+  int rc = check_pass(E, p, kDecodeRows);
+  if (rc == PDEC_OK) rc = enqueue_forward(E, p, kDecodeRows, tokens_dev, logits);
   if (rc != PDEC_OK) E->pool->undo(undo);
   return rc;
+}
+
+int kv_append_prefix_batch(pdec_engine* E, int32_t n_seqs, const int32_t* ids,
+                           const int32_t* n_tokens, const int32_t* tokens_host,
+                           int32_t chunk_tokens, float* last_logits_dev) {
+  if (!E || !ids || !n_tokens || !tokens_host) return fail(PDEC_INVALID_ARG, "null argument");
+  if (n_seqs < 1 || n_seqs > E->pool->max_seqs())
+    return fail(PDEC_INVALID_ARG, "n_seqs outside [1, max_seqs]");
+  if (chunk_tokens < 1 || chunk_tokens > E->max_chunk)
+    return fail(PDEC_INVALID_ARG, "chunk_tokens outside [1, max_chunk]");
+  int64_t total = 0;
+  for (int i = 0; i < n_seqs; ++i) {
+    if (n_tokens[i] < 1) return fail(PDEC_INVALID_ARG, "every n_tokens must be >= 1");
+    total += n_tokens[i];
+  }
+  for (int64_t i = 0; i < total; ++i)
+    if (tokens_host[i] < 0 || tokens_host[i] >= E->cfg.vocab)
+      return fail(PDEC_INVALID_ARG, "token id outside [0, vocab)");
+  std::vector<int32_t> slots(n_seqs), len0(n_seqs);
+  if (++E->epoch == INT32_MAX) {
+    std::fill(E->mark.begin(), E->mark.end(), 0);
+    E->epoch = 1;
+  }
+  for (int i = 0; i < n_seqs; ++i) {
+    Status st = E->pool->resolve(ids[i], &slots[i]);
+    if (!st.good()) return fail(st.code, st.msg);
+    if (E->mark[slots[i]] == E->epoch) return fail(PDEC_INVALID_ARG, "sequence id repeated");
+    E->mark[slots[i]] = E->epoch;
+    len0[i] = E->pool->len(slots[i]);
+  }
+  PagePool::GrowUndo undo;
+  Status st = E->pool->grow_each(slots.data(), n_seqs, n_tokens, &undo);
+  if (!st.good()) return fail(st.code, st.msg);
+
+  // Token batching: the sequences' tokens, in order, are packed into passes
+  // of at most chunk_tokens rows and kMaxPiecesPerPass pieces.  A piece is a
+  // run of one sequence's consecutive tokens; its rows see the sequence's
+  // earlier pages (written by earlier passes or pieces) and, causally, each
+  // other.  Every pass is planned and checked before the first launch.
+  const int pre_rows = prefill_rows(E->cfg);
+  const int QB = pre_rows / (E->cfg.n_q_heads / E->cfg.n_kv_heads);
+  std::vector<Pass> passes;
+  std::vector<QBlockSpec> specs;
+  auto close = [&]() {
+    Pass& p = passes.back();
+    plan_attention(specs,
+                   choose_split_pages(total_key_pages(specs), E->cfg.n_kv_heads,
+                                      kPrefillTargetGroups),
+                   &p.qblocks, &p.items);
+    specs.clear();
+  };
+  int pieces = 0;
+  int64_t tok0 = 0;
+  for (int i = 0; i < n_seqs; ++i) {
+    for (int32_t off = 0; off < n_tokens[i];) {
+      if (passes.empty() || (int64_t)passes.back().rows.size() == chunk_tokens ||
+          pieces == kMaxPiecesPerPass) {
+        if (!passes.empty()) close();
+        passes.emplace_back();
+        pieces = 0;
+      }
+      Pass& p = passes.back();
+      const int32_t row0 = (int32_t)p.rows.size();
+      const int32_t take = std::min<int32_t>(n_tokens[i] - off, chunk_tokens - row0);
+      const int32_t pos = len0[i] + off;
+      for (int32_t j = 0; j < take; ++j) {
+        p.rows.push_back({slots[i], pos + j});
+        p.tokens.push_back(tokens_host[tok0 + off + j]);
+      }
+      for (int32_t k = 0; k * QB < take; ++k)
+        specs.push_back({row0 + k * QB, std::min(QB, take - k * QB), slots[i], pos + k * QB});
+      off += take;
+      ++pieces;
+      if (off == n_tokens[i] && last_logits_dev) {
+        if (p.lm_rows.empty()) p.lm_out0 = i;
+        p.lm_rows.push_back(row0 + take - 1);
+      }
+    }
+    tok0 += n_tokens[i];
+  }
+  close();
+  for (const Pass& p : passes) {
+    int rc = check_pass(E, p, pre_rows);
+    if (rc != PDEC_OK) {
+      E->pool->undo(undo);
+      return rc;
+    }
+  }
+  for (const Pass& p : passes) {
+    int rc = enqueue_forward(E, p, pre_rows, nullptr, last_logits_dev);
+    if (rc != PDEC_OK) {  // a HIP error: earlier passes may already be enqueued
+      E->pool->undo(undo);
+      return rc;
+    }
+  }
+  return PDEC_OK;
 }
 
 int kv_append_prefix(pdec_engine* E, int32_t seq, const int32_t* tokens_host, int32_t n,
                      int32_t chunk_tokens, float* last_logits_dev) {
   if (!E || !tokens_host) return fail(PDEC_INVALID_ARG, "null argument");
   if (n < 1) return fail(PDEC_INVALID_ARG, "n must be >= 1");
-  if (chunk_tokens < 1 || chunk_tokens > E->max_chunk)
-    return fail(PDEC_INVALID_ARG, "chunk_tokens outside [1, max_chunk]");
-  for (int i = 0; i < n; ++i)
-    if (tokens_host[i] < 0 || tokens_host[i] >= E->cfg.vocab)
-      return fail(PDEC_INVALID_ARG, "token id outside [0, vocab)");
-  int32_t slot;
-  Status st = E->pool->resolve(seq, &slot);
-  if (!st.good()) return fail(st.code, st.msg);
-  const int32_t len0 = E->pool->len(slot);
-  PagePool::GrowUndo undo;
-  st = E->pool->grow(&slot, 1, n, &undo);
-  if (!st.good()) return fail(st.code, st.msg);
-
-  const int pre_rows = prefill_rows(E->cfg);
-  const int QB = pre_rows / (E->cfg.n_q_heads / E->cfg.n_kv_heads);
-  std::vector<RowMeta> rows;
-  std::vector<QBlockSpec> specs;
-  std::vector<AttnQBlock> qblocks;
-  std::vector<AttnItem> items;
-  for (int32_t c0 = 0; c0 < n; c0 += chunk_tokens) {
-    const int C = std::min(chunk_tokens, n - c0);
-    rows.resize(C);
-    for (int i = 0; i < C; ++i) rows[i] = {slot, len0 + c0 + i};
-    specs.clear();
-    for (int k = 0; k * QB < C; ++k)
-      specs.push_back({k * QB, std::min(QB, C - k * QB), slot, len0 + c0 + k * QB});
-    plan_attention(specs,
-                   choose_split_pages(total_key_pages(specs), E->cfg.n_kv_heads,
-                                      kPrefillTargetGroups),
-                   &qblocks, &items);
-    const bool last = c0 + C >= n;
-    int rc = enqueue_forward(E, C, rows, qblocks, items, pre_rows, nullptr, tokens_host + c0,
-                             last ? last_logits_dev : nullptr, true);
-    if (rc != PDEC_OK) {
-      E->pool->undo(undo);
-      return rc;
-    }
-  }
-  return PDEC_OK;
+  return kv_append_prefix_batch(E, 1, &seq, &n, tokens_host, chunk_tokens, last_logits_dev);
 }
 
 namespace {

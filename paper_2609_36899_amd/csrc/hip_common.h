@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "fp8_e4m3.h"
+
 namespace pdec {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -109,22 +111,7 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return t;
 }
 
-// ---- fp8 (OCP E4M3FN) KV codes -------------------------------------------
-// sign, 4 exponent bits (bias 7), 3 mantissa bits; subnormals m * 2^-9;
-// largest finite 448; S.1111.111 is NaN (never produced here).
-// Round to nearest, ties to even, saturating at +-448; the sign is kept on
-// values that round to zero.  Exact integer steps on the float's bits.
-__device__ __forceinline__ uint32_t e4m3_from_f32(float x) {
-  const uint32_t b = __float_as_uint(x);
-  const uint32_t sign = (b >> 24) & 0x80u;
-  const float a = fabsf(x);
-  if (!(a < 448.f)) return sign | 0x7Eu;  // saturate (NaN inputs too)
-  if (a < 0x1p-6f) return sign | (uint32_t)rintf(a * 512.f);  // subnormal step 2^-9; 8 -> 0x08
-  const uint32_t mant = b & 0x7FFFFFu;
-  const uint32_t r = mant + 0x7FFFFu + ((mant >> 20) & 1u);  // RNE to 3 mantissa bits
-  const int e = (int)((b >> 23) & 0xFFu) - 127 + (int)(r >> 23);
-  return sign | ((uint32_t)(e + 7) << 3) | ((r >> 20) & 7u);
-}
+// ---- fp8 (OCP E4M3FN) KV codes: e4m3_from_f32 in fp8_e4m3.h --------------
 
 // Eight codes (two dwords, code i in byte i) to eight bf16 values: the
 // hardware fp8 -> f32 conversion, then f32 -> bf16, both exact (every e4m3

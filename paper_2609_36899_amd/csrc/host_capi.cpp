@@ -8,6 +8,7 @@
 #include <string>
 #include <vector>
 
+#include "fp8_e4m3.h"
 #include "pacing.h"
 #include "pagepool.h"
 
@@ -128,6 +129,41 @@ int64_t pp_total_key_pages(const int32_t* specs, int32_t n) {
   for (int i = 0; i < n; ++i)
     sp[i] = {specs[4 * i], specs[4 * i + 1], specs[4 * i + 2], specs[4 * i + 3]};
   return total_key_pages(sp);
+}
+
+// Host bounds checks of a pass (validate_pass / validate_deltas), as the
+// engine runs them under PDEC_VALIDATE.  rows: n_rows x (slot, pos);
+// qblocks: n_qb x (q_row0, n_q, slot, pos0, item_begin, item_end); items:
+// n_items x (qblock, page_begin, n_pages, order); pool (nullable) adds the
+// checks against live sequences and their pages.  Returns 0 or an error code
+// (pp_last_error names the failed check).
+int pp_validate_pass(void* pool, const int32_t* rows, int32_t n_rows, const int32_t* qblocks,
+                     int32_t n_qb, const int32_t* items, int32_t n_items, int32_t max_seqs,
+                     int32_t max_seq_len, int32_t bt_stride) {
+  std::vector<RowMeta> r(n_rows);
+  for (int i = 0; i < n_rows; ++i) r[i] = {rows[2 * i], rows[2 * i + 1]};
+  std::vector<AttnQBlock> q(n_qb);
+  for (int i = 0; i < n_qb; ++i) {
+    const int32_t* v = qblocks + 6 * i;
+    q[i] = AttnQBlock{v[0], v[1], v[2], v[3], v[4], v[5], 0, 0};
+  }
+  std::vector<AttnItem> it(n_items);
+  for (int i = 0; i < n_items; ++i)
+    it[i] = {items[4 * i], items[4 * i + 1], items[4 * i + 2], items[4 * i + 3]};
+  return ret(validate_pass(r, q, it, max_seqs, max_seq_len, bt_stride, (const PagePool*)pool));
+}
+
+// deltas: n x (slot, idx, page).
+int pp_validate_deltas(const int32_t* deltas, int32_t n, int32_t max_seqs, int32_t bt_stride,
+                       int32_t n_pages) {
+  std::vector<BtDelta> d(n);
+  for (int i = 0; i < n; ++i) d[i] = {deltas[3 * i], deltas[3 * i + 1], deltas[3 * i + 2], 0};
+  return ret(validate_deltas(d, max_seqs, bt_stride, n_pages));
+}
+
+// E4M3 codes of n floats, as the fp8 KV page writes compute them.
+void pp_e4m3_encode(const float* x, uint8_t* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = (uint8_t)e4m3_from_f32(x[i]);
 }
 
 // Pacing decision (the same code the device library exports as pacing_plan).

@@ -120,6 +120,9 @@ hipError_t launch_swiglu(int dtype, int M, int F, const float* part, int splits,
 // out[i] = sum_s part[s][i] over `splits` slabs of n floats (n % 4 == 0).
 hipError_t launch_sum_splits(int64_t n, const float* part, int splits, float* out,
                              hipStream_t stream);
+// dst[i] = src[idx[i]] for n rows of row_bytes bytes (row_bytes % 4 == 0).
+hipError_t launch_gather_rows(int n, const int32_t* idx, const void* src, int64_t row_bytes,
+                              void* dst, hipStream_t stream);
 // tokens[b] = argmax_v logits[b][v] (lowest index on ties).
 hipError_t launch_argmax(int B, int V, const float* logits, int32_t* tokens, hipStream_t stream);
 // bt[d.slot * stride + d.idx] = d.page for each delta.

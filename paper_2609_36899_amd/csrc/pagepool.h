@@ -41,6 +41,7 @@ class PagePool {
   // Resolve an id to its slot; BAD_SEQ if unknown or stale.
   Status resolve(int32_t id, int32_t* slot) const;
 
+  bool live(int32_t slot) const { return slot >= 0 && slot < max_seqs_ && seqs_[slot].live; }
   int32_t len(int32_t slot) const { return seqs_[slot].len; }
   const std::vector<int32_t>& pages(int32_t slot) const { return seqs_[slot].pages; }
 
@@ -54,11 +55,16 @@ class PagePool {
   // lengths.  All-or-nothing: on failure nothing changes.  The block-table
   // entries of newly attached pages are appended to the pending list.
   Status grow(const int32_t* slots, int32_t n, int32_t extra, GrowUndo* undo = nullptr);
-  // Take back a successful grow() (used when enqueueing device work fails).
+  // The same with its own count per slot: slot slots[i] grows by extras[i].
+  Status grow_each(const int32_t* slots, int32_t n, const int32_t* extras,
+                   GrowUndo* undo = nullptr);
+  // Take back a successful grow() (used when enqueueing device work fails,
+  // before any other call changes the pool).
   void undo(const GrowUndo& u);
 
   // Block-table entries written on the host but not yet on the device, in
-  // the order they were made.
+  // the order they were made.  No (slot, idx) appears twice: the device
+  // writes them all in parallel.
   const std::vector<BtDelta>& pending() const { return pending_; }
   void clear_pending() { pending_.clear(); }
 
@@ -116,5 +122,22 @@ void plan_attention(const std::vector<QBlockSpec>& specs, int32_t split_pages,
 
 // Total pages touched by the query blocks (the key-axis workload).
 int64_t total_key_pages(const std::vector<QBlockSpec>& specs);
+
+// Bounds of one forward pass, checked on the host before any launch: every
+// row's slot is a sequence slot and its position lies inside the sequence
+// and the rotary table; every query block's rows lie inside the pass and its
+// items inside the block's key range and the block-table row; every item
+// belongs to its block; the dispatch order is a permutation; and each block
+// covers its keys exactly once.  `pool` (nullable) adds: the slot is live,
+// the block's keys are within the sequence length, and every page the block
+// reads is one the sequence holds and below the pool size.
+Status validate_pass(const std::vector<RowMeta>& rows, const std::vector<AttnQBlock>& qblocks,
+                     const std::vector<AttnItem>& items, int32_t max_seqs, int32_t max_seq_len,
+                     int32_t bt_stride, const PagePool* pool);
+
+// Pending block-table entries: slots, indexes and pages in range, and no
+// (slot, idx) twice.
+Status validate_deltas(const std::vector<BtDelta>& d, int32_t max_seqs, int32_t bt_stride,
+                       int32_t n_pages);
 
 }  // namespace pdec

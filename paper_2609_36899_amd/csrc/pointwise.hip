@@ -247,6 +247,16 @@ __global__ __launch_bounds__(256) void sum_splits_kernel(int64_t n4, const float
   }
 }
 
+// One work group per row, 4-byte words.
+__global__ __launch_bounds__(256) void gather_rows_kernel(const int32_t* __restrict__ idx,
+                                                          const uint32_t* __restrict__ src,
+                                                          int64_t row_words,
+                                                          uint32_t* __restrict__ dst) {
+  const uint32_t* s = src + (int64_t)idx[blockIdx.x] * row_words;
+  uint32_t* d = dst + (int64_t)blockIdx.x * row_words;
+  for (int64_t i = threadIdx.x; i < row_words; i += 256) d[i] = s[i];
+}
+
 __device__ __forceinline__ void argmax_merge(float& v, int& i, float v2, int i2) {
   if (v2 > v || (v2 == v && i2 < i)) {
     v = v2;
@@ -381,6 +391,14 @@ hipError_t launch_sum_splits(int64_t n, const float* part, int splits, float* ou
                              hipStream_t stream) {
   if (n == 0) return hipSuccess;
   sum_splits_kernel<<<grid_for(n / 4, 256), 256, 0, stream>>>(n / 4, part, splits, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(int n, const int32_t* idx, const void* src, int64_t row_bytes,
+                              void* dst, hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  gather_rows_kernel<<<n, 256, 0, stream>>>(idx, (const uint32_t*)src, row_bytes / 4,
+                                            (uint32_t*)dst);
   return hipGetLastError();
 }
 

@@ -233,6 +233,24 @@ class Engine:
                                           tok.ctypes.data_as(POINTER(c_int32)), len(tok),
                                           int(chunk_tokens), _ptr(last_logits)))
 
+    def kv_append_prefix_batch(self, seq_ids: Sequence[int], tokens: Sequence[Sequence[int]],
+                               chunk_tokens: int,
+                               last_logits: Optional[torch.Tensor] = None) -> None:
+        """Append tokens[i] to seq_ids[i] for every i in one call (packed passes)."""
+        ids = np.ascontiguousarray(np.asarray(seq_ids, dtype=np.int32))
+        parts = [np.asarray(t, dtype=np.int32).ravel() for t in tokens]
+        assert len(parts) == len(ids)
+        counts = np.ascontiguousarray(np.array([len(t) for t in parts], dtype=np.int32))
+        flat = np.ascontiguousarray(np.concatenate(parts) if parts else np.zeros(0, np.int32))
+        if last_logits is not None:
+            assert last_logits.is_cuda and last_logits.dtype == torch.float32
+            assert last_logits.numel() >= len(ids) * self.shape.vocab
+            assert last_logits.is_contiguous()
+        N.check(self.lib.kv_append_prefix_batch(
+            self.handle, len(ids), ids.ctypes.data_as(POINTER(c_int32)),
+            counts.ctypes.data_as(POINTER(c_int32)), flat.ctypes.data_as(POINTER(c_int32)),
+            int(chunk_tokens), _ptr(last_logits)))
+
     def decode_step(self, seq_ids: Sequence[int], tokens: torch.Tensor,
                     logits: torch.Tensor) -> None:
         ids = np.ascontiguousarray(np.asarray(seq_ids, dtype=np.int32))

@@ -17,7 +17,10 @@ from hypothesis import given, settings
 from hypothesis import strategies as st
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HOST_LIB = os.path.join(ROOT, "paper_2609_36899_amd", "libpdec_host.so")
+# PDEC_HOST_LIB selects another build of the host library (the sanitizer
+# build, see tests/test_sanitizers.py).
+HOST_LIB = os.environ.get("PDEC_HOST_LIB") or os.path.join(ROOT, "paper_2609_36899_amd",
+                                                           "libpdec_host.so")
 
 OK, INVALID_ARG, OUT_OF_PAGES, BAD_SEQ, SEQ_TOO_LONG = 0, -1, -2, -3, -4
 
@@ -48,6 +51,14 @@ def lib():
                           POINTER(c_int32), c_int32]
     L.pp_total_key_pages.restype = c_int64
     L.pp_total_key_pages.argtypes = [POINTER(c_int32), c_int32]
+    L.pp_last_error.restype = ctypes.c_char_p
+    L.pp_validate_pass.argtypes = [c_void_p, POINTER(c_int32), c_int32, POINTER(c_int32),
+                                   c_int32, POINTER(c_int32), c_int32, c_int32, c_int32, c_int32]
+    L.pp_validate_deltas.argtypes = [POINTER(c_int32), c_int32, c_int32, c_int32, c_int32]
+    L.pp_pacing_plan.argtypes = [c_int64, c_int64, c_int64, c_int32, POINTER(c_int32),
+                                 POINTER(c_int32), POINTER(ctypes.c_int64), c_int32,
+                                 POINTER(c_int32), POINTER(c_int32), POINTER(c_int32),
+                                 POINTER(c_int32), POINTER(c_int32), POINTER(c_int32)]
     return L
 
 
@@ -193,7 +204,29 @@ class ModelPool:
         return OK
 
 
-ops = st.lists(st.tuples(st.sampled_from(["alloc", "free", "grow", "grow_all"]),
+def test_free_then_realloc_leaves_no_stale_pending_entry(lib):
+    # The device applies all pending entries in parallel, in no order, so a
+    # freed slot's unflushed entry beside its next occupant's entry for the
+    # same (slot, idx) could point that occupant at another sequence's page.
+    p = Pool(lib, n_pages=8, max_seqs=4, max_len=256)
+    rc, a = p.alloc(32)                      # slot 0, pages 0, 1
+    assert rc == OK
+    assert p.free(a) == OK
+    rc, b = p.alloc(16)                      # slot 0 again
+    rc2, c = p.alloc(16)                     # slot 1
+    assert rc == rc2 == OK
+    assert p.grow([b], 17) == OK             # slot 0 attaches a second page
+    pend = p.pending()
+    keys = [(s, i) for s, i, _ in pend]
+    assert len(keys) == len(set(keys))
+    table = {(s, i): pg for s, i, pg in pend}
+    for sid in (b, c):
+        slot = lib.pp_slot(p.h, sid)
+        assert [table[(slot, k)] for k in range(len(p.pages(sid)))] == p.pages(sid)
+    assert set(p.pages(b)).isdisjoint(p.pages(c))
+
+
+ops = st.lists(st.tuples(st.sampled_from(["alloc", "free", "grow", "grow_all", "flush"]),
                          st.integers(0, 200), st.integers(0, 7)), min_size=1, max_size=60)
 
 
@@ -205,7 +238,19 @@ def test_pool_matches_python_model(lib, seq_ops):
     m = ModelPool(n_pages, max_seqs, max_len)
     live = []  # (id, key)
     key = 0
+    device = {}  # the device block table: (slot, idx) -> page
+
+    def flush():
+        pend = p.pending()
+        keys = [(s, i) for s, i, _ in pend]
+        assert len(keys) == len(set(keys)), "a (slot, idx) pending twice"
+        for s, i, pg in pend:
+            device[(s, i)] = pg
+        lib.pp_clear_pending(p.h)
+
     for op, a, b in seq_ops:
+        if op == "flush":
+            flush()
         if op == "alloc":
             rc, sid = p.alloc(a)
             exp = m.alloc(a)
@@ -230,6 +275,12 @@ def test_pool_matches_python_model(lib, seq_ops):
         for sid, k in live:
             assert p.len(sid) == (OK, m.seqs[k][0])
             assert len(p.pages(sid)) == m.seqs[k][1]
+    # After the deltas reach the device, its table matches every live
+    # sequence's pages.
+    flush()
+    for sid, _ in live:
+        slot = lib.pp_slot(p.h, sid)
+        assert [device[(slot, k)] for k in range(len(p.pages(sid)))] == p.pages(sid)
     # pages of live sequences are distinct and disjoint from each other
     allp = [pg for sid, _ in live for pg in p.pages(sid)]
     assert len(allp) == len(set(allp))
@@ -285,3 +336,132 @@ def test_split_targets_work_group_count(lib):
     s = lib.pp_choose_split(total, 8)
     items = -(-total // s)
     assert lib.pp_target_items(8) // 2 <= items <= lib.pp_target_items(8)
+
+
+def _arr(vals):
+    vals = [int(v) for v in vals]
+    return (c_int32 * max(len(vals), 1))(*vals)
+
+
+def _validate(lib, pool, rows, qbs, items, max_seqs=8, max_len=4096, bt_stride=256):
+    return lib.pp_validate_pass(pool, _arr([v for r in rows for v in r]), len(rows),
+                                _arr([v for q in qbs for v in q]), len(qbs),
+                                _arr([v for it in items for v in it]), len(items),
+                                max_seqs, max_len, bt_stride)
+
+
+def _decode_pass(lib, p, ids):
+    """Rows, query blocks and items of one decode step over ids (after growth)."""
+    rows, specs = [], []
+    for b, sid in enumerate(ids):
+        slot, pos = lib.pp_slot(p.h, sid), p.len(sid)[1] - 1
+        rows.append((slot, pos))
+        specs.append((b, 1, slot, pos))
+    arr = _arr([v for sp in specs for v in sp])
+    split = lib.pp_choose_split(lib.pp_total_key_pages(arr, len(specs)), 8)
+    qb = (c_int32 * (6 * len(specs)))()
+    it = (c_int32 * (4 * 4096))()
+    n = lib.pp_plan(arr, len(specs), split, qb, it, 4096)
+    assert n > 0
+    return (rows, [tuple(qb[6 * i:6 * i + 6]) for i in range(len(specs))],
+            [tuple(it[4 * i:4 * i + 4]) for i in range(n)])
+
+
+def test_validate_accepts_planned_passes_and_names_each_violation(lib):
+    p = Pool(lib, n_pages=64, max_seqs=8, max_len=4096)
+    ids = [p.alloc(0)[1] for _ in range(3)]
+    for sid, n in zip(ids, (40, 300, 17)):
+        assert p.grow([sid], n) == OK
+    rows, qbs, items = _decode_pass(lib, p, ids)
+    assert _validate(lib, p.h, rows, qbs, items) == OK
+    assert _validate(lib, None, rows, qbs, items) == OK
+
+    def rejects(rows_, qbs_, items_, pool=p.h, **kw):
+        rc = _validate(lib, pool, rows_, qbs_, items_, **kw)
+        assert rc == INVALID_ARG, rc
+        return lib.pp_last_error().decode()
+
+    # item range past the block's keys, and a gap in the covered keys
+    bad = list(items)
+    q, pb, npg, o = bad[qbs[0][4]]
+    bad[qbs[0][4]] = (q, pb, npg + 1, o)
+    assert "keys not covered" in rejects(rows, qbs, bad)
+    bad = list(items)
+    bad[qbs[1][4] + 1] = (1, bad[qbs[1][4] + 1][1] + 1, bad[qbs[1][4] + 1][2], bad[qbs[1][4] + 1][3])
+    assert "item" in rejects(rows, qbs, bad)
+    # dispatch order not a permutation
+    bad = list(items)
+    bad[0] = bad[0][:3] + (bad[1][3],)
+    assert "dispatch order" in rejects(rows, qbs, bad)
+    # a row past its sequence, a slot out of range, a position past the rope table
+    assert "outside its sequence" in rejects([(rows[0][0], rows[0][1] + 1)] + rows[1:],
+                                             [(0, 1, rows[0][0], rows[0][1] + 1) + qbs[0][4:]] +
+                                             qbs[1:], items)
+    assert "slot" in rejects([(9, 0)] + rows[1:], qbs, items, pool=None)
+    assert "position" in rejects(rows, qbs, items, pool=None, max_len=100)
+    # keys past the block-table row
+    assert "block-table row" in rejects(rows, qbs, items, pool=None, bt_stride=2)
+    # a freed sequence's block
+    assert p.free(ids[2]) == OK
+    assert "outside its sequence" in rejects(rows, qbs, items)
+
+
+def test_validate_deltas(lib):
+    ok = [(0, 0, 5), (0, 1, 6), (1, 0, 7)]
+    flat = _arr([v for d in ok for v in d])
+    assert lib.pp_validate_deltas(flat, 3, 4, 16, 8) == OK
+    dup = ok + [(0, 1, 3)]
+    assert lib.pp_validate_deltas(_arr([v for d in dup for v in d]), 4, 4, 16, 8) == INVALID_ARG
+    assert "twice" in lib.pp_last_error().decode()
+    for bad in ([(0, 0, 8)], [(4, 0, 1)], [(0, 16, 1)], [(0, -1, 1)], [(0, 0, -1)]):
+        assert lib.pp_validate_deltas(_arr([v for d in bad for v in d]), 1, 4, 16, 8) == INVALID_ARG
+
+
+@settings(max_examples=100, deadline=None)
+@given(ops)
+def test_every_decode_pass_of_a_random_history_validates(lib, seq_ops):
+    p = Pool(lib, 40, 6, 300)
+    live = []
+    for op, a, b in seq_ops:
+        if op == "alloc":
+            rc, sid = p.alloc(a)
+            if rc == OK:
+                live.append(sid)
+        elif op == "free" and live:
+            assert p.free(live.pop(b % len(live))) == OK
+        elif op in ("grow", "grow_all") and live:
+            chosen = live if op == "grow_all" else [live[b % len(live)]]
+            p.grow(chosen, a % 70)
+        elif op == "flush":
+            lib.pp_clear_pending(p.h)
+        pend = p.pending()
+        assert lib.pp_validate_deltas(_arr([v for d in pend for v in d]), len(pend), 6,
+                                      19, 40) == OK
+        nonempty = [s for s in live if p.len(s)[1] > 0]
+        if nonempty:
+            rows, qbs, items = _decode_pass(lib, p, nonempty)
+            assert _validate(lib, p.h, rows, qbs, items, max_seqs=6, max_len=300,
+                             bt_stride=19) == OK
+
+
+@settings(max_examples=200, deadline=None)
+@given(st.integers(0, 6000), st.integers(0, 5000), st.integers(0, 400),
+       st.lists(st.tuples(st.integers(0, 4000), st.booleans()), max_size=20),
+       st.lists(st.integers(0, 4000), max_size=12), st.integers(0, 1000))
+def test_host_pacing_plan_equals_oracle(lib, h, h_min, delta, act, pend, seed):
+    """The pacing decision in the host library (the same source the device
+    library exports as pacing_plan) against the oracle."""
+    from oracle import pacing as op
+    ids = np.random.default_rng(seed).permutation(1000)[:len(act) + len(pend)].tolist()
+    active = [(ids[i], ln, op.footprint(ln) + (16 if extra else 0))
+              for i, (ln, extra) in enumerate(act)]
+    pending = [(ids[len(act) + j], ln) for j, ln in enumerate(pend)]
+    na, npd = len(active), len(pending)
+    ev, pl = _arr([0] * na), _arr([0] * (na + npd))
+    n_ev, n_pl = c_int32(), c_int32()
+    held = (ctypes.c_int64 * max(na, 1))(*[a[2] for a in active])
+    lib.pp_pacing_plan(h, h_min, delta, na, _arr([a[0] for a in active]),
+                       _arr([a[1] for a in active]), held, npd, _arr([q[0] for q in pending]),
+                       _arr([q[1] for q in pending]), ev, byref(n_ev), pl, byref(n_pl))
+    got = (list(ev[:n_ev.value]), list(pl[:n_pl.value]))
+    assert got == op.pacing_plan(h, h_min, delta, active, pending)

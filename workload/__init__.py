@@ -122,6 +122,20 @@ def make_weights(shape: ModelShape, seed: int = 0, bf16: bool = False,
     return weights
 
 
+def cached_kv(n_tokens: int, n_kv_heads: int, head_dim: int, seed: int, k_std: float = 1.0,
+              bf16: bool = True):
+    """Seeded K and V values of one layer's cache, ``[n_tokens][Hkv][Dh]`` each:
+    K ~ N(0, k_std^2), V ~ N(0, 1), float32 (bf16-representable with ``bf16``).
+    Used to stage long contexts directly into pages (and into the oracle's
+    contiguous cache) instead of running a long prefill."""
+    rng = np.random.default_rng(seed)
+    k = rng.standard_normal((n_tokens, n_kv_heads, head_dim), dtype=np.float32) * np.float32(k_std)
+    v = rng.standard_normal((n_tokens, n_kv_heads, head_dim), dtype=np.float32)
+    if bf16:
+        k, v = round_to_bf16(k), round_to_bf16(v)
+    return k, v
+
+
 def random_tokens(n: int, vocab: int, seed: int) -> np.ndarray:
     return np.random.default_rng(seed).integers(0, vocab, size=n, dtype=np.int64).astype(np.int32)
 
