@@ -351,6 +351,25 @@ int sample_top_p(int32_t batch, int32_t vocab, const float* logits_dev, float te
                  float top_p, const float* uniforms_dev, int32_t* tokens_dev_out,
                  void* workspace, int64_t workspace_bytes, void* stream);
 
+/* sample_top_p for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same tokens as sample_top_p, with the split form's scratch (row states and
+ * per-chunk partial results, no more than about 4 MiB) in a static device
+ * array that the library holds instead of a caller workspace.  The call
+ * itself allocates nothing: the array exists once per GPU, from the time
+ * the library is loaded until the process ends, and its device address is
+ * looked up on the first call on each device (hipGetSymbolAddress).  Every
+ * call on one GPU shares that GPU's array, so calls that overlap on one GPU
+ * (on different streams, or from different threads) race and must not be
+ * made; calls in one stream's order are safe.  Batches above 32 rows use
+ * the one-group form, which needs no scratch.
+ * Errors: as sample_top_p (without the workspace cases), and
+ * PDEC_INVALID_ARG if a batch would need more scratch than the array holds
+ * (the message gives both sizes). */
+int sample_top_p_noalloc(int32_t batch, int32_t vocab, const float* logits_dev,
+                         float temperature, float top_p, const float* uniforms_dev,
+                         int32_t* tokens_dev_out, void* stream);
+
 /* ---------------------------------------------------------------------------
  * Weight packing.  Each decode step streams every projection matrix from HBM
  * once for the whole batch (Introduction; Design Principles, "Specialization

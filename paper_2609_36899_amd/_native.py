@@ -90,6 +90,8 @@ SIGNATURES = {
     "sample_top_p_workspace_bytes": (c_int64, [c_int32]),
     "sample_top_p": (c_int32, [c_int32, c_int32, c_void_p, c_float, c_float, c_void_p, c_void_p,
                                c_void_p, c_int64, c_void_p]),
+    "sample_top_p_noalloc": (c_int32, [c_int32, c_int32, c_void_p, c_float, c_float, c_void_p,
+                                       c_void_p, c_void_p]),
     "packed_weight_bytes": (c_int64, [c_int32, c_int32, c_int32]),
     "pack_weight": (c_int32, [c_int32, c_int32, c_int32, c_void_p, c_void_p, c_void_p]),
     "weight_projection_workspace_bytes": (c_int64, [c_int32, c_int32, c_int32, c_int32]),

@@ -1018,6 +1018,28 @@ int sample_top_p(int32_t batch, int32_t vocab, const float* logits_dev, float te
   return PDEC_OK;
 }
 
+int sample_top_p_noalloc(int32_t batch, int32_t vocab, const float* logits_dev,
+                         float temperature, float top_p, const float* uniforms_dev,
+                         int32_t* tokens_dev_out, void* stream) {
+  if (batch < 1 || vocab < 1) return fail(PDEC_INVALID_ARG, "batch and vocab must be positive");
+  if (!logits_dev || !uniforms_dev || !tokens_dev_out)
+    return fail(PDEC_INVALID_ARG, "null argument");
+  if (!(temperature > 0.f) || !std::isfinite(temperature))
+    return fail(PDEC_INVALID_ARG, "temperature must be positive and finite");
+  if (!(top_p > 0.f && top_p <= 1.f)) return fail(PDEC_INVALID_ARG, "top_p must be in (0, 1]");
+  const int64_t need = sample_workspace_bytes(batch), have = sample_scratch_bytes();
+  if (need > have)
+    return fail(PDEC_INVALID_ARG, "batch " + std::to_string(batch) + " needs " +
+                                      std::to_string(need) + " bytes of scratch; the static "
+                                      "scratch holds " + std::to_string(have));
+  void* scratch = nullptr;
+  if (need > 0) HIP_OR_FAIL(sample_scratch_ptr(&scratch));
+  HIP_OR_FAIL(launch_sample_top_p(batch, vocab, logits_dev, temperature, top_p, uniforms_dev,
+                                  tokens_dev_out, scratch, need > 0 ? have : 0,
+                                  (hipStream_t)stream));
+  return PDEC_OK;
+}
+
 int64_t packed_weight_bytes(int32_t dtype, int32_t N, int32_t K) {
   if ((dtype != PDEC_F32 && dtype != PDEC_BF16) || N < 1 || K < 1)
     return fail(PDEC_INVALID_ARG, "bad weight shape");

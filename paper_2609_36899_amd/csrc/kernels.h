@@ -86,6 +86,11 @@ hipError_t launch_gemm_swiglu(int M, int F, int K, const void* A, int64_t lda, c
 // With a workspace of sample_workspace_bytes(B) (> 0 only for small batches)
 // every pass is split over several work groups per row; same tokens.
 int64_t sample_workspace_bytes(int B);
+// The static scratch of sample_top_p_noalloc: its size (at least
+// sample_workspace_bytes(B) for every B) and this GPU's device address of it
+// (looked up on the first call per device).
+int64_t sample_scratch_bytes();
+hipError_t sample_scratch_ptr(void** out);
 hipError_t launch_sample_top_p(int B, int V, const float* logits, float temperature, float top_p,
                                const float* uniforms, int32_t* tokens, void* workspace,
                                int64_t ws_bytes, hipStream_t stream);

@@ -27,6 +27,7 @@
 #include "kernels.h"
 
 #include <climits>
+#include <mutex>
 
 namespace pdec {
 
@@ -598,18 +599,70 @@ __global__ __launch_bounds__(kST) void split_walk(int V, int C, const float* __r
 
 }  // namespace
 
-int sample_split_chunks(int B) {
+namespace {
+
+constexpr int sample_split_chunks(int B) {
   // About 256 work groups per pass: 16 chunks per row up to 16 rows, 8 up
   // to 32, none above (at 64 rows the split form's eleven launches already
   // cost more than its wider passes save).
-  const int c = B > 0 ? 256 / B : 1;
-  return c >= 16 ? 16 : c >= 8 ? 8 : 1;
+  return (B > 0 ? 256 / B : 1) >= 16 ? 16 : (B > 0 ? 256 / B : 1) >= 8 ? 8 : 1;
 }
 
-int64_t sample_workspace_bytes(int B) {
-  const int C = sample_split_chunks(B);
-  if (C == 1) return 0;
-  return (int64_t)B * (sizeof(RowState) + C * 4 + C * kMaxBins * 8 + C * 16) + 1024;
+constexpr int64_t split_workspace_bytes(int B) {
+  return sample_split_chunks(B) == 1
+             ? 0
+             : (int64_t)B * ((int64_t)sizeof(RowState) + sample_split_chunks(B) * 4 +
+                             (int64_t)sample_split_chunks(B) * kMaxBins * 8 +
+                             sample_split_chunks(B) * 16) +
+                   1024;
+}
+
+constexpr int64_t max_split_workspace_bytes() {
+  int64_t m = 0;
+  for (int B = 1; B <= 256; ++B) m = split_workspace_bytes(B) > m ? split_workspace_bytes(B) : m;
+  return m;
+}
+
+// ---------------------------------------------------------------------------
+// Scratch of the no-allocation entry point (sample_top_p_noalloc): the split
+// form's row states and per-chunk partial results in a static device array
+// sized for the largest batch that takes the split form (about 4 MiB).  Each
+// GPU the library runs on holds its own copy until the process ends; every
+// call on a GPU shares that GPU's copy, so such calls must not overlap.  No
+// entry of it needs clearing: every kernel of the split form writes what
+// the next one reads before it is read.
+// ---------------------------------------------------------------------------
+constexpr int64_t kSampleScratchBytes = max_split_workspace_bytes();
+__device__ __align__(256) char sample_scratch[kSampleScratchBytes];
+
+std::mutex g_scratch_mu;
+constexpr int kMaxDevices = 64;
+void* g_scratch_dev[kMaxDevices] = {};
+
+}  // namespace
+
+int64_t sample_workspace_bytes(int B) { return split_workspace_bytes(B); }
+
+int64_t sample_scratch_bytes() { return kSampleScratchBytes; }
+
+// The device address of this GPU's copy of the scratch array.  In host code
+// the array's name is only a host-side stand-in, so the address is looked up
+// once per device (with that device current) and kept.
+hipError_t sample_scratch_ptr(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(sample_scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_sample_top_p(int B, int V, const float* logits, float temperature, float top_p,
