@@ -302,7 +302,19 @@ def cpu_baseline(shape, lens, budget_s=15.0, seed=7):
 # GPU decode run.
 # ---------------------------------------------------------------------------
 
-def run_decode(workload, steps, warmup, with_cpu):
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo), else the machine type."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def run_decode(workload, steps, warmup, with_cpu, seed=1):
     """One decode workload; names in FP8_KV run the same batch with fp8 KV pages,
     names in QK_NORM with per-head q/k RMSNorm."""
     import torch
@@ -315,7 +327,7 @@ def run_decode(workload, steps, warmup, with_cpu):
     shape = dataclasses.replace(EIGHT_B, qk_norm=True) if qk else EIGHT_B
     kv_fp8 = (1.0, 1.0) if workload in FP8_KV else None
     batch, spec = WORKLOADS[FP8_KV.get(workload, QK_NORM.get(workload, workload))]
-    lens = draw_lengths(batch, spec)
+    lens = draw_lengths(batch, spec, seed=seed)
     grow = warmup + steps + min(steps, 8) + 1  # warmup, timed and breakdown steps
     pages = int(np.sum((lens + grow + 15) // 16)) + 64
     per_tok = P.kv_bytes_per_token(shape, P.BF16, kv_fp8)
@@ -422,7 +434,7 @@ def run_decode(workload, steps, warmup, with_cpu):
                    "Dh 128, FFN 14336, vocab 128256), random init",
                    "batch": int(batch), "context_mean": round(float(lens.mean()), 1),
                    "context_min": int(lens.min()), "context_max": int(lens.max()),
-                   "length_distribution": list(spec), "page_tokens": 16,
+                   "length_distribution": list(spec), "length_seed": seed, "page_tokens": 16,
                    "kv_pages": "fp8 e4m3, scales 1" if kv_fp8 is not None else "bf16",
                    "qk_norm": qk},
         "hbm_gbps": round(hbm, 1), "hbm_frac_of_peak": round(hbm / HBM_PEAK_GBS, 4),
@@ -459,18 +471,41 @@ def run_decode(workload, steps, warmup, with_cpu):
     return out
 
 
-def run_multiturn(workload, segments, seg_steps, warmup):
+def append_flops(shape, ctx0, n):
+    """Algorithmic flops of appending n tokens onto a cached context of ctx0
+    tokens: the layer projections for every new token (2 flops per weight)
+    plus attention, 4 Dh flops per (new query, visible key) pair and query
+    head; no LM head."""
+    per_layer_w = (shape.d_model * (shape.q_dim + 2 * shape.kv_dim) + shape.q_dim * shape.d_model
+                   + 3 * shape.d_model * shape.ffn_dim)
+    gemm = 2.0 * n * shape.n_layers * per_layer_w
+    pairs = n * ctx0 + n * (n + 1) / 2
+    return gemm + 4.0 * shape.head_dim * pairs * shape.n_q_heads * shape.n_layers
+
+
+def run_multiturn(workload, segments, seg_steps, warmup, per_sequence_appends=False,
+                  append_chunk=2048):
     """Decode segments with tool-output appends in between.
 
     Capacity: the pool takes what HBM leaves after weights and workspace.
     When an append does not fit, trajectories depart longest first until it
     does (the pacing rule of evicting the longest resident), and the batch
     continues without them.  Decode tokens/s counts decode_step + sample only;
-    append time is reported separately.
+    append time is reported separately.  Each round of appends is one
+    kv_append_prefix_batch call over every live trajectory (tokens packed into
+    passes of append_chunk rows), or with per_sequence_appends one
+    kv_append_prefix call per trajectory.
+
+    Per decode segment: algorithmic HBM bytes per step (weights once, each
+    cached KV byte once, the new KV, the logits write and argmax read) at
+    that segment's contexts, and the attention pass's bytes per launch over
+    its average launch time (one launch in every n_layers + 1 timed, as in
+    the decode workloads).
     """
     import torch
 
     import paper_2609_36899_amd as P
+    from paper_2609_36899_amd import _native as N
     from workload import EIGHT_B, lengths_uniform
 
     shape = EIGHT_B
@@ -478,6 +513,7 @@ def run_multiturn(workload, segments, seg_steps, warmup):
     lens = draw_lengths(batch, ("pareto", 1.5, 1024, 65536))
     adds = [lengths_uniform(batch, 512, 2048, seed=10 + k) for k in range(segments - 1)]
     per_tok = P.kv_bytes_per_token(shape, P.BF16)
+    kv_layer_tok = shape.n_kv_heads * shape.head_dim * 2 * 2  # K + V bytes per token per layer
     torch.cuda.set_device(0)
     weights = gpu_weights(shape)
     free_b, _ = torch.cuda.mem_get_info()
@@ -487,7 +523,7 @@ def run_multiturn(workload, segments, seg_steps, warmup):
     max_len = int(lens.max()) + int(sum(a.max() for a in adds)) + segments * seg_steps + warmup + 32
     log(f"{workload}: B={batch}, mean context {lens.mean():.0f}, pool {pool_bytes / 2**30:.1f} GiB")
     E = P.Engine(shape, weights, P.BF16, pool_bytes, max_seqs=batch, max_seq_len=max_len,
-                 max_batch=batch, max_chunk=2048)
+                 max_batch=batch, max_chunk=append_chunk)
     g = torch.Generator(device="cuda")
     g.manual_seed(3)
     pool_bf16 = E.kv_pool.view(torch.bfloat16)
@@ -500,7 +536,11 @@ def run_multiturn(workload, segments, seg_steps, warmup):
     tok = torch.randint(0, shape.vocab, (batch,), dtype=torch.int32, device="cuda", generator=g)
     logits = torch.empty((batch, shape.vocab), dtype=torch.float32, device="cuda")
     rng = np.random.default_rng(5)
-    dec_ms, dec_tokens, app_ms, app_tokens, departed = 0.0, 0, 0.0, 0, 0
+    dec_ms, dec_tokens, app_ms, app_tokens, app_flops, departed = 0.0, 0, 0.0, 0, 0.0, 0
+    dec_bytes = 0.0
+    seg_rows = []
+    attn_every = shape.n_layers + 1
+    w_bytes_b = {}
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     for seg in range(segments):
         idarr = np.array([ids[i] for i in live], dtype=np.int32)
@@ -508,16 +548,38 @@ def run_multiturn(workload, segments, seg_steps, warmup):
         for _ in range(warmup if seg == 0 else 0):
             E.decode_step(idarr, tok, logits)
             E.sample(logits, tok, batch=B)
+        ctx = np.array([E.kv_len(int(s)) for s in idarr], dtype=np.int64)
         torch.cuda.synchronize()
+        E.profile([N.TIMER_ATTENTION], every=attn_every)
         ev0.record()
         for _ in range(seg_steps):
             E.decode_step(idarr, tok, logits)
             E.sample(logits, tok, batch=B)
         ev1.record()
         torch.cuda.synchronize()
-        dec_ms += ev0.elapsed_time(ev1)
+        E.profile([])
+        ms = ev0.elapsed_time(ev1)
+        attn_ms, attn_n = E.profile_read(N.TIMER_ATTENTION)
+        # Keys read at step t: sum(ctx + t + 1); the mean over the segment.
+        mean_keys = float(np.sum(ctx)) + B * (seg_steps + 1) / 2.0
+        if B not in w_bytes_b:
+            w_bytes_b[B] = weight_bytes_per_step(shape, B)
+        step_bytes = (mean_keys * per_tok + B * per_tok + w_bytes_b[B]
+                      + 2 * B * shape.vocab * 4)
+        hbm = step_bytes / (ms / seg_steps / 1e3) / 1e9
+        attn_launch_bytes = mean_keys * kv_layer_tok
+        attn_avg_ms = attn_ms / max(attn_n, 1)
+        seg_rows.append({"segment": seg, "batch": B, "context_mean": round(float(ctx.mean()), 1),
+                         "ms_per_step": round(ms / seg_steps, 4),
+                         "tokens_per_s": round(B * seg_steps / (ms / 1e3), 1),
+                         "hbm_gbps": round(hbm, 1), "hbm_frac_of_peak": round(hbm / HBM_PEAK_GBS, 4),
+                         "attention_gbps": round(attn_launch_bytes / (attn_avg_ms / 1e3) / 1e9, 1),
+                         "attention_avg_launch_ms": round(attn_avg_ms, 5),
+                         "attention_launches": int(attn_n)})
+        dec_ms += ms
+        dec_bytes += step_bytes * seg_steps
         dec_tokens += B * seg_steps
-        log(f"segment {seg}: B={B}, {ev0.elapsed_time(ev1) / seg_steps:.2f} ms/step")
+        log(f"segment {seg}: B={B}, {ms / seg_steps:.2f} ms/step, {hbm:.0f} GB/s")
         if seg == segments - 1:
             break
         need = int(sum(adds[seg][i] for i in live)) + len(live) * (seg_steps + 32)
@@ -527,16 +589,25 @@ def run_multiturn(workload, segments, seg_steps, warmup):
             live.remove(longest)
             departed += 1
             need = int(sum(adds[seg][i] for i in live)) + len(live) * (seg_steps + 32)
+        toks = [rng.integers(0, shape.vocab, size=int(adds[seg][i]), dtype=np.int32) for i in live]
+        app_flops += sum(append_flops(shape, E.kv_len(ids[i]), len(t)) for i, t in zip(live, toks))
         torch.cuda.synchronize()
         ev0.record()
-        for i in live:
-            t = rng.integers(0, shape.vocab, size=int(adds[seg][i]), dtype=np.int32)
-            E.kv_append_prefix(ids[i], t, chunk_tokens=2048)
-            app_tokens += len(t)
+        if per_sequence_appends:
+            for i, t in zip(live, toks):
+                E.kv_append_prefix(ids[i], t, chunk_tokens=append_chunk)
+        else:
+            E.kv_append_prefix_batch([ids[i] for i in live], toks, chunk_tokens=append_chunk)
         ev1.record()
         torch.cuda.synchronize()
+        app_tokens += int(sum(len(t) for t in toks))
         app_ms += ev0.elapsed_time(ev1)
         log(f"append {seg}: {app_tokens} tokens so far, {ev0.elapsed_time(ev1):.0f} ms")
+    hbm_all = dec_bytes / (dec_ms / 1e3) / 1e9
+    # Attention roofline over all segments: bytes-weighted over the segments' launches.
+    a_bytes = sum(r["attention_gbps"] * r["attention_avg_launch_ms"] for r in seg_rows)
+    a_ms = sum(r["attention_avg_launch_ms"] for r in seg_rows)
+    attn_gbs = a_bytes / a_ms if a_ms else None
     out = {
         "metric": METRIC, "value": round(dec_tokens / (dec_ms / 1e3), 2), "unit": "tokens/s",
         "n_gpus": 1, "steps": segments * seg_steps, "warmup": warmup,
@@ -544,11 +615,26 @@ def run_multiturn(workload, segments, seg_steps, warmup):
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": workload, "batch": batch, "segments": segments,
                    "steps_per_segment": seg_steps, "append_tokens": "U[512, 2048] per trajectory",
+                   "append_call": ("kv_append_prefix per trajectory" if per_sequence_appends
+                                   else "kv_append_prefix_batch over the live trajectories"),
+                   "append_chunk_tokens": append_chunk,
                    "context_mean_initial": round(float(lens.mean()), 1),
                    "pool_tokens": int(pool_bytes // per_tok)},
+        "hbm_gbps": round(hbm_all, 1), "hbm_frac_of_peak": round(hbm_all / HBM_PEAK_GBS, 4),
+        "segments_detail": seg_rows,
+        "roofline": {"kernel": "attn_split_bf16<128>", "bound": "hbm",
+                     "achieved": round(attn_gbs, 1) if attn_gbs else None,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(attn_gbs / HBM_PEAK_GBS, 4) if attn_gbs else None,
+                     "traffic": None,
+                     "launch_sample": f"1 in {attn_every} attention launches of the decode "
+                                      "segments (layer rotating), bytes-weighted over segments"},
         "departed": departed, "final_batch": len(live),
         "append": {"tokens": int(app_tokens), "ms": round(app_ms, 1),
-                   "prefill_tokens_per_s": round(app_tokens / (app_ms / 1e3), 1) if app_ms else None},
+                   "prefill_tokens_per_s": round(app_tokens / (app_ms / 1e3), 1) if app_ms else None,
+                   "tflops_per_s": round(app_flops / (app_ms / 1e3) / 1e12, 1) if app_ms else None,
+                   "mfma_frac": round(app_flops / (app_ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+                   if app_ms else None},
         # decoded tokens over decode and append time together
         "end_to_end_tokens_per_s": round(dec_tokens / ((dec_ms + app_ms) / 1e3), 2),
         "cpu_baseline": None,
@@ -1079,6 +1165,12 @@ def main():
                     + ["kv-transfer-8b", "projections-8b", "landscape-8b", "sampling-8b",
                        "copy-1gib", "paced-rollout-8b", "attention-b64", "tiny-fp32"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seed", type=int, default=1,
+                    help="seed of the context-length draw of the decode workloads")
+    ap.add_argument("--append-per-sequence", action="store_true",
+                    help="multi-turn: one kv_append_prefix call per trajectory")
+    ap.add_argument("--append-chunk", type=int, default=2048,
+                    help="multi-turn: rows per prefill pass of the appends")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the decode engine is one worker's backend "
@@ -1102,10 +1194,13 @@ def main():
     elif args.workload == "paced-rollout-8b":
         out = run_paced_rollout()
     elif args.workload in MULTITURN:
-        out = run_multiturn(args.workload, segments=3, seg_steps=args.steps, warmup=args.warmup)
+        out = run_multiturn(args.workload, segments=3, seg_steps=args.steps, warmup=args.warmup,
+                            per_sequence_appends=args.append_per_sequence,
+                            append_chunk=args.append_chunk)
     else:
-        out = run_decode(args.workload, args.steps, args.warmup, not args.no_cpu_baseline)
-    out["host"] = {"cpu": platform.processor() or platform.machine(), "cpu_count": os.cpu_count()}
+        out = run_decode(args.workload, args.steps, args.warmup, not args.no_cpu_baseline,
+                         seed=args.seed)
+    out["host"] = {"cpu": cpu_model(), "cpu_count": os.cpu_count()}
     print(json.dumps(out), flush=True)
 
 

@@ -45,3 +45,15 @@ def test_prefill_flops_8b_magnitudes():
     n = 65536
     proj = 2.0 * n * EIGHT_B.n_layers * sum(r * c for r, c in _matrices(EIGHT_B))
     assert bench.prefill_flops(EIGHT_B, n) - proj > proj
+
+
+def test_append_flops_by_enumeration():
+    """Appending n tokens onto ctx0 cached ones: every new query sees the
+    cached keys and the new keys up to itself."""
+    for shape in (TINY, EIGHT_B):
+        macs_per_token = shape.n_layers * sum(r * c for r, c in _matrices(shape))
+        for ctx0, n in ((0, 5), (3, 1), (17, 4), (100, 9)):
+            pairs = sum(1 for q in range(ctx0, ctx0 + n) for k in range(ctx0 + n) if k <= q)
+            attn_macs = shape.n_layers * shape.n_q_heads * pairs * 2 * shape.head_dim
+            assert bench.append_flops(shape, ctx0, n) == 2 * (n * macs_per_token + attn_macs)
+        assert bench.append_flops(shape, 0, 12) == bench.prefill_flops(shape, 12)
