@@ -484,7 +484,7 @@ def append_flops(shape, ctx0, n):
 
 
 def run_multiturn(workload, segments, seg_steps, warmup, per_sequence_appends=False,
-                  append_chunk=2048):
+                  append_chunk=4096):
     """Decode segments with tool-output appends in between.
 
     Capacity: the pool takes what HBM leaves after weights and workspace.
@@ -1169,7 +1169,7 @@ def main():
                     help="seed of the context-length draw of the decode workloads")
     ap.add_argument("--append-per-sequence", action="store_true",
                     help="multi-turn: one kv_append_prefix call per trajectory")
-    ap.add_argument("--append-chunk", type=int, default=2048,
+    ap.add_argument("--append-chunk", type=int, default=4096,
                     help="multi-turn: rows per prefill pass of the appends")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:

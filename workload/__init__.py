@@ -122,6 +122,51 @@ def make_weights(shape: ModelShape, seed: int = 0, bf16: bool = False,
     return weights
 
 
+def make_weights_parallel(shape: ModelShape, seed: int = 0, bf16: bool = True,
+                          std: float = 0.02, threads: int = 16,
+                          chunk: int = 1 << 25) -> Dict[str, object]:
+    """The same layout and distributions as make_weights, drawn in parallel for
+    full-size models: every matrix is cut into chunks of ``chunk`` elements in
+    the fixed order of make_weights, and chunk i is filled by its own PCG64
+    stream ``SeedSequence(seed).spawn(...)[i]`` (N(0, std), float32, then bf16
+    RNE with ``bf16``) on a thread pool.  The values differ from
+    make_weights' (another stream layout) and do not depend on ``threads``."""
+    import concurrent.futures as cf
+    s = shape
+    dims = [("embed", s.vocab, s.d_model)]
+    for l in range(s.n_layers):
+        dims += [((l, "wq"), s.q_dim, s.d_model), ((l, "wk"), s.kv_dim, s.d_model),
+                 ((l, "wv"), s.kv_dim, s.d_model), ((l, "wo"), s.d_model, s.q_dim),
+                 ((l, "w_gate"), s.ffn_dim, s.d_model), ((l, "w_up"), s.ffn_dim, s.d_model),
+                 ((l, "w_down"), s.d_model, s.ffn_dim)]
+    dims.append(("lm_head", s.vocab, s.d_model))
+    mats = {key: np.empty((r, c), dtype=np.float32) for key, r, c in dims}
+    jobs = []
+    for key, r, c in dims:
+        flat = mats[key].reshape(-1)
+        for o in range(0, flat.size, chunk):
+            jobs.append(flat[o:o + chunk])
+    streams = np.random.SeedSequence(seed).spawn(len(jobs))
+
+    def fill(i):
+        out = jobs[i]
+        np.random.default_rng(streams[i]).standard_normal(out.size, dtype=np.float32, out=out)
+        out *= np.float32(std)
+        if bf16:
+            out[:] = round_to_bf16(out)
+
+    with cf.ThreadPoolExecutor(max_workers=threads) as ex:
+        list(ex.map(fill, range(len(jobs))))
+    weights: Dict[str, object] = {"embed": mats["embed"], "lm_head": mats["lm_head"],
+                                  "final_norm": np.ones(s.d_model, dtype=np.float32), "layers": []}
+    for l in range(s.n_layers):
+        lay = {k: mats[(l, k)] for k in layer_matrix_names()}
+        lay["attn_norm"] = np.ones(s.d_model, dtype=np.float32)
+        lay["ffn_norm"] = np.ones(s.d_model, dtype=np.float32)
+        weights["layers"].append(lay)
+    return weights
+
+
 def cached_kv(n_tokens: int, n_kv_heads: int, head_dim: int, seed: int, k_std: float = 1.0,
               bf16: bool = True):
     """Seeded K and V values of one layer's cache, ``[n_tokens][Hkv][Dh]`` each:
