@@ -36,6 +36,24 @@ __device__ __forceinline__ int kswz(int k, int p) {
   return (k & 3) | (((k >> 3) & 1) << 2) | (p << 3);  // < 16 chunks per 128-dim key row
 }
 
+// IEEE maximum: one v_maximum3_f32, with no canonicalising self-max on its
+// inputs as fmaxf needs.  Inputs here are finite scores or -inf (masked keys
+// are set to -inf before any maximum, so no NaN reaches it).
+__device__ __forceinline__ float max2(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
+// Maximum over the four lanes l, l^16, l^32, l^48 (the four key groups of a
+// score column) with the gfx950 cross-row swaps, which stay in the VALU:
+// a __shfl_xor would be an LDS permute whose wait also drains every LDS read
+// in flight.  Swapping a value with itself leaves rows (0,0,2,2) in one
+// result and (1,1,3,3) in the other (16-lane rows), or halves (0,0) and
+// (1,1) (32-lane halves), so their maximum is the xor-16 / xor-32 maximum.
+__device__ __forceinline__ float max_over_key_groups(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = max2(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return max2(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 template <int DH>  // 128
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_prefill_bf16(
     const AttnItem* __restrict__ items, const AttnQBlock* __restrict__ qblocks,
@@ -112,10 +130,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   // The stage's two page numbers are read with uniform indices (scalar
   // loads): a per-lane page-table read would be a vector load, and waiting
   // for it would also wait for every stage in flight (loads retire in order).
-  auto issue = [&](int st, int buf) {
+  // A missing second page reads a valid page whose keys are masked.
+  auto page_a_of = [&](int st) { return btrow[2 * st]; };
+  auto page_b_of = [&](int st) { return btrow[min(2 * st + 1, it.n_pages - 1)]; };
+  auto issue = [&](int page_a, int page_b, int buf) {
     uint16_t* base = stage_ptr(buf) + wave * 64 * 8;
-    const int page_a = btrow[2 * st];
-    const int page_b = btrow[min(2 * st + 1, it.n_pages - 1)];  // missing: a valid page, masked
     const int64_t base_a = (int64_t)page_a * page_stride + head_off;
     const int64_t base_b = (int64_t)page_b * page_stride + head_off;
 #pragma unroll
@@ -176,17 +195,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
       }
       // Raw scores; the scale (> 0) is applied to the max and inside the
       // exponent's FMA.  Masked keys are -inf, whose weight is exactly 0.
+      // The mask sits under a uniform branch: most stages need none, and a
+      // select merged with the open test would cost three VALU ops a score.
       float sv[8];
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
-        for (int rr = 0; rr < 4; ++rr)
-          sv[4 * u + rr] = (open || kbase + 4 * u + rr < row_lim[r]) ? s[u][rr] : -INFINITY;
-      float mloc = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
-                         fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-      const float m_new = fmaxf(m[r], mloc * scale_log2);
+        for (int rr = 0; rr < 4; ++rr) sv[4 * u + rr] = s[u][rr];
+      if (!open) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          sv[e] = (kbase + e < row_lim[r]) ? sv[e] : -INFINITY;
+      }
+      float mloc = max2(max2(max2(sv[0], sv[1]), sv[2]), max2(max2(sv[3], sv[4]), sv[5]));
+      mloc = max_over_key_groups(max2(max2(mloc, sv[6]), sv[7]));
+      const float m_new = max2(m[r], mloc * scale_log2);
       const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
       if (__any(m_new != m[r])) {
         const float alpha = __builtin_amdgcn_exp2f(m[r] - m_use);
@@ -230,28 +253,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   // loads in flight is fixed).  After the barrier of step st every wave has
   // finished step st-1, whose stage then takes step st+3.
 #pragma unroll
-  for (int b = 0; b < D - 1; ++b) issue(min(b, last), b);
+  for (int b = 0; b < D - 1; ++b) issue(page_a_of(min(b, last)), page_b_of(min(b, last)), b);
+  // Page numbers of the next stage to issue, read one step ahead so that the
+  // wait for the scalar loads (which also waits for LDS reads) finds them
+  // arrived.
+  int next_a = page_a_of(min(D - 1, last)), next_b = page_b_of(min(D - 1, last));
+  auto step = [&](int s, int b) {
+    wait_vmem<(D - 2) * LPT>();
+    wg_barrier();
+    issue(next_a, next_b, (b + D - 1) % D);  // stage min(s + D - 1, last)
+    next_a = page_a_of(min(s + D, last));
+    next_b = page_b_of(min(s + D, last));
+    __builtin_amdgcn_sched_barrier(0);
+    compute(s, b);
+  };
   int st = 0;
   for (; st + D <= n_st; st += D) {
 #pragma unroll
-    for (int b = 0; b < D; ++b) {
-      wait_vmem<(D - 2) * LPT>();
-      wg_barrier();
-      issue(min(st + b + D - 1, last), (b + D - 1) % D);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(st + b, b);
-    }
+    for (int b = 0; b < D; ++b) step(st + b, b);
   }
   const int tail = n_st - st;  // uniform over the work group
 #pragma unroll
   for (int b = 0; b < D; ++b)
-    if (b < tail) {
-      wait_vmem<(D - 2) * LPT>();
-      wg_barrier();
-      issue(min(st + b + D - 1, last), (b + D - 1) % D);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(st + b, b);
-    }
+    if (b < tail) step(st + b, b);
   wait_vmem<0>();  // no LDS write may still be in flight when the group ends
 
 #pragma unroll
