@@ -184,11 +184,10 @@ __attribute__((amdgpu_waves_per_eu(sizeof(KT) == 1 ? 2 : 3))) void attn_split_bf
         const int e = 4 * u + rr;
         const float x = (kbase + e < row_lim) ? s[u][rr] * scale_log2 : -INFINITY;
         sv[e] = x;
-        mloc = fmaxf(mloc, x);
+        mloc = max2(mloc, x);
       }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m, mloc);
+    mloc = max_over_key_groups(mloc);
+    const float m_new = max2(m, mloc);
     const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
     // Rescale only when some row's running max moved (wave-uniform test).
     if (__any(m_new != m)) {
@@ -282,8 +281,7 @@ __attribute__((amdgpu_waves_per_eu(sizeof(KT) == 1 ? 2 : 3))) void attn_split_bf
     }
   }
 
-  l += __shfl_xor(l, 16, 64);
-  l += __shfl_xor(l, 32, 64);
+  l = sum_over_key_groups(l);
   if constexpr (PW > 1) {
     // Page-split waves hand (m, l, acc) to wave 0, which merges them in wave
     // order with the online-softmax rule.

@@ -36,24 +36,6 @@ __device__ __forceinline__ int kswz(int k, int p) {
   return (k & 3) | (((k >> 3) & 1) << 2) | (p << 3);  // < 16 chunks per 128-dim key row
 }
 
-// IEEE maximum: one v_maximum3_f32, with no canonicalising self-max on its
-// inputs as fmaxf needs.  Inputs here are finite scores or -inf (masked keys
-// are set to -inf before any maximum, so no NaN reaches it).
-__device__ __forceinline__ float max2(float a, float b) { return __builtin_elementwise_maximum(a, b); }
-
-// Maximum over the four lanes l, l^16, l^32, l^48 (the four key groups of a
-// score column) with the gfx950 cross-row swaps, which stay in the VALU:
-// a __shfl_xor would be an LDS permute whose wait also drains every LDS read
-// in flight.  Swapping a value with itself leaves rows (0,0,2,2) in one
-// result and (1,1,3,3) in the other (16-lane rows), or halves (0,0) and
-// (1,1) (32-lane halves), so their maximum is the xor-16 / xor-32 maximum.
-__device__ __forceinline__ float max_over_key_groups(float v) {
-  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  v = max2(__uint_as_float(a[0]), __uint_as_float(a[1]));
-  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return max2(__uint_as_float(b[0]), __uint_as_float(b[1]));
-}
-
 template <int DH>  // 128
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_prefill_bf16(
     const AttnItem* __restrict__ items, const AttnQBlock* __restrict__ qblocks,

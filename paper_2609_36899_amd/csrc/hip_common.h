@@ -98,6 +98,34 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// IEEE maximum: one v_maximum3_f32, with no canonicalising self-max on its
+// inputs as fmaxf needs.  Callers pass finite scores or -inf (masked keys are
+// set to -inf before any maximum, so no NaN reaches it).
+__device__ __forceinline__ float max2(float a, float b) {
+  return __builtin_elementwise_maximum(a, b);
+}
+
+// Maximum and sum over the four lanes l, l^16, l^32, l^48 (the four key
+// groups of an MFMA score column) with the gfx950 cross-row swaps, which stay
+// in the VALU: a __shfl_xor is an LDS permute, and its wait also drains every
+// LDS read in flight.  Swapping a value with itself leaves 16-lane rows
+// (0,0,2,2) in one result and (1,1,3,3) in the other, or 32-lane halves (0,0)
+// and (1,1), so combining the two gives the xor-16 / xor-32 reduction; each
+// lane adds the same two operands as the shuffle form (in swapped order), so
+// the sum is bit-identical to it.
+__device__ __forceinline__ float max_over_key_groups(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = max2(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return max2(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float sum_over_key_groups(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // Sum over a work group of up to 1024 threads (multiple of 64).  `red` is
 // __shared__ scratch of at least blockDim.x / 64 floats.  All threads get it.
 __device__ __forceinline__ float block_sum(float v, float* red) {
