@@ -1088,14 +1088,15 @@ def prefill_flops(shape, n):
     return gemm + attn
 
 
-def run_kv_transfer(lengths=(4096, 16384, 65536)):
+def run_kv_transfer(lengths=(4096, 16384, 65536), chunk=4096):
     """Prepared KV versus re-prefill for one departing trajectory.
 
     For each context length: kv_export of the trajectory's KV into pinned
     host memory (device to host), kv_import into a fresh sequence (host to
-    device), and kv_append_prefix re-prefilling the same tokens.  This is
-    the prepared-transfer versus re-prefill trade-off of late-bound KV
-    preparation, on one GPU.
+    device), and kv_append_prefix re-prefilling the same tokens in passes of
+    `chunk` rows.  This is the prepared-transfer versus re-prefill trade-off
+    of late-bound KV preparation, on one GPU.  One untimed pass first loads
+    the kernels.
     """
     import torch
 
@@ -1108,15 +1109,19 @@ def run_kv_transfer(lengths=(4096, 16384, 65536)):
     weights = gpu_weights(shape)
     pool_tokens = 3 * max(lengths) + 4096
     E = P.Engine(shape, weights, P.BF16, pool_tokens * per_tok, max_seqs=8,
-                 max_seq_len=max(lengths) + 64, max_batch=8, max_chunk=2048)
+                 max_seq_len=max(lengths) + 64, max_batch=8, max_chunk=chunk)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    warm = E.kv_alloc(0)
+    E.kv_append_prefix(warm, random_tokens(chunk, shape.vocab, seed=1), chunk_tokens=chunk)
+    torch.cuda.synchronize()
+    E.kv_free(warm)
     rows = []
     for n in lengths:
         toks = random_tokens(n, shape.vocab, seed=n)
         a = E.kv_alloc(0)
         torch.cuda.synchronize()
         ev0.record()
-        E.kv_append_prefix(a, toks, chunk_tokens=2048)
+        E.kv_append_prefix(a, toks, chunk_tokens=chunk)
         ev1.record()
         torch.cuda.synchronize()
         prefill_ms = ev0.elapsed_time(ev1)
@@ -1150,7 +1155,8 @@ def run_kv_transfer(lengths=(4096, 16384, 65536)):
     return {"metric": "KV snapshot/restore vs re-prefill, 8B-shaped, 1 MI355X",
             "value": rows[-1]["reprefill_ms"] / rows[-1]["import_ms"], "unit": "x (re-prefill / import)",
             "n_gpus": 1, "higher_is_better": True, "data": "synthetic", "dtype": "bf16",
-            "config": {"workload": "kv-transfer-8b", "lengths": list(lengths)}, "rows": rows,
+            "config": {"workload": "kv-transfer-8b", "lengths": list(lengths),
+                       "chunk_tokens": chunk}, "rows": rows,
             "cpu_baseline": None}
 
 
@@ -1170,7 +1176,7 @@ def main():
     ap.add_argument("--append-per-sequence", action="store_true",
                     help="multi-turn: one kv_append_prefix call per trajectory")
     ap.add_argument("--append-chunk", type=int, default=4096,
-                    help="multi-turn: rows per prefill pass of the appends")
+                    help="rows per prefill pass: multi-turn appends and the kv-transfer re-prefill")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the decode engine is one worker's backend "
@@ -1178,7 +1184,7 @@ def main():
               "exchange).  Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
     if args.workload == "kv-transfer-8b":
-        out = run_kv_transfer()
+        out = run_kv_transfer(chunk=args.append_chunk)
     elif args.workload == "projections-8b":
         out = run_projections()
     elif args.workload == "landscape-8b":
