@@ -425,12 +425,16 @@ __global__ __launch_bounds__(512) void gemm_bf16_wide(int M, int N, int K, int k
     col_end = gw < n_groups ? gr.col_end : 0;  // a clamped second group writes nothing
   }
 
-  // A: chunk id = row * 4 + slot, holding source chunk slot ^ ((row >> 2) & 3).
+  // A: chunk id = row * 4 + slot, holding source chunk slot ^ ((row >> 1) & 3).
+  // A row is 64 bytes, so two rows share one 128-byte span of the banks; a
+  // fragment read (eight consecutive lanes = eight consecutive rows, one
+  // logical chunk) then lands on eight distinct 16-byte bank groups: even and
+  // odd rows take the two halves, and (row >> 1) & 3 spreads the four of each.
   const uint16_t* asrc[ACH];
 #pragma unroll
   for (int j = 0; j < ACH; ++j) {
     const int id = j * THREADS + tid, r = id >> 2, slot = id & 3;
-    asrc[j] = A + (int64_t)min(m_blk + r, M - 1) * lda + kbeg + ((slot ^ ((r >> 2) & 3)) * 8);
+    asrc[j] = A + (int64_t)min(m_blk + r, M - 1) * lda + kbeg + ((slot ^ ((r >> 1) & 3)) * 8);
   }
   // W: chunk id = (g2 * 8 + sp) * 64 + lane of staged group g2 (the wave
   // column that reads it), staged strip sp.
@@ -450,7 +454,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_wide(int M, int N, int K, int k
 #pragma unroll
   for (int t = 0; t < MT; ++t) {
     const int ra = wm * 64 + t * 16 + c16;
-    aoff[t] = ra * 32 + ((q4 ^ ((ra >> 2) & 3)) * 8);
+    aoff[t] = ra * 32 + ((q4 ^ ((ra >> 1) & 3)) * 8);
   }
 
   f32x4 acc[MT][NT];
