@@ -208,12 +208,22 @@ def stream_copy_gbs(n=1 << 30, iters=10):
             "gbps": round(2 * n / (ms / 1e3) / 1e9, 1), "kernel": "torch copy_ (uint8, 1 GiB)"}
 
 
-def file_hash(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+# The decode attention kernel's sources: its counters are reused only while
+# all of these are unchanged.
+ATTENTION_SOURCES = tuple(os.path.join(ROOT, "paper_2609_36899_amd", "csrc", f)
+                          for f in ("attention.hip", "hip_common.h", "fp8_e4m3.h"))
 
 
-def load_traffic(workload, kernel_src):
+def file_hash(*paths):
+    """First 16 hex digits of the SHA-256 of the files' contents, in order."""
+    h = hashlib.sha256()
+    for path in paths:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload, kernel_srcs=ATTENTION_SOURCES):
     """Counter-based HBM bytes per attention launch, if measured for this
     exact kernel source and workload (profiles/attention_traffic.json)."""
     path = os.path.join(ROOT, "profiles", "attention_traffic.json")
@@ -223,7 +233,7 @@ def load_traffic(workload, kernel_src):
         rec = json.load(open(path)).get(workload)
     except (OSError, ValueError):
         return None
-    if not rec or rec.get("kernel_sha256_16") != file_hash(kernel_src):
+    if not rec or rec.get("kernel_sha256_16") != file_hash(*kernel_srcs):
         return None
     return rec.get("bytes_per_launch")
 
@@ -423,8 +433,7 @@ def run_decode(workload, steps, warmup, with_cpu, seed=1):
     attn_bytes = mean_keys * shape.n_kv_heads * shape.head_dim * 2 * kv_elem  # per layer launch
     attn_avg_ms = attn_ms / max(attn_n, 1)
     attn_gbs = attn_bytes / (attn_avg_ms / 1e3) / 1e9
-    src = os.path.join(ROOT, "paper_2609_36899_amd", "csrc", "attention.hip")
-    traffic = load_traffic(workload, src)
+    traffic = load_traffic(workload)
     out = {
         "metric": METRIC, "value": round(tok_s, 2), "unit": "tokens/s", "n_gpus": 1,
         "steps": steps, "warmup": warmup, "ms_per_step": round(ms_step, 4),
