@@ -493,15 +493,15 @@ hipError_t launch_attention_split(int dtype, int kv_fp8, float k_scale, float v_
   } else {                                                                                   \
     if (rows_per_item == 64) PDEC_ATTN_BF16(64, 4, 1, KT_); else PDEC_ATTN_BF16(64, 1, 4, KT_); \
   }
-    // 128-row items: prefill with bf16 pages and 128-dim heads, the
+    // 128-row items: prefill with 128-dim heads (bf16 or E4M3 pages), the
     // LDS-staged prefill kernel.
-    if (rows_per_item == 128 && !kv_fp8 && head_dim == 128)
-      return launch_attention_prefill_bf16(n_items, n_q_heads, n_kv_heads, items, qblocks, q,
-                                           k_pages, v_pages, page_stride_elems, block_table,
-                                           bt_stride, scale_log2, part_ml, part_acc, stream,
-                                           ev_start, ev_stop);
-    // Other prefill (fp8 pages, 64-dim heads): waves split rows.  16-row
-    // items (decode): waves split pages.
+    if (rows_per_item == 128 && head_dim == 128)
+      return launch_attention_prefill_bf16(n_items, n_q_heads, n_kv_heads, kv_fp8, items,
+                                           qblocks, q, k_pages, v_pages, page_stride_elems,
+                                           block_table, bt_stride, scale_log2, v_scale, part_ml,
+                                           part_acc, stream, ev_start, ev_stop);
+    // Other prefill (64-dim heads): waves split rows.  16-row items
+    // (decode): waves split pages.
     if (kv_fp8) {
       PDEC_ATTN_KT(uint8_t)
     } else {

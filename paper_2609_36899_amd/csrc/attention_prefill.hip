@@ -36,13 +36,23 @@ __device__ __forceinline__ int kswz(int k, int p) {
   return (k & 3) | (((k >> 3) & 1) << 2) | (p << 3);  // < 16 chunks per 128-dim key row
 }
 
-template <int DH>  // 128
+//
+// Pages of E4M3 codes (KT = uint8_t) are staged through registers instead:
+// after the barrier each thread loads the 8-byte code chunks of its four LDS
+// chunks of the next stage, and after the stage's compute it converts them to
+// bf16 (exact: every E4M3 value is a bf16 value) and writes them where the
+// DMA would have put the bf16 chunks.  Each code is converted once per work
+// group rather than once per wave, and the compute is the bf16 one.  The K
+// scale is folded into scale_log2 by the caller; the V scale multiplies the
+// partial output once.
+template <int DH, typename KT>  // DH = 128; KT = uint16_t (bf16 pages) or uint8_t (E4M3 codes)
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_prefill_bf16(
     const AttnItem* __restrict__ items, const AttnQBlock* __restrict__ qblocks,
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kpool,
-    const uint16_t* __restrict__ vpool, int64_t page_stride, const int32_t* __restrict__ bt,
-    int32_t bt_stride, int32_t n_q_heads, int32_t n_kv_heads, float scale_log2,
+    const uint16_t* __restrict__ q, const KT* __restrict__ kpool,
+    const KT* __restrict__ vpool, int64_t page_stride, const int32_t* __restrict__ bt,
+    int32_t bt_stride, int32_t n_q_heads, int32_t n_kv_heads, float scale_log2, float v_scale,
     float* __restrict__ part_ml, float* __restrict__ part_acc) {
+  constexpr bool kFp8 = sizeof(KT) == 1;
   constexpr int KC = DH / 32;   // k-steps of QK^T
   constexpr int DT = DH / 16;   // 16-wide dim tiles of PV
   constexpr int RT = 2;         // 16-row tiles per wave
@@ -123,6 +133,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     for (int j = 0; j < LPT; ++j)
       dma16((j < 2 ? kpool : vpool) + ((j & 1) ? base_b : base_a) + src_off[j],
             base + j * 256 * 8);
+  };
+  // E4M3 pages: the codes of chunk j of a stage (8 bytes), then their bf16
+  // values into LDS chunk j * 256 + tid, as the DMA would place them.
+  u32x2 codes[LPT];
+  auto load_codes = [&](int page_a, int page_b) {
+    const int64_t base_a = (int64_t)page_a * page_stride + head_off;
+    const int64_t base_b = (int64_t)page_b * page_stride + head_off;
+#pragma unroll
+    for (int j = 0; j < LPT; ++j)
+      codes[j] = load_stream<u32x2>((j < 2 ? kpool : vpool) + ((j & 1) ? base_b : base_a) +
+                                    src_off[j]);
+  };
+  auto store_codes = [&](int buf) {
+    uint16_t* base = stage_ptr(buf) + tid * 8;
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) *(bf16x8*)(base + j * 256 * 8) = e4m3x8_to_bf16(codes[j]);
   };
 
   // Lane-constant fragment offsets (as in the split kernel).
@@ -235,19 +261,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   // loads in flight is fixed).  After the barrier of step st every wave has
   // finished step st-1, whose stage then takes step st+3.
 #pragma unroll
-  for (int b = 0; b < D - 1; ++b) issue(page_a_of(min(b, last)), page_b_of(min(b, last)), b);
+  for (int b = 0; b < D - 1; ++b) {
+    if constexpr (kFp8) {
+      load_codes(page_a_of(min(b, last)), page_b_of(min(b, last)));
+      store_codes(b);
+    } else {
+      issue(page_a_of(min(b, last)), page_b_of(min(b, last)), b);
+    }
+  }
   // Page numbers of the next stage to issue, read one step ahead so that the
   // wait for the scalar loads (which also waits for LDS reads) finds them
   // arrived.
   int next_a = page_a_of(min(D - 1, last)), next_b = page_b_of(min(D - 1, last));
   auto step = [&](int s, int b) {
-    wait_vmem<(D - 2) * LPT>();
-    wg_barrier();
-    issue(next_a, next_b, (b + D - 1) % D);  // stage min(s + D - 1, last)
+    if constexpr (kFp8) {
+      wait_lds();  // this wave's stage writes of the previous step
+      wg_barrier();
+      load_codes(next_a, next_b);  // stage min(s + D - 1, last)
+    } else {
+      wait_vmem<(D - 2) * LPT>();
+      wg_barrier();
+      issue(next_a, next_b, (b + D - 1) % D);  // stage min(s + D - 1, last)
+    }
     next_a = page_a_of(min(s + D, last));
     next_b = page_b_of(min(s + D, last));
     __builtin_amdgcn_sched_barrier(0);
     compute(s, b);
+    // The stage of step s - 1, free since this step's barrier.
+    if constexpr (kFp8) store_codes((b + D - 1) % D);
   };
   int st = 0;
   for (; st + D <= n_st; st += D) {
@@ -259,6 +300,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   for (int b = 0; b < D; ++b)
     if (b < tail) step(st + b, b);
   wait_vmem<0>();  // no LDS write may still be in flight when the group ends
+  if constexpr (kFp8) {
+    wait_lds();
+#pragma unroll
+    for (int r = 0; r < RT; ++r)
+#pragma unroll
+      for (int t = 0; t < DT; ++t) acc[r][t] *= v_scale;
+  }
 
 #pragma unroll
   for (int r = 0; r < RT; ++r) {
@@ -369,18 +417,24 @@ hipError_t launch_attention_combine_rows(int head_dim, int rows_per_item, int n_
   return hipGetLastError();
 }
 
-hipError_t launch_attention_prefill_bf16(int n_items, int n_q_heads, int n_kv_heads,
+hipError_t launch_attention_prefill_bf16(int n_items, int n_q_heads, int n_kv_heads, int kv_fp8,
                                          const AttnItem* items, const AttnQBlock* qblocks,
                                          const void* q, const void* k_pages, const void* v_pages,
                                          int64_t page_stride_elems, const int32_t* block_table,
-                                         int32_t bt_stride, float scale_log2, float* part_ml,
-                                         float* part_acc, hipStream_t stream, hipEvent_t ev_start,
-                                         hipEvent_t ev_stop) {
+                                         int32_t bt_stride, float scale_log2, float v_scale,
+                                         float* part_ml, float* part_acc, hipStream_t stream,
+                                         hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (n_items == 0) return hipSuccess;
-  return launch_timed(attn_prefill_bf16<128>, dim3(n_kv_heads, n_items), dim3(256), stream,
-                      ev_start, ev_stop, items, qblocks, (const uint16_t*)q,
+  if (kv_fp8)
+    return launch_timed(attn_prefill_bf16<128, uint8_t>, dim3(n_kv_heads, n_items), dim3(256),
+                        stream, ev_start, ev_stop, items, qblocks, (const uint16_t*)q,
+                        (const uint8_t*)k_pages, (const uint8_t*)v_pages, page_stride_elems,
+                        block_table, bt_stride, n_q_heads, n_kv_heads, scale_log2, v_scale,
+                        part_ml, part_acc);
+  return launch_timed(attn_prefill_bf16<128, uint16_t>, dim3(n_kv_heads, n_items), dim3(256),
+                      stream, ev_start, ev_stop, items, qblocks, (const uint16_t*)q,
                       (const uint16_t*)k_pages, (const uint16_t*)v_pages, page_stride_elems,
-                      block_table, bt_stride, n_q_heads, n_kv_heads, scale_log2, part_ml,
+                      block_table, bt_stride, n_q_heads, n_kv_heads, scale_log2, 1.f, part_ml,
                       part_acc);
 }
 

@@ -211,9 +211,9 @@ constexpr int kMaxPiecesPerPass = 64;
 // Query rows per attention work item: decode (one wave) and prefill (four).
 constexpr int kDecodeRows = 16;
 // Query rows per prefill block: 128 for the LDS-staged prefill kernel (bf16
-// pages, 128-dim heads), 64 for the others.
+// activations, 128-dim heads; bf16 or E4M3 pages), 64 for the others.
 int prefill_rows(const pdec_model_cfg& c) {
-  return (c.dtype == PDEC_BF16 && !c.kv_fp8 && c.head_dim == 128) ? 128 : 64;
+  return (c.dtype == PDEC_BF16 && c.head_dim == 128) ? 128 : 64;
 }
 
 int check_cfg(const pdec_model_cfg* c) {

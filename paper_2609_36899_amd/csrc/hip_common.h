@@ -51,6 +51,12 @@ __device__ __forceinline__ void wait_vmem() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// Wait until this wave's LDS (and scalar memory) operations have completed,
+// leaving the vector-memory counter alone.
+__device__ __forceinline__ void wait_lds() {
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+}
+
 // Work-group barrier without the fence of __syncthreads, whose release would
 // wait for every load in flight (LDS-DMA loads included).  Callers order
 // their memory with explicit counter waits; the empty asm statements keep

@@ -219,18 +219,21 @@ def test_bf16_8b_geometry_two_layers_parity():
     _bf16_parity(shape, seed=6, prefix_lens=[9, 33, 48, 20], n_steps=4, chunk=32)
 
 
+@pytest.mark.parametrize("kv_fp8", [None, (0.5, 0.25)])
 @pytest.mark.parametrize("n_kv_heads", [16, 4])
-def test_bf16_long_prefill_items(n_kv_heads):
+def test_bf16_long_prefill_items(n_kv_heads, kv_fp8):
     """Prefill attention over long items: with 16 query heads of 128 dims the
     planner cuts each query block's keys into items of 10-56 pages (5-28
     two-page stages) and 5-8 items per block, so the prefill kernel's
     four-stage LDS ring wraps several times and the row-split merge sees
     several items per row; chunks of 1000 tokens start mid-page and the last
-    item of a block can have an odd page count.  G = 1 and G = 4."""
+    item of a block can have an odd page count.  G = 1 and G = 4; bf16 pages,
+    and E4M3 pages (staged through registers and converted into the same LDS
+    layout; K and V scales other than 1)."""
     shape = ModelShape(n_layers=1, d_model=256, n_q_heads=16, n_kv_heads=n_kv_heads,
                        head_dim=128, ffn_dim=256, vocab=512)
     _bf16_parity(shape, seed=12, prefix_lens=[4000, 1531], n_steps=2, chunk=1000,
-                 pool_tokens=6144, max_seq_len=4096)
+                 kv_fp8=kv_fp8, pool_tokens=6144, max_seq_len=4096)
 
 
 @pytest.mark.parametrize("ffn", [8256, 14336])
