@@ -1097,7 +1097,7 @@ def prefill_flops(shape, n):
     return gemm + attn
 
 
-def run_kv_transfer(lengths=(4096, 16384, 65536), chunk=4096):
+def run_kv_transfer(lengths=(4096, 16384, 65536), chunk=4096, kv_fp8=None):
     """Prepared KV versus re-prefill for one departing trajectory.
 
     For each context length: kv_export of the trajectory's KV into pinned
@@ -1105,7 +1105,7 @@ def run_kv_transfer(lengths=(4096, 16384, 65536), chunk=4096):
     device), and kv_append_prefix re-prefilling the same tokens in passes of
     `chunk` rows.  This is the prepared-transfer versus re-prefill trade-off
     of late-bound KV preparation, on one GPU.  One untimed pass first loads
-    the kernels.
+    the kernels.  kv_fp8 = (k_scale, v_scale) stores the pages as E4M3 codes.
     """
     import torch
 
@@ -1113,12 +1113,12 @@ def run_kv_transfer(lengths=(4096, 16384, 65536), chunk=4096):
     from workload import EIGHT_B, random_tokens
 
     shape = EIGHT_B
-    per_tok = P.kv_bytes_per_token(shape, P.BF16)
+    per_tok = P.kv_bytes_per_token(shape, P.BF16, kv_fp8)
     torch.cuda.set_device(0)
     weights = gpu_weights(shape)
     pool_tokens = 3 * max(lengths) + 4096
     E = P.Engine(shape, weights, P.BF16, pool_tokens * per_tok, max_seqs=8,
-                 max_seq_len=max(lengths) + 64, max_batch=8, max_chunk=chunk)
+                 max_seq_len=max(lengths) + 64, max_batch=8, max_chunk=chunk, kv_fp8=kv_fp8)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     warm = E.kv_alloc(0)
     E.kv_append_prefix(warm, random_tokens(chunk, shape.vocab, seed=1), chunk_tokens=chunk)
@@ -1164,8 +1164,9 @@ def run_kv_transfer(lengths=(4096, 16384, 65536), chunk=4096):
     return {"metric": "KV snapshot/restore vs re-prefill, 8B-shaped, 1 MI355X",
             "value": rows[-1]["reprefill_ms"] / rows[-1]["import_ms"], "unit": "x (re-prefill / import)",
             "n_gpus": 1, "higher_is_better": True, "data": "synthetic", "dtype": "bf16",
-            "config": {"workload": "kv-transfer-8b", "lengths": list(lengths),
-                       "chunk_tokens": chunk}, "rows": rows,
+            "config": {"workload": "kv-transfer-8b" + ("-fp8kv" if kv_fp8 else ""),
+                       "lengths": list(lengths), "chunk_tokens": chunk,
+                       "kv_pages": "fp8 e4m3, scales 1" if kv_fp8 else "bf16"}, "rows": rows,
             "cpu_baseline": None}
 
 
@@ -1177,7 +1178,7 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
                     choices=sorted(WORKLOADS) + sorted(FP8_KV) + sorted(QK_NORM)
                     + sorted(MULTITURN)
-                    + ["kv-transfer-8b", "projections-8b", "landscape-8b", "sampling-8b",
+                    + ["kv-transfer-8b", "kv-transfer-8b-fp8kv", "projections-8b", "landscape-8b", "sampling-8b",
                        "copy-1gib", "paced-rollout-8b", "attention-b64", "tiny-fp32"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=1,
@@ -1194,6 +1195,8 @@ def main():
         sys.exit(2)
     if args.workload == "kv-transfer-8b":
         out = run_kv_transfer(chunk=args.append_chunk)
+    elif args.workload == "kv-transfer-8b-fp8kv":
+        out = run_kv_transfer(chunk=args.append_chunk, kv_fp8=(1.0, 1.0))
     elif args.workload == "projections-8b":
         out = run_projections()
     elif args.workload == "landscape-8b":
