@@ -489,19 +489,21 @@ hipError_t launch_attention_split(int dtype, int kv_fp8, float k_scale, float v_
                       n_q_heads, n_kv_heads, scale_log2, v_scale, part_ml, part_acc)
 #define PDEC_ATTN_KT(KT_)                                                                    \
   if (head_dim == 128) {                                                                     \
-    if (rows_per_item == 64) PDEC_ATTN_BF16(128, 4, 1, KT_); else PDEC_ATTN_BF16(128, 1, 4, KT_); \
+    PDEC_ATTN_BF16(128, 1, 4, KT_);                                                          \
   } else {                                                                                   \
     if (rows_per_item == 64) PDEC_ATTN_BF16(64, 4, 1, KT_); else PDEC_ATTN_BF16(64, 1, 4, KT_); \
   }
-    // 128-row items: prefill with 128-dim heads (bf16 or E4M3 pages), the
-    // LDS-staged prefill kernel.
-    if (rows_per_item == 128 && head_dim == 128)
+    // Prefill with 128-dim heads (128-row items, bf16 or E4M3 pages): the
+    // LDS-staged prefill kernel.  Prefill with 64-dim heads (64-row items):
+    // the split kernel with waves splitting rows.  Decode (16-row items):
+    // the split kernel with waves splitting pages.
+    if (head_dim == 128 && rows_per_item == 128)
       return launch_attention_prefill_bf16(n_items, n_q_heads, n_kv_heads, kv_fp8, items,
                                            qblocks, q, k_pages, v_pages, page_stride_elems,
                                            block_table, bt_stride, scale_log2, v_scale, part_ml,
                                            part_acc, stream, ev_start, ev_stop);
-    // Other prefill (64-dim heads): waves split rows.  16-row items
-    // (decode): waves split pages.
+    const bool rows_ok = rows_per_item == 16 || (head_dim == 64 && rows_per_item == 64);
+    if (!rows_ok || (head_dim != 128 && head_dim != 64)) return hipErrorInvalidValue;
     if (kv_fp8) {
       PDEC_ATTN_KT(uint8_t)
     } else {
