@@ -8,7 +8,9 @@ float64 oracle, through the C ABI.
   normwise 2e-2;
 * the Qwen3-style per-head q/k norm variant, fp32 (Dh 64) and bf16 (Dh 128);
 * chunking, re-prefill after departure, batch-order invariance and atomic
-  failure of page growth.
+  failure of page growth;
+* the prefill and decode attention kernels against each other over identical
+  pages (bf16 and E4M3).
 """
 
 import numpy as np
@@ -261,6 +263,57 @@ def test_decode_many_items_per_sequence(kv_fp8):
     shape, bf16 and fp8 pages."""
     _bf16_parity(ModelShape(**LONG_G4), seed=14, prefix_lens=[3000, 700, 17], n_steps=3,
                  chunk=1024, kv_fp8=kv_fp8, pool_tokens=4096, max_seq_len=4096)
+
+
+# Two attention kernels over the same pages: summation orders and item splits
+# differ, every other step of the two paths is bitwise the same.  Where the
+# two float32 attention outputs straddle a bf16 rounding boundary they differ
+# by one bf16 step (2^-8 relative), which the one-layer model carries into
+# the logits (measured 2.4e-3 to 3.3e-3 of max|logit|, 0 for a single item).
+KERNEL_PAIR_TOL = 1e-2
+
+
+@pytest.mark.parametrize("kv_fp8", [None, (0.5, 0.25)])
+def test_prefill_attention_equals_decode_attention(kv_fp8):
+    """The LDS-staged prefill kernel against the decode split kernel over the
+    same cached pages.  Each trajectory's prefix (17 to 3001 tokens) is
+    prefilled once and copied by snapshot/restore into a second sequence, so
+    the two hold identical pages (bf16 values or E4M3 codes).  The next token
+    goes through decode_step for one copy (decode attention, 16-row items,
+    split merge) and through kv_append_prefix_batch as a one-row piece for
+    the other (prefill attention, 128-row items, row-split merge).  Both paths
+    run the same four-row projections, so q, k, v and the new pages are
+    bitwise the same, and the logits differ only by the attention kernels'
+    summation orders and item splits: 1e-2 of max|logit| per row, against
+    the oracle bars of 2e-2 (bf16) and 6e-2 (fp8)."""
+    shape = ModelShape(**LONG_G4)
+    arrays = make_weights(shape, seed=16, bf16=True)
+    lens = [17, 300, 1500, 3001]
+    E = _engine(shape, arrays, bf16=True, pool_tokens=2 * sum(lens) + 4096, max_seq_len=4096,
+                max_chunk=1024, kv_fp8=kv_fp8)
+    toks = [random_tokens(n + 1, shape.vocab, seed=70 + i) for i, n in enumerate(lens)]
+    dec, pre = [], []
+    for t, n in zip(toks, lens):
+        a = E.kv_alloc(0)
+        E.kv_append_prefix(a, t[:n], chunk_tokens=1024)
+        snap = torch.empty(E.kv_snapshot_bytes(n), dtype=torch.uint8).pin_memory()
+        assert E.kv_export(a, snap) == n
+        torch.cuda.synchronize()
+        b = E.kv_alloc(0)
+        E.kv_import(b, snap, n)
+        dec.append(a)
+        pre.append(b)
+    nxt = np.array([t[n] for t, n in zip(toks, lens)], dtype=np.int32)
+    out_dec = _logits_buf(len(lens), shape.vocab)
+    E.decode_step(dec, torch.from_numpy(nxt).cuda(), out_dec)
+    out_pre = _logits_buf(len(lens), shape.vocab)
+    E.kv_append_prefix_batch(pre, [[int(x)] for x in nxt], chunk_tokens=1024, last_logits=out_pre)
+    got_dec, got_pre = out_dec.cpu().numpy(), out_pre.cpu().numpy()
+    assert np.isfinite(got_dec).all() and np.isfinite(got_pre).all()
+    for r in range(len(lens)):
+        err = float(np.max(np.abs(got_dec[r] - got_pre[r])))
+        assert err <= KERNEL_PAIR_TOL * float(np.max(np.abs(got_dec[r]))), (r, lens[r], err)
+    E.close()
 
 
 def test_decode_many_items_batch_order_is_bitwise_invariant():
