@@ -7,10 +7,12 @@ departed, in a 30-page pool, so that freed pages and sequence slots are
 reused many times over.  Operations that do not fit the pool must fail with
 OUT_OF_PAGES and leave every trajectory as it was; a departed trajectory's id
 must be refused afterwards.  Every logits row the engine returns is compared
-with the oracle's recompute over that trajectory's whole token history (tiny
-fp32 decoder, 1e-4 as in the other fp32 parity tests).  This drives the host
-bookkeeping (free list, slot reuse, pending block-table entries, work lists,
-undo on failure) and the kernels together.
+with the oracle's recompute over that trajectory's whole token history: the
+tiny fp32 decoder within 1e-4, and a bf16 decoder with 128-dim heads (GQA
+groups of 4: the LDS-staged prefill kernel) within the bf16 bars of the other
+parity tests, 2e-2 of max|logit| with bf16 pages and 6e-2 with E4M3 pages.
+This drives the host bookkeeping (free list, slot reuse, pending block-table
+entries, work lists, undo on failure) and the kernels together.
 """
 
 import numpy as np
@@ -18,36 +20,47 @@ import pytest
 import torch
 
 from oracle import decoder as od
-from workload import TINY, make_weights
+from workload import TINY, ModelShape, make_weights
 
 pytestmark = pytest.mark.gpu
 
-F32_TOL = 1e-4
 MAX_SEQS = 6
 MAX_SEQ_LEN = 512
+# One layer, d 256, 8 query heads and 2 KV heads of 128 dims.
+BF16_G4 = ModelShape(n_layers=1, d_model=256, n_q_heads=8, n_kv_heads=2, head_dim=128,
+                     ffn_dim=256, vocab=512)
 
 
-def test_random_lifecycle_matches_oracle():
+@pytest.mark.parametrize("case", ["fp32", "bf16", "bf16-fp8kv"])
+def test_random_lifecycle_matches_oracle(case):
     import paper_2609_36899_amd as P
     from paper_2609_36899_amd import _native as N
 
+    bf16 = case != "fp32"
+    shape = BF16_G4 if bf16 else TINY
+    kv_fp8 = (0.5, 0.25) if case == "bf16-fp8kv" else None
+    dt = P.BF16 if bf16 else P.F32
+    # fp32: absolute; bf16: relative to max|ref| per row
+    tol = {"fp32": 1e-4, "bf16": 2e-2, "bf16-fp8kv": 6e-2}[case]
     rng = np.random.default_rng(2024)
-    arrays = make_weights(TINY, seed=30)
-    w64 = od.ModelWeights.from_arrays(TINY, arrays)
-    per_tok = P.kv_bytes_per_token(TINY, P.F32)
-    E = P.Engine(TINY, P.weights_to_device(arrays, P.F32), P.F32, 480 * per_tok,
-                 max_seqs=MAX_SEQS, max_seq_len=MAX_SEQ_LEN, max_batch=MAX_SEQS, max_chunk=48)
+    arrays = make_weights(shape, seed=30, bf16=bf16)
+    w64 = od.ModelWeights.from_arrays(shape, arrays)
+    per_tok = P.kv_bytes_per_token(shape, dt, kv_fp8)
+    E = P.Engine(shape, P.weights_to_device(arrays, dt), dt, 480 * per_tok,
+                 max_seqs=MAX_SEQS, max_seq_len=MAX_SEQ_LEN, max_batch=MAX_SEQS, max_chunk=48,
+                 kv_fp8=kv_fp8)
     hist = {}  # live sequence id -> its token history
-    buf = torch.empty((MAX_SEQS, TINY.vocab), dtype=torch.float32, device="cuda")
+    buf = torch.empty((MAX_SEQS, shape.vocab), dtype=torch.float32, device="cuda")
     counts = dict(checks=0, out_of_pages=0, moves=0, departures=0)
 
     def draw(n):
-        return [int(x) for x in rng.integers(0, TINY.vocab, n)]
+        return [int(x) for x in rng.integers(0, shape.vocab, n)]
 
     def check(seq, row):
-        ref = od.recompute_logits(w64, hist[seq])[-1]
+        ref = od.recompute_logits(w64, hist[seq], kv_fp8=kv_fp8)[-1]
         err = float(np.max(np.abs(row - ref)))
-        assert err <= F32_TOL, (seq, len(hist[seq]), err)
+        bound = tol * (float(np.max(np.abs(ref))) if bf16 else 1.0)
+        assert np.isfinite(row).all() and err <= bound, (seq, len(hist[seq]), err, bound)
         counts["checks"] += 1
 
     def lens_unchanged():
