@@ -36,7 +36,6 @@ __device__ __forceinline__ int kswz(int k, int p) {
   return (k & 3) | (((k >> 3) & 1) << 2) | (p << 3);  // < 16 chunks per 128-dim key row
 }
 
-//
 // Pages of E4M3 codes (KT = uint8_t) are staged through registers instead:
 // after the barrier each thread loads the 8-byte code chunks of its four LDS
 // chunks of the next stage, and after the stage's compute it converts them to
