@@ -27,6 +27,13 @@
  *     against the pool, and pending block-table entries (range, and no entry
  *     written twice).  A failed check returns PDEC_INVALID_ARG ("validate:
  *     ...") with nothing enqueued.  Off by default (host cost per call).
+ *   - Prefill with bf16 activations and 128-dim heads groups query rows in
+ *     blocks of 128 (work groups of four waves); a pass whose blocks read
+ *     long key ranges (on average at least 1024 pages, 16K keys, per
+ *     128-row block) takes 256-row blocks (eight waves sharing each staged
+ *     page).  PDEC_PREFILL_WIDE_PAGES=<pages> before engine_create sets that
+ *     threshold for the engine (0: always 256-row blocks).  Results agree to
+ *     float32 summation order either way.
  *   - Device memory (weights, KV pool, workspace, tokens, logits) is owned by
  *     the caller and must outlive the engine.  The library owns host metadata
  *     and a small pinned staging ring only.

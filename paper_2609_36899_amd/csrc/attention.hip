@@ -493,13 +493,13 @@ hipError_t launch_attention_split(int dtype, int kv_fp8, float k_scale, float v_
   } else {                                                                                   \
     if (rows_per_item == 64) PDEC_ATTN_BF16(64, 4, 1, KT_); else PDEC_ATTN_BF16(64, 1, 4, KT_); \
   }
-    // Prefill with 128-dim heads (128-row items, bf16 or E4M3 pages): the
-    // LDS-staged prefill kernel.  Prefill with 64-dim heads (64-row items):
-    // the split kernel with waves splitting rows.  Decode (16-row items):
-    // the split kernel with waves splitting pages.
-    if (head_dim == 128 && rows_per_item == 128)
-      return launch_attention_prefill_bf16(n_items, n_q_heads, n_kv_heads, kv_fp8, items,
-                                           qblocks, q, k_pages, v_pages, page_stride_elems,
+    // Prefill with 128-dim heads (128- or 256-row items, bf16 or E4M3 pages):
+    // the LDS-staged prefill kernel.  Prefill with 64-dim heads (64-row
+    // items): the split kernel with waves splitting rows.  Decode (16-row
+    // items): the split kernel with waves splitting pages.
+    if (head_dim == 128 && (rows_per_item == 128 || rows_per_item == 256))
+      return launch_attention_prefill_bf16(n_items, rows_per_item, n_q_heads, n_kv_heads, kv_fp8,
+                                           items, qblocks, q, k_pages, v_pages, page_stride_elems,
                                            block_table, bt_stride, scale_log2, v_scale, part_ml,
                                            part_acc, stream, ev_start, ev_stop);
     const bool rows_ok = rows_per_item == 16 || (head_dim == 64 && rows_per_item == 64);

@@ -44,8 +44,13 @@ __device__ __forceinline__ int kswz(int k, int p) {
 // group rather than once per wave, and the compute is the bf16 one.  The K
 // scale is folded into scale_log2 by the caller; the V scale multiplies the
 // partial output once.
-template <int DH, typename KT>  // DH = 128; KT = uint16_t (bf16 pages) or uint8_t (E4M3 codes)
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_prefill_bf16(
+//
+// WAVES = 4 takes 128-row blocks (two work groups per CU).  WAVES = 8 takes
+// 256-row blocks: the same stages then feed twice the MFMA work, which halves
+// the load work (DMA issue and LDS writes) per flop; the engine picks it for
+// passes whose blocks read long key ranges, where that work weighs most.
+template <int DH, typename KT, int WAVES>  // DH = 128; KT = uint16_t (bf16) or uint8_t (E4M3)
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(2))) void attn_prefill_bf16(
     const AttnItem* __restrict__ items, const AttnQBlock* __restrict__ qblocks,
     const uint16_t* __restrict__ q, const KT* __restrict__ kpool,
     const KT* __restrict__ vpool, int64_t page_stride, const int32_t* __restrict__ bt,
@@ -55,14 +60,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   constexpr int KC = DH / 32;   // k-steps of QK^T
   constexpr int DT = DH / 16;   // 16-wide dim tiles of PV
   constexpr int RT = 2;         // 16-row tiles per wave
-  constexpr int R = 64 * RT;    // query rows per item
+  constexpr int THREADS = 64 * WAVES;
+  constexpr int R = 16 * RT * WAVES;  // query rows per item
   constexpr int BLK = kPage * DH;          // elements of one page's K (or V^T) block
   constexpr int STAGE = 4 * BLK;           // K0 K1 V0 V1
   constexpr int CPK = DH / 8;              // 16-byte chunks per K row
-  constexpr int LPT = STAGE * 2 / 16 / 256;  // DMA loads per thread per stage
+  constexpr int LPT = STAGE * 2 / 16 / THREADS;  // DMA loads per thread per stage
   constexpr int D = 4;
   static_assert(DH == 128, "the K swizzle spans 16 chunks per key row");
-  static_assert(LPT * 256 * 8 == STAGE, "stage is a whole number of loads");
+  static_assert(WAVES == 4 || WAVES == 8, "128- or 256-row blocks");
+  static_assert(LPT * THREADS * 8 == STAGE, "stage is a whole number of loads");
   __shared__ __attribute__((aligned(16))) uint16_t st0[STAGE];
   __shared__ __attribute__((aligned(16))) uint16_t st1[STAGE];
   __shared__ __attribute__((aligned(16))) uint16_t st2[STAGE];
@@ -106,16 +113,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
   const int n_st = (it.n_pages + 1) >> 1;
   const int last = n_st - 1;
 
-  // DMA: load j of a stage fills chunks j*256 + tid: block j (K page 0,
-  // K page 1, V page 0, V page 1), chunk tid.
-  int src_off[LPT];
+  // DMA: load j of a stage fills chunk id = j * THREADS + tid of the stage,
+  // i.e. chunk id & 255 of block id >> 8 (K page 0, K page 1, V page 0,
+  // V page 1).  With four waves load j fills block j; with eight, blocks 2j
+  // and 2j + 1 (the block is uniform over a wave).
+  int src_off[LPT], src_blk[LPT];
 #pragma unroll
   for (int j = 0; j < LPT; ++j) {
-    if (j < 2) {
-      const int k = tid / CPK, slot = tid % CPK;
-      src_off[j] = k * DH + ((slot ^ kswz(k, j)) * 8);
+    const int blk = j * (WAVES / 4) + (WAVES == 8 ? (tid >> 8) : 0), c = tid & 255;
+    src_blk[j] = blk;
+    if (blk < 2) {
+      const int k = c / CPK, slot = c % CPK;
+      src_off[j] = k * DH + ((slot ^ kswz(k, blk)) * 8);
     } else {
-      src_off[j] = tid * 8;
+      src_off[j] = c * 8;
     }
   }
   // The stage's two page numbers are read with uniform indices (scalar
@@ -130,24 +141,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     const int64_t base_b = (int64_t)page_b * page_stride + head_off;
 #pragma unroll
     for (int j = 0; j < LPT; ++j)
-      dma16((j < 2 ? kpool : vpool) + ((j & 1) ? base_b : base_a) + src_off[j],
-            base + j * 256 * 8);
+      dma16((src_blk[j] < 2 ? kpool : vpool) + ((src_blk[j] & 1) ? base_b : base_a) + src_off[j],
+            base + j * THREADS * 8);
   };
   // E4M3 pages: the codes of chunk j of a stage (8 bytes), then their bf16
-  // values into LDS chunk j * 256 + tid, as the DMA would place them.
+  // values into LDS chunk j * THREADS + tid, as the DMA would place them.
   u32x2 codes[LPT];
   auto load_codes = [&](int page_a, int page_b) {
     const int64_t base_a = (int64_t)page_a * page_stride + head_off;
     const int64_t base_b = (int64_t)page_b * page_stride + head_off;
 #pragma unroll
     for (int j = 0; j < LPT; ++j)
-      codes[j] = load_stream<u32x2>((j < 2 ? kpool : vpool) + ((j & 1) ? base_b : base_a) +
-                                    src_off[j]);
+      codes[j] = load_stream<u32x2>((src_blk[j] < 2 ? kpool : vpool) +
+                                    ((src_blk[j] & 1) ? base_b : base_a) + src_off[j]);
   };
   auto store_codes = [&](int buf) {
     uint16_t* base = stage_ptr(buf) + tid * 8;
 #pragma unroll
-    for (int j = 0; j < LPT; ++j) *(bf16x8*)(base + j * 256 * 8) = e4m3x8_to_bf16(codes[j]);
+    for (int j = 0; j < LPT; ++j) *(bf16x8*)(base + j * THREADS * 8) = e4m3x8_to_bf16(codes[j]);
   };
 
   // Lane-constant fragment offsets (as in the split kernel).
@@ -416,25 +427,31 @@ hipError_t launch_attention_combine_rows(int head_dim, int rows_per_item, int n_
   return hipGetLastError();
 }
 
-hipError_t launch_attention_prefill_bf16(int n_items, int n_q_heads, int n_kv_heads, int kv_fp8,
-                                         const AttnItem* items, const AttnQBlock* qblocks,
-                                         const void* q, const void* k_pages, const void* v_pages,
+hipError_t launch_attention_prefill_bf16(int n_items, int rows_per_item, int n_q_heads,
+                                         int n_kv_heads, int kv_fp8, const AttnItem* items,
+                                         const AttnQBlock* qblocks, const void* q,
+                                         const void* k_pages, const void* v_pages,
                                          int64_t page_stride_elems, const int32_t* block_table,
                                          int32_t bt_stride, float scale_log2, float v_scale,
                                          float* part_ml, float* part_acc, hipStream_t stream,
                                          hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (n_items == 0) return hipSuccess;
-  if (kv_fp8)
-    return launch_timed(attn_prefill_bf16<128, uint8_t>, dim3(n_kv_heads, n_items), dim3(256),
-                        stream, ev_start, ev_stop, items, qblocks, (const uint16_t*)q,
-                        (const uint8_t*)k_pages, (const uint8_t*)v_pages, page_stride_elems,
-                        block_table, bt_stride, n_q_heads, n_kv_heads, scale_log2, v_scale,
-                        part_ml, part_acc);
-  return launch_timed(attn_prefill_bf16<128, uint16_t>, dim3(n_kv_heads, n_items), dim3(256),
-                      stream, ev_start, ev_stop, items, qblocks, (const uint16_t*)q,
-                      (const uint16_t*)k_pages, (const uint16_t*)v_pages, page_stride_elems,
-                      block_table, bt_stride, n_q_heads, n_kv_heads, scale_log2, 1.f, part_ml,
-                      part_acc);
+  if (rows_per_item != 128 && rows_per_item != 256) return hipErrorInvalidValue;
+  // 32 rows per wave: 4 waves (256 threads) for 128 rows, 8 (512) for 256.
+  const dim3 grid(n_kv_heads, n_items), block(2 * rows_per_item);
+  const uint16_t* qq = (const uint16_t*)q;
+#define PDEC_PREFILL(KT_, WAVES_, VS_)                                                          \
+  return launch_timed(attn_prefill_bf16<128, KT_, WAVES_>, grid, block, stream, ev_start,     \
+                      ev_stop, items, qblocks, qq, (const KT_*)k_pages, (const KT_*)v_pages,  \
+                      page_stride_elems, block_table, bt_stride, n_q_heads, n_kv_heads,       \
+                      scale_log2, VS_, part_ml, part_acc)
+  if (kv_fp8) {
+    if (rows_per_item == 256) PDEC_PREFILL(uint8_t, 8, v_scale);
+    PDEC_PREFILL(uint8_t, 4, v_scale);
+  }
+  if (rows_per_item == 256) PDEC_PREFILL(uint16_t, 8, 1.f);
+  PDEC_PREFILL(uint16_t, 4, 1.f);
+#undef PDEC_PREFILL
 }
 
 }  // namespace pdec

@@ -215,6 +215,13 @@ constexpr int kDecodeRows = 16;
 int prefill_rows(const pdec_model_cfg& c) {
   return (c.dtype == PDEC_BF16 && c.head_dim == 128) ? 128 : 64;
 }
+// The LDS-staged kernel also takes 256-row blocks (eight waves share each
+// stage, halving the load work per flop).  A pass switches to them when its
+// 128-row blocks read at least this many key pages each on average (16K
+// keys): measured on 4096-row re-prefill passes of the 8B shape, 256-row
+// blocks were 2-9% slower at 0-2.5K cached keys, +1.8% at 12K, +3.8% at 28K
+// and +10% at 61K.  PDEC_PREFILL_WIDE_PAGES at engine creation overrides it.
+constexpr int64_t kWidePrefillPages = 1024;
 
 int check_cfg(const pdec_model_cfg* c) {
   if (!c) return fail(PDEC_INVALID_ARG, "null cfg");
@@ -274,13 +281,20 @@ int make_layout(const pdec_model_cfg* c, int32_t max_seqs, int32_t max_seq_len,
   // queries per block, prefill_rows-row items.
   const int pre_rows = prefill_rows(*c);
   // Each piece of a packed pass may leave one partly filled query block.
-  const int64_t pre_blocks = (max_chunk + (pre_rows / G) - 1) / (pre_rows / G) +
-                             std::min(kMaxPiecesPerPass, max_chunk);
+  auto blocks_for = [&](int rows) {
+    return (max_chunk + (rows / G) - 1) / (rows / G) + std::min(kMaxPiecesPerPass, max_chunk);
+  };
+  auto items_for = [&](int rows) {
+    return attn_target_items(c->n_kv_heads, kPrefillTargetGroups) + blocks_for(rows) + 16;
+  };
+  const int64_t pre_blocks = blocks_for(pre_rows);
   L->qblocks_cap = std::max<int64_t>(max_batch, pre_blocks);
   const int64_t items_dec = attn_target_items(c->n_kv_heads, kDecodeTargetGroups) + max_batch + 16;
-  const int64_t items_pre = attn_target_items(c->n_kv_heads, kPrefillTargetGroups) + pre_blocks + 16;
+  const int64_t items_pre = items_for(pre_rows);
   L->items_cap = std::max(items_dec, items_pre);
   L->part_row_slots = std::max(items_dec * kDecodeRows, items_pre * pre_rows);
+  if (pre_rows == 128)  // passes with 256-row blocks: fewer blocks and items, more rows each
+    L->part_row_slots = std::max(L->part_row_slots, items_for(256) * 256);
   L->bt_stride = PagePool::pages_for(max_seq_len);
   L->meta_bytes = align_up(L->rows_cap * sizeof(RowMeta)) +
                   align_up(L->qblocks_cap * sizeof(AttnQBlock)) +
@@ -349,6 +363,9 @@ struct pdec_engine {
   // items, pages and pending block-table entries are bounds-checked on the
   // host before anything is enqueued.
   bool validate = false;
+  // Mean key pages per 128-row block from which a prefill pass takes
+  // 256-row blocks (kWidePrefillPages unless PDEC_PREFILL_WIDE_PAGES is set).
+  int64_t wide_prefill_pages = kWidePrefillPages;
 
   int64_t ab() const { return elem_bytes(cfg.dtype); }
   int64_t kvb() const { return kv_elem_bytes(&cfg); }
@@ -385,6 +402,7 @@ int max_items_per_qblock(const std::vector<AttnQBlock>& qblocks) {
 
 // One forward pass of the decoder over M = rows.size() rows.
 struct Pass {
+  int32_t rows_per_item = 0;  // query rows per block and item: 16 (decode), 64, 128 or 256
   std::vector<RowMeta> rows;
   std::vector<AttnQBlock> qblocks;
   std::vector<AttnItem> items;
@@ -396,13 +414,20 @@ struct Pass {
 
 // Workspace bounds of one pass; checked for every pass of a call before the
 // first launch, so that a call either enqueues all of its work or none.
-int check_pass(const pdec_engine* E, const Pass& p, int rows_per_item) {
+int check_pass(const pdec_engine* E, const Pass& p) {
+  const int rows_per_item = p.rows_per_item;
   if ((int64_t)p.items.size() > E->ws.items_cap ||
       (int64_t)p.qblocks.size() > E->ws.qblocks_cap ||
       (int64_t)p.rows.size() > E->ws.rows_cap ||
       (int64_t)p.items.size() * rows_per_item > E->ws.part_row_slots ||
       (int64_t)p.lm_rows.size() > kMaxPiecesPerPass)
     return fail(PDEC_INVALID_ARG, "attention work list exceeds the workspace bound");
+  // The attention kernels compute rows_per_item rows of a block (its queries
+  // times the GQA group); a larger block would lose rows silently.
+  const int G = E->cfg.n_q_heads / E->cfg.n_kv_heads;
+  for (const AttnQBlock& q : p.qblocks)
+    if ((int64_t)q.n_q * G > rows_per_item)
+      return fail(PDEC_INVALID_ARG, "query block larger than its work items' rows");
   if (E->validate) {
     Status st = validate_pass(p.rows, p.qblocks, p.items, E->pool->max_seqs(),
                               E->pool->max_seq_len(), E->ws.bt_stride, E->pool);
@@ -415,9 +440,9 @@ int check_pass(const pdec_engine* E, const Pass& p, int rows_per_item) {
 
 // Enqueues one pass (its bounds already checked).  Logits of the selected
 // rows go to logits + lm_out0 * vocab (nullable logits: none).
-int enqueue_forward(pdec_engine* E, const Pass& p, int rows_per_item, const int32_t* tokens_dev,
-                    float* logits) {
+int enqueue_forward(pdec_engine* E, const Pass& p, const int32_t* tokens_dev, float* logits) {
   const pdec_model_cfg& c = E->cfg;
+  const int rows_per_item = p.rows_per_item;
   const int M = (int)p.rows.size();
   int rc = flush_deltas(E);
   if (rc != PDEC_OK) return rc;
@@ -640,6 +665,8 @@ int engine_create(const pdec_model_cfg* cfg, const pdec_weights* w, void* kv_poo
   {
     const char* v = std::getenv("PDEC_VALIDATE");
     E->validate = v && v[0] && std::strcmp(v, "0") != 0;
+    const char* w = std::getenv("PDEC_PREFILL_WIDE_PAGES");
+    if (w && w[0]) E->wide_prefill_pages = std::max<int64_t>(0, std::atoll(w));
   }
 
   auto cleanup = [&](int code, const std::string& msg) {
@@ -777,8 +804,9 @@ int decode_step(pdec_engine* E, int32_t B, const int32_t* ids, const int32_t* to
   p.lm_all = true;
   plan_attention(specs, choose_split_pages(total_key_pages(specs), E->cfg.n_kv_heads), &p.qblocks,
                  &p.items);
-  int rc = check_pass(E, p, kDecodeRows);
-  if (rc == PDEC_OK) rc = enqueue_forward(E, p, kDecodeRows, tokens_dev, logits);
+  p.rows_per_item = kDecodeRows;
+  int rc = check_pass(E, p);
+  if (rc == PDEC_OK) rc = enqueue_forward(E, p, tokens_dev, logits);
   if (rc != PDEC_OK) E->pool->undo(undo);
   return rc;
 }
@@ -821,16 +849,38 @@ int kv_append_prefix_batch(pdec_engine* E, int32_t n_seqs, const int32_t* ids,
   // earlier pages (written by earlier passes or pieces) and, causally, each
   // other.  Every pass is planned and checked before the first launch.
   const int pre_rows = prefill_rows(E->cfg);
-  const int QB = pre_rows / (E->cfg.n_q_heads / E->cfg.n_kv_heads);
+  const int G = E->cfg.n_q_heads / E->cfg.n_kv_heads;
   std::vector<Pass> passes;
+  struct Piece {
+    int32_t row0, take, slot, pos;
+  };
+  std::vector<Piece> pass_pieces;
   std::vector<QBlockSpec> specs;
+  // Query blocks of the current pass (rows / G queries each, per piece),
+  // then its work items.  The pass takes 256-row blocks where its 128-row
+  // blocks would read long key ranges (kWidePrefillPages).
   auto close = [&]() {
     Pass& p = passes.back();
+    auto build = [&](int rows) {
+      const int QB = rows / G;
+      specs.clear();
+      for (const Piece& pc : pass_pieces)
+        for (int32_t k = 0; k * QB < pc.take; ++k)
+          specs.push_back({pc.row0 + k * QB, std::min(QB, pc.take - k * QB), pc.slot,
+                           pc.pos + k * QB});
+    };
+    p.rows_per_item = pre_rows;
+    build(pre_rows);
+    if (pre_rows == 128 &&
+        total_key_pages(specs) >= E->wide_prefill_pages * (int64_t)specs.size()) {
+      p.rows_per_item = 256;
+      build(256);
+    }
     plan_attention(specs,
                    choose_split_pages(total_key_pages(specs), E->cfg.n_kv_heads,
                                       kPrefillTargetGroups),
                    &p.qblocks, &p.items);
-    specs.clear();
+    pass_pieces.clear();
   };
   int pieces = 0;
   int64_t tok0 = 0;
@@ -850,8 +900,7 @@ int kv_append_prefix_batch(pdec_engine* E, int32_t n_seqs, const int32_t* ids,
         p.rows.push_back({slots[i], pos + j});
         p.tokens.push_back(tokens_host[tok0 + off + j]);
       }
-      for (int32_t k = 0; k * QB < take; ++k)
-        specs.push_back({row0 + k * QB, std::min(QB, take - k * QB), slots[i], pos + k * QB});
+      pass_pieces.push_back({row0, take, slots[i], pos});
       off += take;
       ++pieces;
       if (off == n_tokens[i] && last_logits_dev) {
@@ -863,14 +912,14 @@ int kv_append_prefix_batch(pdec_engine* E, int32_t n_seqs, const int32_t* ids,
   }
   close();
   for (const Pass& p : passes) {
-    int rc = check_pass(E, p, pre_rows);
+    int rc = check_pass(E, p);
     if (rc != PDEC_OK) {
       E->pool->undo(undo);
       return rc;
     }
   }
   for (const Pass& p : passes) {
-    int rc = enqueue_forward(E, p, pre_rows, nullptr, last_logits_dev);
+    int rc = enqueue_forward(E, p, nullptr, last_logits_dev);
     if (rc != PDEC_OK) {  // a HIP error: earlier passes may already be enqueued
       E->pool->undo(undo);
       return rc;

@@ -40,13 +40,14 @@ hipError_t launch_attention_split(int dtype, int kv_fp8, float k_scale, float v_
                                   hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
 
 // The LDS-staged prefill kernel (attention_prefill.hip) behind
-// launch_attention_split for 128-row items with 128-dim heads, bf16 pages
-// (kv_fp8 = 0) or E4M3 pages (kv_fp8 = 1; scale_log2 then includes the K
-// scale, and v_scale multiplies the partial outputs); scale_log2 =
+// launch_attention_split for 128- or 256-row items with 128-dim heads, bf16
+// pages (kv_fp8 = 0) or E4M3 pages (kv_fp8 = 1; scale_log2 then includes the
+// K scale, and v_scale multiplies the partial outputs); scale_log2 =
 // log2(e) / sqrt(head_dim) [* k_scale].
-hipError_t launch_attention_prefill_bf16(int n_items, int n_q_heads, int n_kv_heads, int kv_fp8,
-                                         const AttnItem* items, const AttnQBlock* qblocks,
-                                         const void* q, const void* k_pages, const void* v_pages,
+hipError_t launch_attention_prefill_bf16(int n_items, int rows_per_item, int n_q_heads,
+                                         int n_kv_heads, int kv_fp8, const AttnItem* items,
+                                         const AttnQBlock* qblocks, const void* q,
+                                         const void* k_pages, const void* v_pages,
                                          int64_t page_stride_elems, const int32_t* block_table,
                                          int32_t bt_stride, float scale_log2, float v_scale,
                                          float* part_ml, float* part_acc, hipStream_t stream,

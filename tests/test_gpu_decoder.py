@@ -221,9 +221,10 @@ def test_bf16_8b_geometry_two_layers_parity():
     _bf16_parity(shape, seed=6, prefix_lens=[9, 33, 48, 20], n_steps=4, chunk=32)
 
 
+@pytest.mark.parametrize("wide", [False, True])
 @pytest.mark.parametrize("kv_fp8", [None, (0.5, 0.25)])
 @pytest.mark.parametrize("n_kv_heads", [16, 4])
-def test_bf16_long_prefill_items(n_kv_heads, kv_fp8):
+def test_bf16_long_prefill_items(n_kv_heads, kv_fp8, wide, monkeypatch):
     """Prefill attention over long items: with 16 query heads of 128 dims the
     planner cuts each query block's keys into items of 10-56 pages (5-28
     two-page stages) and 5-8 items per block, so the prefill kernel's
@@ -231,7 +232,11 @@ def test_bf16_long_prefill_items(n_kv_heads, kv_fp8):
     several items per row; chunks of 1000 tokens start mid-page and the last
     item of a block can have an odd page count.  G = 1 and G = 4; bf16 pages,
     and E4M3 pages (staged through registers and converted into the same LDS
-    layout; K and V scales other than 1)."""
+    layout; K and V scales other than 1).  wide: every pass takes 256-row
+    blocks and the eight-wave kernel (the threshold the engine uses for long
+    key ranges forced to 0)."""
+    if wide:
+        monkeypatch.setenv("PDEC_PREFILL_WIDE_PAGES", "0")
     shape = ModelShape(n_layers=1, d_model=256, n_q_heads=16, n_kv_heads=n_kv_heads,
                        head_dim=128, ffn_dim=256, vocab=512)
     _bf16_parity(shape, seed=12, prefix_lens=[4000, 1531], n_steps=2, chunk=1000,
@@ -273,8 +278,9 @@ def test_decode_many_items_per_sequence(kv_fp8):
 KERNEL_PAIR_TOL = 1e-2
 
 
+@pytest.mark.parametrize("wide", [False, True])
 @pytest.mark.parametrize("kv_fp8", [None, (0.5, 0.25)])
-def test_prefill_attention_equals_decode_attention(kv_fp8):
+def test_prefill_attention_equals_decode_attention(kv_fp8, wide, monkeypatch):
     """The LDS-staged prefill kernel against the decode split kernel over the
     same cached pages.  Each trajectory's prefix (17 to 3001 tokens) is
     prefilled once and copied by snapshot/restore into a second sequence, so
@@ -285,7 +291,10 @@ def test_prefill_attention_equals_decode_attention(kv_fp8):
     run the same four-row projections, so q, k, v and the new pages are
     bitwise the same, and the logits differ only by the attention kernels'
     summation orders and item splits: 1e-2 of max|logit| per row, against
-    the oracle bars of 2e-2 (bf16) and 6e-2 (fp8)."""
+    the oracle bars of 2e-2 (bf16) and 6e-2 (fp8).  wide: the prefix passes
+    and the appended pieces take 256-row blocks (eight-wave kernel)."""
+    if wide:
+        monkeypatch.setenv("PDEC_PREFILL_WIDE_PAGES", "0")
     shape = ModelShape(**LONG_G4)
     arrays = make_weights(shape, seed=16, bf16=True)
     lens = [17, 300, 1500, 3001]

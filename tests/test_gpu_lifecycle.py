@@ -31,17 +31,20 @@ BF16_G4 = ModelShape(n_layers=1, d_model=256, n_q_heads=8, n_kv_heads=2, head_di
                      ffn_dim=256, vocab=512)
 
 
-@pytest.mark.parametrize("case", ["fp32", "bf16", "bf16-fp8kv"])
-def test_random_lifecycle_matches_oracle(case):
+@pytest.mark.parametrize("case", ["fp32", "bf16", "bf16-fp8kv", "bf16-wide"])
+def test_random_lifecycle_matches_oracle(case, monkeypatch):
+    """bf16-wide: every prefill pass takes 256-row blocks (eight-wave kernel)."""
     import paper_2609_36899_amd as P
     from paper_2609_36899_amd import _native as N
 
+    if case == "bf16-wide":
+        monkeypatch.setenv("PDEC_PREFILL_WIDE_PAGES", "0")
     bf16 = case != "fp32"
     shape = BF16_G4 if bf16 else TINY
     kv_fp8 = (0.5, 0.25) if case == "bf16-fp8kv" else None
     dt = P.BF16 if bf16 else P.F32
     # fp32: absolute; bf16: relative to max|ref| per row
-    tol = {"fp32": 1e-4, "bf16": 2e-2, "bf16-fp8kv": 6e-2}[case]
+    tol = {"fp32": 1e-4, "bf16": 2e-2, "bf16-fp8kv": 6e-2, "bf16-wide": 2e-2}[case]
     rng = np.random.default_rng(2024)
     arrays = make_weights(shape, seed=30, bf16=bf16)
     w64 = od.ModelWeights.from_arrays(shape, arrays)
