@@ -32,8 +32,9 @@
  *     long key ranges (on average at least 1024 pages, 16K keys, per
  *     128-row block) takes 256-row blocks (eight waves sharing each staged
  *     page).  PDEC_PREFILL_WIDE_PAGES=<pages> before engine_create sets that
- *     threshold for the engine (0: always 256-row blocks).  Results agree to
- *     float32 summation order either way.
+ *     threshold for the engine (0: always 256-row blocks; a value that is not
+ *     a non-negative decimal integer is ignored).  Results agree to float32
+ *     summation order either way.
  *   - Device memory (weights, KV pool, workspace, tokens, logits) is owned by
  *     the caller and must outlive the engine.  The library owns host metadata
  *     and a small pinned staging ring only.

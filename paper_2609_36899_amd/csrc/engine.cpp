@@ -665,8 +665,15 @@ int engine_create(const pdec_model_cfg* cfg, const pdec_weights* w, void* kv_poo
   {
     const char* v = std::getenv("PDEC_VALIDATE");
     E->validate = v && v[0] && std::strcmp(v, "0") != 0;
+    // A plain non-negative decimal count; anything else keeps the default.
+    // Values are capped at 2^40 pages so the comparison cannot overflow.
     const char* w = std::getenv("PDEC_PREFILL_WIDE_PAGES");
-    if (w && w[0]) E->wide_prefill_pages = std::max<int64_t>(0, std::atoll(w));
+    if (w && w[0]) {
+      char* end = nullptr;
+      const long long n = std::strtoll(w, &end, 10);
+      if (end && *end == '\0' && n >= 0)
+        E->wide_prefill_pages = std::min<int64_t>(n, int64_t(1) << 40);
+    }
   }
 
   auto cleanup = [&](int code, const std::string& msg) {
