@@ -163,7 +163,7 @@ int64_t engine_workspace_bytes(const pdec_model_cfg* cfg, int32_t max_seqs, int3
  * The engine starts with an empty resident set and every page free.
  * Errors: PDEC_INVALID_ARG (bad sizes, null pointers), PDEC_UNSUPPORTED
  * (shapes the kernels do not handle: head_dim other than 64/128, GQA group
- * size not dividing 16, BF16 dims not multiples of 64), PDEC_HIP_ERROR. */
+ * size above 16, BF16 dims not multiples of 64), PDEC_HIP_ERROR. */
 int engine_create(const pdec_model_cfg* cfg, const pdec_weights* weights, void* kv_pool,
                   int64_t kv_pool_bytes, int32_t max_seqs, int32_t max_seq_len, int32_t max_batch,
                   int32_t max_chunk, void* workspace, int64_t workspace_bytes, void* stream,
@@ -465,8 +465,8 @@ int swiglu_projection(int32_t dtype, int32_t M, int32_t F, int32_t K, const void
  * stream.
  * Errors: PDEC_INVALID_ARG (null pointers, sizes < 1, n_q_heads not a
  * multiple of n_kv_heads, lens[b] outside [1, bt_stride * 16], workspace too
- * small), PDEC_UNSUPPORTED (head_dim other than 64 / 128, GQA group size not
- * dividing 16), PDEC_HIP_ERROR.
+ * small), PDEC_UNSUPPORTED (head_dim other than 64 / 128, GQA group size
+ * above 16), PDEC_HIP_ERROR.
  * ------------------------------------------------------------------------- */
 int64_t paged_attention_workspace_bytes(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
                                         int32_t head_dim, int64_t max_total_tokens);

@@ -235,7 +235,10 @@ int check_cfg(const pdec_model_cfg* c) {
   if (c->n_q_heads % c->n_kv_heads != 0)
     return fail(PDEC_INVALID_ARG, "n_q_heads must be a multiple of n_kv_heads");
   const int G = c->n_q_heads / c->n_kv_heads;
-  if (16 % G != 0) return fail(PDEC_UNSUPPORTED, "GQA group size must divide 16");
+  // A decode query block is the G query heads of one token: its rows fill
+  // part of one 16-row MFMA tile, so groups of up to 16 heads (any size, rows
+  // past G masked) are supported.
+  if (G > 16) return fail(PDEC_UNSUPPORTED, "GQA group size must be at most 16");
   if (c->head_dim != 64 && c->head_dim != 128)
     return fail(PDEC_UNSUPPORTED, "head_dim must be 64 or 128");
   if (c->qk_norm != 0 && c->qk_norm != 1) return fail(PDEC_INVALID_ARG, "qk_norm must be 0 or 1");
@@ -1206,7 +1209,7 @@ static int paged_attention_impl(int32_t kv_dtype, float k_scale, float v_scale, 
     return fail(PDEC_INVALID_ARG, "null argument");
   if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || bt_stride < 1)
     return fail(PDEC_INVALID_ARG, "bad sizes");
-  if (16 % (Hq / Hkv)) return fail(PDEC_UNSUPPORTED, "GQA group size must divide 16");
+  if (Hq / Hkv > 16) return fail(PDEC_UNSUPPORTED, "GQA group size must be at most 16");
   if (Dh != 64 && Dh != 128) return fail(PDEC_UNSUPPORTED, "head_dim must be 64 or 128");
   const int64_t need = paged_attention_workspace_bytes(B, Hq, Hkv, Dh, 0);
   if (ws_bytes < need) return fail(PDEC_INVALID_ARG, "workspace too small: need " + std::to_string(need));

@@ -54,7 +54,8 @@ def _check_rows(got, ref, tol, normwise):
 EDGE_LENS = [1, 2, 15, 16, 17, 31, 32, 33, 48, 127, 128, 129, 300, 1000, 2049]
 
 
-@pytest.mark.parametrize("hq,hkv,dh", [(32, 8, 128), (8, 2, 128), (16, 16, 128), (16, 1, 64)])
+@pytest.mark.parametrize("hq,hkv,dh", [(32, 8, 128), (8, 2, 128), (16, 16, 128), (16, 1, 64),
+                                        (40, 8, 128), (6, 2, 64)])
 def test_bf16_edge_lengths(hq, hkv, dh):
     lens = np.array(EDGE_LENS)
     case = paged_attention_case(len(lens), hq, hkv, dh, lens, n_pool_pages=700, seed=1)
@@ -64,7 +65,7 @@ def test_bf16_edge_lengths(hq, hkv, dh):
     _check_rows(got, ref, BF16_TOL, normwise=True)
 
 
-@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128)])
+@pytest.mark.parametrize("hq,hkv,dh", [(4, 2, 64), (32, 8, 128), (15, 3, 128)])
 def test_f32_edge_lengths(hq, hkv, dh):
     lens = np.array(EDGE_LENS[:12])
     case = paged_attention_case(len(lens), hq, hkv, dh, lens, n_pool_pages=120, seed=2,

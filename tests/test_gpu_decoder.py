@@ -4,8 +4,8 @@ float64 oracle, through the C ABI.
 * tiny fp32 decoder (2 layers, d 256, 4/2 heads, Dh 64): prefixes of 17, 40,
   96, 128 tokens, then 32 greedy steps, teacher-forced with the oracle's
   tokens; 33 logit rows per trajectory within 1e-4 absolute;
-* bf16 decoders (small, and the 8B layer geometry with 2 layers): per-row
-  normwise 2e-2;
+* bf16 decoders (small, the 8B layer geometry with 2 layers, and the layer
+  widths of the 14B and 32B Qwen3 shapes with 2 layers): per-row normwise 2e-2;
 * the Qwen3-style per-head q/k norm variant, fp32 (Dh 64) and bf16 (Dh 128);
 * chunking, re-prefill after departure, batch-order invariance and atomic
   failure of page growth;
@@ -20,7 +20,7 @@ import torch
 import oracle
 from oracle import decoder as od
 from workload import (EIGHT_B, SMALL_BF16, SMALL_BF16_QK, TINY, TINY_QK, ModelShape,
-                      make_weights, random_tokens)
+                      make_weights, make_weights_parallel, random_tokens)
 
 pytestmark = pytest.mark.gpu
 
@@ -170,10 +170,12 @@ def test_batch_order_is_bitwise_invariant(bf16):
     np.testing.assert_array_equal(a[order], b)
 
 
-def _bf16_parity(shape, seed, prefix_lens, n_steps, chunk, kv_fp8=None, **engine_kw):
+def _bf16_parity(shape, seed, prefix_lens, n_steps, chunk, kv_fp8=None, parallel_draw=False,
+                 **engine_kw):
     tol = FP8_KV_TOL if kv_fp8 is not None else BF16_TOL
     closer = []
-    arrays = make_weights(shape, seed=seed, bf16=True)
+    draw = make_weights_parallel if parallel_draw else make_weights
+    arrays = draw(shape, seed=seed, bf16=True)
     w64 = od.ModelWeights.from_arrays(shape, arrays)
     E = _engine(shape, arrays, bf16=True, max_chunk=max(chunk, 16), kv_fp8=kv_fp8, **engine_kw)
     seqs, toks = [], []
@@ -219,6 +221,33 @@ def test_bf16_8b_geometry_two_layers_parity():
                        n_kv_heads=EIGHT_B.n_kv_heads, head_dim=EIGHT_B.head_dim,
                        ffn_dim=EIGHT_B.ffn_dim, vocab=4096)
     _bf16_parity(shape, seed=6, prefix_lens=[9, 33, 48, 20], n_steps=4, chunk=32)
+
+
+@pytest.mark.parametrize("hq,hkv,dh", [(6, 2, 64), (10, 2, 128), (7, 1, 128), (12, 1, 128)])
+def test_bf16_odd_gqa_groups(hq, hkv, dh):
+    """GQA groups that do not divide the 16-row MFMA tile (3, 5, 7, 12): a
+    decode block's rows fill part of a tile, a 128-row prefill block holds
+    128 // G queries (42, 25, 18, 10) and a 64-row one 64 // G, so pieces end
+    mid-block and mid-tile.  Prefill in 37-token chunks, then decode."""
+    shape = ModelShape(n_layers=1, d_model=256, n_q_heads=hq, n_kv_heads=hkv, head_dim=dh,
+                       ffn_dim=256, vocab=512)
+    _bf16_parity(shape, seed=17, prefix_lens=[3, 130, 77, 41], n_steps=3, chunk=37)
+
+
+@pytest.mark.parametrize("width", ["14b", "32b"])
+def test_bf16_qwen3_widths_two_layers_parity(width):
+    """The layer widths of the paper's larger rollout models (the Qwen3-14B and
+    -32B dimensions: d 5120, 40 / 64 query heads over 8 KV heads of 128 dims,
+    FFN 17408 / 25600, per-head q/k RMSNorm, RoPE base 1e6) with two layers
+    and a 5000-entry vocabulary (a part-filled last LM-head column group).
+    GQA groups of 5 (14B) put 25 queries in a 128-row prefill block and 5
+    rows in a decode block; at 32B the query width (8192) differs from the
+    model width.  Real prefill over pieces that end mid-block, then decode."""
+    heads, ffn = {"14b": (40, 17408), "32b": (64, 25600)}[width]
+    shape = ModelShape(n_layers=2, d_model=5120, n_q_heads=heads, n_kv_heads=8, head_dim=128,
+                       ffn_dim=ffn, vocab=5000, rope_base=1e6, qk_norm=True)
+    _bf16_parity(shape, seed=16, prefix_lens=[9, 61, 48, 26], n_steps=3, chunk=32,
+                 parallel_draw=True)
 
 
 @pytest.mark.parametrize("wide", [False, True])

@@ -130,7 +130,9 @@ def make_weights_parallel(shape: ModelShape, seed: int = 0, bf16: bool = True,
     the fixed order of make_weights, and chunk i is filled by its own PCG64
     stream ``SeedSequence(seed).spawn(...)[i]`` (N(0, std), float32, then bf16
     RNE with ``bf16``) on a thread pool.  The values differ from
-    make_weights' (another stream layout) and do not depend on ``threads``."""
+    make_weights' (another stream layout) and do not depend on ``threads``.
+    A shape with q/k norm also gets per-layer q and k gains 1 + 0.1 N(0, 1),
+    drawn from one further stream."""
     import concurrent.futures as cf
     s = shape
     dims = [("embed", s.vocab, s.d_model)]
@@ -164,6 +166,11 @@ def make_weights_parallel(shape: ModelShape, seed: int = 0, bf16: bool = True,
         lay["attn_norm"] = np.ones(s.d_model, dtype=np.float32)
         lay["ffn_norm"] = np.ones(s.d_model, dtype=np.float32)
         weights["layers"].append(lay)
+    if s.qk_norm:  # as in make_weights, from one more stream after the matrices
+        rng = np.random.default_rng(np.random.SeedSequence(seed).spawn(len(jobs) + 1)[-1])
+        for lay in weights["layers"]:
+            for name in ("q_norm", "k_norm"):
+                lay[name] = (1.0 + 0.1 * rng.standard_normal(s.head_dim)).astype(np.float32)
     return weights
 
 
