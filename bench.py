@@ -45,7 +45,13 @@ WORKLOADS = {
     "decode-8b-b64-pareto": (64, ("pareto", 1.5, 1024, 65536)),
     "decode-8b-b256-pareto": (256, ("pareto", 1.5, 1024, 65536)),
     "decode-8b-b512-pareto": (512, ("pareto", 1.5, 1024, 65536)),
+    # The same lognormal contexts at the 14B and 32B Qwen3 dimensions (batches
+    # sized so that weights and KV fit in one GPU's 288 GB).
+    "decode-14b-b128-lognormal": (128, ("lognormal", 4096, 0.8, 256, 32768)),
+    "decode-32b-b64-lognormal": (64, ("lognormal", 4096, 0.8, 256, 32768)),
 }
+# Decoder shape by the model tag in a workload name (decode-<tag>-...).
+SHAPE_TAGS = ("8b", "14b", "32b")
 # The same workloads with KV pages stored as fp8 (E4M3) codes, scales 1.
 FP8_KV = {f"{name}-fp8kv": name for name in ("decode-8b-b256-lognormal", "decode-8b-b8-long",
                                                "decode-8b-b16-pareto", "decode-8b-b64-pareto")}
@@ -55,6 +61,15 @@ DEFAULT_WORKLOAD = "decode-8b-b256-lognormal"
 # Multi-turn rollouts: decode segments of 128 steps separated by tool-output
 # appends of U[512, 2048] tokens per trajectory through kv_append_prefix.
 MULTITURN = {f"multiturn-8b-b{b}": b for b in (16, 64, 256, 512)}
+
+
+def describe_shape(shape):
+    """One line naming a decoder shape, for the JSON config."""
+    tag = {4096: "8B", 5120: "14B" if shape.n_layers == 40 else "32B"}.get(shape.d_model, "")
+    extra = ", q/k norm" if shape.qk_norm else ""
+    return (f"{tag}-shaped decoder ({shape.n_layers}x{shape.d_model}, {shape.n_q_heads}/"
+            f"{shape.n_kv_heads} heads, Dh {shape.head_dim}, FFN {shape.ffn_dim}, vocab "
+            f"{shape.vocab}{extra}, RoPE base {shape.rope_base:g}), random init")
 
 
 def log(msg):
@@ -331,10 +346,11 @@ def run_decode(workload, steps, warmup, with_cpu, seed=1):
 
     import paper_2609_36899_amd as P
     from paper_2609_36899_amd import _native as N
-    from workload import EIGHT_B
+    from workload import EIGHT_B, QWEN3_14B_SHAPED, QWEN3_32B_SHAPED
 
-    qk = workload in QK_NORM
-    shape = dataclasses.replace(EIGHT_B, qk_norm=True) if qk else EIGHT_B
+    base = {"8b": EIGHT_B, "14b": QWEN3_14B_SHAPED, "32b": QWEN3_32B_SHAPED}[workload.split("-")[1]]
+    qk = workload in QK_NORM or base.qk_norm
+    shape = dataclasses.replace(base, qk_norm=True) if qk else base
     kv_fp8 = (1.0, 1.0) if workload in FP8_KV else None
     batch, spec = WORKLOADS[FP8_KV.get(workload, QK_NORM.get(workload, workload))]
     lens = draw_lengths(batch, spec, seed=seed)
@@ -439,8 +455,7 @@ def run_decode(workload, steps, warmup, with_cpu, seed=1):
         "steps": steps, "warmup": warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": workload, "decoder_shape": "8B-shaped decoder (32x4096, 32/8 heads, "
-                   "Dh 128, FFN 14336, vocab 128256), random init",
+        "config": {"workload": workload, "decoder_shape": describe_shape(shape),
                    "batch": int(batch), "context_mean": round(float(lens.mean()), 1),
                    "context_min": int(lens.min()), "context_max": int(lens.max()),
                    "length_distribution": list(spec), "length_seed": seed, "page_tokens": 16,

@@ -61,6 +61,16 @@ SMALL_BF16 = ModelShape(n_layers=2, d_model=512, n_q_heads=8, n_kv_heads=2, head
 # The same two with Qwen3-style q/k norm.
 TINY_QK = dataclasses.replace(TINY, qk_norm=True)
 SMALL_BF16_QK = dataclasses.replace(SMALL_BF16, qk_norm=True)
+# Decoders with the dimensions of the paper's larger rollout models (Qwen3-14B
+# and Qwen3-32B, as their public configurations give them; the paper states no
+# hyperparameters): per-head q/k norm, RoPE base 1e6, untied LM head.  Random
+# init like the others; used for throughput at those widths and depths.
+QWEN3_14B_SHAPED = ModelShape(n_layers=40, d_model=5120, n_q_heads=40, n_kv_heads=8,
+                              head_dim=128, ffn_dim=17408, vocab=151936, rope_base=1e6,
+                              qk_norm=True)
+QWEN3_32B_SHAPED = ModelShape(n_layers=64, d_model=5120, n_q_heads=64, n_kv_heads=8,
+                              head_dim=128, ffn_dim=25600, vocab=151936, rope_base=1e6,
+                              qk_norm=True)
 
 
 def round_to_bf16(x: np.ndarray) -> np.ndarray:
