@@ -272,6 +272,20 @@ def test_bf16_long_prefill_items(n_kv_heads, kv_fp8, wide, monkeypatch):
                  kv_fp8=kv_fp8, pool_tokens=6144, max_seq_len=4096)
 
 
+@pytest.mark.parametrize("wide", [False, True])
+def test_bf16_long_prefill_items_group_of_5(wide, monkeypatch):
+    """The same long prefill with GQA groups of 5 (the 14B shape's): 128-row
+    blocks hold 25 queries and 256-row blocks (eight-wave kernel) 51, so
+    every block leaves rows of its last tile empty and 1000-token chunks end
+    mid-block."""
+    if wide:
+        monkeypatch.setenv("PDEC_PREFILL_WIDE_PAGES", "0")
+    shape = ModelShape(n_layers=1, d_model=256, n_q_heads=10, n_kv_heads=2, head_dim=128,
+                       ffn_dim=256, vocab=512)
+    _bf16_parity(shape, seed=18, prefix_lens=[4000, 1531], n_steps=2, chunk=1000,
+                 pool_tokens=6144, max_seq_len=4096)
+
+
 @pytest.mark.parametrize("ffn", [8256, 14336])
 def test_bf16_wide_ffn_fused_swiglu_parity(ffn):
     """An FFN wide enough that the gate/up projection runs unsplit with
