@@ -58,6 +58,15 @@ def test_host_only_calls_without_gpu():
     assert b"multiple" in lib.last_error()
     odd = N.ModelCfg(2, 256, 4, 2, 96, 688, 1024, 1e-6, 1e4, N.F32)
     assert lib.kv_bytes_per_token(byref(odd)) == N.UNSUPPORTED
+    # GQA groups of any size up to 16 query heads (a decode query's rows share
+    # one 16-row tile): 5 and 16 are accepted, 17 is not.
+    g5 = N.ModelCfg(2, 256, 10, 2, 128, 688, 1024, 1e-6, 1e4, N.F32)
+    assert lib.kv_bytes_per_token(byref(g5)) == 2 * 2 * 2 * 128 * 4
+    g16 = N.ModelCfg(2, 256, 16, 1, 64, 688, 1024, 1e-6, 1e4, N.F32)
+    assert lib.kv_bytes_per_token(byref(g16)) == 2 * 2 * 1 * 64 * 4
+    g17 = N.ModelCfg(2, 256, 17, 1, 64, 688, 1024, 1e-6, 1e4, N.F32)
+    assert lib.kv_bytes_per_token(byref(g17)) == N.UNSUPPORTED
+    assert b"at most 16" in lib.last_error()
     assert lib.paged_attention_workspace_bytes(64, 32, 8, 128, 0) > 0
     qk = N.ModelCfg(2, 256, 4, 2, 64, 688, 1024, 1e-6, 1e4, N.F32, 1)
     assert lib.kv_bytes_per_token(byref(qk)) == 2048
