@@ -1001,7 +1001,8 @@ PROJ_SHAPES = [("qkv", 6144, 4096), ("o", 4096, 4096), ("gate_up", 28672, 4096),
                ("down", 4096, 14336), ("lm_head", 128256, 4096)]
 
 
-def run_projections(batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), iters=24):
+def run_projections(batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), iters=24,
+                    workload="projections-8b", value_batch=256):
     """The 8B projection shapes through weight_projection, swept over the batch,
     and the gate/up pair through swiglu_projection (the decode step's path).
 
@@ -1088,10 +1089,10 @@ def run_projections(batches=(1, 2, 4, 8, 16, 32, 64, 128, 256, 512), iters=24):
             layer[r["M"]] = layer.get(r["M"], 0.0) + r["us"]
         if r["shape"] in ("qkv", "o", "gate_up", "down"):
             layer_ref[r["M"]] = layer_ref.get(r["M"], 0.0) + r["torch_matmul_us"]
-    return {"metric": "weight projection time per 8B layer, 1 MI355X", "value": layer.get(256),
-            "unit": "us at batch 256", "n_gpus": 1, "higher_is_better": False,
-            "data": "synthetic", "dtype": "bf16",
-            "config": {"workload": "projections-8b", "batches": list(batches)},
+    return {"metric": "weight projection time per 8B layer, 1 MI355X",
+            "value": layer.get(value_batch), "unit": f"us at batch {value_batch}", "n_gpus": 1,
+            "higher_is_better": False, "data": "synthetic", "dtype": "bf16",
+            "config": {"workload": workload, "batches": list(batches)},
             "layer_us": {str(m): round(v, 1) for m, v in layer.items()},
             "layer_us_torch_matmul": {str(m): round(v, 1) for m, v in layer_ref.items()},
             "rows": rows, "cpu_baseline": None}
@@ -1194,7 +1195,8 @@ def main():
                     choices=sorted(WORKLOADS) + sorted(FP8_KV) + sorted(QK_NORM)
                     + sorted(MULTITURN)
                     + ["kv-transfer-8b", "kv-transfer-8b-fp8kv", "projections-8b", "landscape-8b", "sampling-8b",
-                       "copy-1gib", "paced-rollout-8b", "attention-b64", "tiny-fp32"])
+                       "copy-1gib", "paced-rollout-8b", "attention-b64", "tiny-fp32",
+                       "projections-8b-prefill"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=1,
                     help="seed of the context-length draw of the decode workloads")
@@ -1212,6 +1214,9 @@ def main():
         out = run_kv_transfer(chunk=args.append_chunk)
     elif args.workload == "kv-transfer-8b-fp8kv":
         out = run_kv_transfer(chunk=args.append_chunk, kv_fp8=(1.0, 1.0))
+    elif args.workload == "projections-8b-prefill":
+        out = run_projections(batches=(1024, 2048, 4096), workload="projections-8b-prefill",
+                              value_batch=4096)
     elif args.workload == "projections-8b":
         out = run_projections()
     elif args.workload == "landscape-8b":
