@@ -44,7 +44,7 @@ def _check(case, k_scale, v_scale):
             assert err <= TOL * np.max(np.abs(ref[b, h])), (b, h, err)
 
 
-@pytest.mark.parametrize("hq,hkv,dh", [(32, 8, 128), (8, 2, 128), (16, 1, 64)])
+@pytest.mark.parametrize("hq,hkv,dh", [(32, 8, 128), (8, 2, 128), (16, 1, 64), (40, 8, 128)])
 def test_edge_lengths(hq, hkv, dh):
     lens = np.array(EDGE_LENS)
     case = paged_attention_case_fp8(len(lens), hq, hkv, dh, lens, n_pool_pages=700, seed=21)
