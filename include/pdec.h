@@ -28,7 +28,8 @@
  *     written twice).  A failed check returns PDEC_INVALID_ARG ("validate:
  *     ...") with nothing enqueued.  Off by default (host cost per call).
  *   - Prefill with bf16 activations and 128-dim heads groups query rows in
- *     blocks of 128 (work groups of four waves); a pass whose blocks read
+ *     blocks of 128 (128 / G queries, G the GQA group, rounded down; work
+ *     groups of four waves); a pass whose blocks read
  *     long key ranges (on average at least 1024 pages, 16K keys, per
  *     128-row block) takes 256-row blocks (eight waves sharing each staged
  *     page).  PDEC_PREFILL_WIDE_PAGES=<pages> before engine_create sets that
