@@ -16,8 +16,10 @@ struct RowMeta {
   int32_t pos;   // position of this token in its sequence
 };
 
-// A block of consecutive query rows of one sequence that share attention
-// work items: 1 row in decode, up to 16 / group rows in prefill.
+// A block of consecutive query rows (tokens) of one sequence that share
+// attention work items: 1 token in decode; in prefill up to R / G tokens,
+// G the GQA group and R the kernel's rows per item (128 or 256 with 128-dim
+// heads, 64 with 64-dim heads), each token contributing G (token, head) rows.
 struct AttnQBlock {
   int32_t q_row0;      // first activation row of the block
   int32_t n_q;         // rows in the block
