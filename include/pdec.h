@@ -427,7 +427,12 @@ int weight_projection(int32_t dtype, int32_t M, int32_t N, int32_t K, const void
  * chooses no K split, as for every 8B-shaped batch), the product and the
  * SwiGLU run in one kernel and the fp32 gate/up values never reach memory;
  * otherwise the split-K partials go to the workspace and a second kernel sums
- * them and applies SwiGLU with the same fp32 arithmetic.
+ * them and applies SwiGLU with the same fp32 arithmetic.  Up to 256 rows, if
+ * the fused kernel's work groups would fill whole rounds of the GPU's 256
+ * compute units plus a last round at most half full (F = 17408, the 14B
+ * shape's FFN), the columns of that last round take the split form instead
+ * (its partials in the workspace), so the tail runs as one round of short
+ * work groups.
  *   x: device [M][K] in dtype; w_gate, w_up: [F][K] weights as produced by
  *   pack_weight; u: device [M][F] in dtype (bf16 rounded to nearest even);
  *   workspace: device, at least swiglu_projection_workspace_bytes(...) bytes

@@ -265,12 +265,15 @@ size_t part_elems_for(const pdec_model_cfg* c, int64_t rows_cap) {
                             {2 * c->ffn_dim, c->d_model},
                             {c->d_model, c->ffn_dim}};
   size_t best = 0;
-  for (int64_t m = 1; m <= rows_cap; ++m)
+  for (int64_t m = 1; m <= rows_cap; ++m) {
     for (auto& s : shapes) {
       int ks;
       const int S = gemm_plan_splits(c->dtype, (int)m, s[0], s[1], &ks);
       best = std::max(best, (size_t)S * (size_t)m * (size_t)s[0]);
     }
+    if (c->dtype == PDEC_BF16)  // the split tail of a fused gate/up launch
+      best = std::max(best, (size_t)swiglu_tail_part_elems((int)m, c->ffn_dim, c->d_model));
+  }
   return best;
 }
 
@@ -514,7 +517,7 @@ int enqueue_forward(pdec_engine* E, const Pass& p, const int32_t* tokens_dev, fl
     HIP_OR_FAIL(E->timer.pair(PDEC_TIMER_GEMM, &ea, &eb));
     if (dt == PDEC_BF16 && S == 1) {  // one work group per column: SwiGLU in the epilogue
       HIP_OR_FAIL(launch_gemm_swiglu(M, F, d, E->h, d, E->w_gu[l].ptr[0], E->w_gu[l].ptr[1],
-                                     E->u, s, ea, eb));
+                                     E->u, E->part, s, ea, eb));
     } else {
       HIP_OR_FAIL(launch_gemm(dt, M, 2 * F, d, E->h, d, E->w_gu[l], E->part, S, ks, s, ea, eb));
       HIP_OR_FAIL(launch_swiglu(dt, M, F, E->part, S, E->u, s));
@@ -1154,7 +1157,8 @@ int64_t swiglu_projection_workspace_bytes(int32_t dtype, int32_t M, int32_t F, i
     return fail(PDEC_INVALID_ARG, "bad projection arguments");
   int ks;
   const int S = gemm_plan_splits(dtype, M, 2 * F, K, &ks);
-  return (dtype == PDEC_BF16 && S == 1) ? 0 : (int64_t)S * M * 2 * F * 4;
+  return (dtype == PDEC_BF16 && S == 1) ? swiglu_tail_part_elems(M, F, K) * 4
+                                         : (int64_t)S * M * 2 * F * 4;
 }
 
 int swiglu_projection(int32_t dtype, int32_t M, int32_t F, int32_t K, const void* x,
@@ -1173,7 +1177,8 @@ int swiglu_projection(int32_t dtype, int32_t M, int32_t F, int32_t K, const void
   hipStream_t s = (hipStream_t)stream;
   // The same choice as the decoder layer.
   if (dtype == PDEC_BF16 && S == 1) {
-    HIP_OR_FAIL(launch_gemm_swiglu(M, F, K, x, K, w_gate, w_up, u, s));
+    HIP_OR_FAIL(launch_gemm_swiglu(M, F, K, x, K, w_gate, w_up, u,
+                                   need > 0 ? (float*)workspace : nullptr, s));
     return PDEC_OK;
   }
   WSegs ws{};

@@ -706,9 +706,46 @@ hipError_t launch_gemm_bf16(int M, int N, int K, const uint16_t* a, int64_t lda,
 
 }  // namespace
 
+namespace {
+
+// The fused gate/up grid has one work group per half column-group of both
+// matrices (up to 256 rows: one M-block).  When that count is whole rounds
+// of the 256 CUs plus a last round at most half full (F = 17408: 272
+// half-groups), the last round runs nearly as long as a full one while most
+// CUs idle: at K = 5120 and 128 rows, 272 half-groups took 112 us against
+// 70 us for 256.  Those tail columns then take the plain kernels with their
+// K axis split (up to 16 ways, so that the tail fills one round of short
+// work groups) and a SwiGLU pass over the summed partials.
+struct GluPlan {
+  int fused_halves;  // half-groups of the fused launch (a multiple of 256 when split)
+  int tail_halves;   // half-groups left to the split launch (0: none)
+  int splits, k_split;
+};
+
+GluPlan plan_glu(int M, int F, int K) {
+  const int halves = 2 * ((F + kGroupCols - 1) / kGroupCols);
+  GluPlan p{halves, 0, 1, K};
+  const int tail = halves % 256;
+  if (M > 256 || halves < 256 || tail == 0 || tail > 128) return p;
+  const int ksteps = K / 64;
+  const int per = (ksteps + std::min(16, 256 / tail) - 1) / std::min(16, 256 / tail);
+  const int splits = (ksteps + per - 1) / per;
+  if (splits < 2) return p;
+  return {halves - tail, tail, splits, per * 64};
+}
+
+}  // namespace
+
+int64_t swiglu_tail_part_elems(int M, int F, int K) {
+  const GluPlan g = plan_glu(M, F, K);
+  if (g.tail_halves == 0) return 0;
+  const int64_t ft = F - (int64_t)(g.fused_halves / 2) * kGroupCols;  // tail columns per matrix
+  return (int64_t)g.splits * M * 2 * ft;
+}
+
 hipError_t launch_gemm_swiglu(int M, int F, int K, const void* A, int64_t lda, const void* w_gate,
-                              const void* w_up, void* u, hipStream_t stream, hipEvent_t ev_start,
-                              hipEvent_t ev_stop) {
+                              const void* w_up, void* u, float* tail_part, hipStream_t stream,
+                              hipEvent_t ev_start, hipEvent_t ev_stop) {
   if (M <= 0 || F <= 0) return hipSuccess;
   WSegs w{};
   w.ptr[0] = w_gate;
@@ -716,9 +753,30 @@ hipError_t launch_gemm_swiglu(int M, int F, int K, const void* A, int64_t lda, c
   w.row_end[0] = F;
   w.row_end[1] = 2 * F;
   w.n_seg = 2;
-  const int halves = 2 * ((F + kGroupCols - 1) / kGroupCols);
-  return launch_gemm_bf16<true>(M, F, K, (const uint16_t*)A, lda, w, halves, nullptr,
-                                (uint16_t*)u, 1, K, stream, ev_start, ev_stop);
+  const GluPlan g = plan_glu(M, F, K);
+  if (g.tail_halves == 0 || !tail_part)
+    return launch_gemm_bf16<true>(M, F, K, (const uint16_t*)A, lda, w, 2 * ((F + 127) / 128),
+                                  nullptr, (uint16_t*)u, 1, K, stream, ev_start, ev_stop);
+  // Whole groups [0, g0) of both matrices fused; groups [g0, ...) split.
+  hipError_t e = launch_gemm_bf16<true>(M, F, K, (const uint16_t*)A, lda, w, g.fused_halves,
+                                        nullptr, (uint16_t*)u, 1, K, stream, ev_start, nullptr);
+  if (e != hipSuccess) return e;
+  const int g0 = g.fused_halves / 2, ft = F - g0 * kGroupCols, tg = (ft + kGroupCols - 1) / kGroupCols;
+  WSegs t{};
+  t.ptr[0] = (const uint16_t*)w_gate + (int64_t)g0 * kGroupCols * K;
+  t.ptr[1] = (const uint16_t*)w_up + (int64_t)g0 * kGroupCols * K;
+  t.row_end[0] = ft;
+  t.row_end[1] = 2 * ft;
+  t.grp_end[0] = tg;
+  t.grp_end[1] = 2 * tg;
+  t.n_seg = 2;
+  e = launch_gemm_bf16<false>(M, 2 * ft, K, (const uint16_t*)A, lda, t, 2 * tg, tail_part, nullptr,
+                              g.splits, g.k_split, stream, nullptr, nullptr);
+  if (e != hipSuccess) return e;
+  e = launch_swiglu(1, M, ft, tail_part, g.splits, (uint16_t*)u + (int64_t)g0 * kGroupCols, stream,
+                    F);
+  if (e == hipSuccess && ev_stop) e = hipEventRecord(ev_stop, stream);
+  return e;
 }
 
 hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t lda,

@@ -82,9 +82,15 @@ hipError_t launch_gemm(int dtype, int M, int N, int K, const void* A, int64_t ld
 // u[m][n] = bf16(silu(g) * up), g and up the products of row m of A with
 // column n of the packed gate and up matrices ([F][K] each), n < F.  Equals
 // launch_gemm over the two segments (splits = 1) followed by launch_swiglu.
+// Where the fused grid would leave a second round of work groups at most
+// half full (up to 256 rows), the columns of that tail take launch_gemm with
+// a K split into tail_part (fp32, at least swiglu_tail_part_elems floats)
+// and launch_swiglu; with tail_part null the whole product is fused.
 hipError_t launch_gemm_swiglu(int M, int F, int K, const void* A, int64_t lda, const void* w_gate,
-                              const void* w_up, void* u, hipStream_t stream,
+                              const void* w_up, void* u, float* tail_part, hipStream_t stream,
                               hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+// fp32 elements launch_gemm_swiglu needs in tail_part for this shape (0: fused only).
+int64_t swiglu_tail_part_elems(int M, int F, int K);
 // Temperature / top-p sampling (sample.hip).
 // With a workspace of sample_workspace_bytes(B) (> 0 only for small batches)
 // every pass is split over several work groups per row; same tokens.
@@ -123,8 +129,9 @@ hipError_t launch_qkv_rope_kv(int dtype, int kv_fp8, float k_scale, float v_scal
                               const float* q_gain, const float* k_gain, float eps,
                               hipStream_t stream);
 // u[m][n] = silu(g) * up with g, up the summed partials of columns n and F+n.
+// Row m of u starts at u + m * ldu (ldu 0: F).
 hipError_t launch_swiglu(int dtype, int M, int F, const float* part, int splits, void* u,
-                         hipStream_t stream);
+                         hipStream_t stream, int64_t ldu = 0);
 // out[i] = sum_s part[s][i] over `splits` slabs of n floats (n % 4 == 0).
 hipError_t launch_sum_splits(int64_t n, const float* part, int splits, float* out,
                              hipStream_t stream);

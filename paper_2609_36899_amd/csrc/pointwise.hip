@@ -217,10 +217,11 @@ __global__ __launch_bounds__(kRowThreads) void qkv_rope_kv_kernel(
   }
 }
 
-// Four columns per thread (F % 4 == 0).
+// Four columns per thread (F % 4 == 0); row m of u starts at u + m * ldu.
 template <typename HT>
 __global__ __launch_bounds__(256) void swiglu_kernel(int M, int F, const float* __restrict__ part,
-                                                     int splits, HT* __restrict__ u) {
+                                                     int splits, HT* __restrict__ u,
+                                                     int64_t ldu) {
   const int64_t n4 = (int64_t)M * F / 4;
   const int64_t slab = (int64_t)M * 2 * F;
   for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n4;
@@ -232,7 +233,7 @@ __global__ __launch_bounds__(256) void swiglu_kernel(int M, int F, const float* 
     const float4 up = add_splits4(*(const float4*)(pg + F), pg + slab + F, slab, splits - 1);
     const float4 r = make_float4(gt.x / (1.f + expf(-gt.x)) * up.x, gt.y / (1.f + expf(-gt.y)) * up.y,
                                  gt.z / (1.f + expf(-gt.z)) * up.z, gt.w / (1.f + expf(-gt.w)) * up.w);
-    Pack4<HT>::store(u + idx, r);
+    Pack4<HT>::store(u + m * ldu + c, r);
   }
 }
 
@@ -376,14 +377,16 @@ hipError_t launch_qkv_rope_kv(int dtype, int kv_fp8, float k_scale, float v_scal
 }
 
 hipError_t launch_swiglu(int dtype, int M, int F, const float* part, int splits, void* u,
-                         hipStream_t stream) {
+                         hipStream_t stream, int64_t ldu) {
   const int64_t n = (int64_t)M * F / 4;
   if (n == 0) return hipSuccess;
+  if (ldu == 0) ldu = F;
   if (dtype == 1)
     swiglu_kernel<uint16_t><<<grid_for(n, 256), 256, 0, stream>>>(M, F, part, splits,
-                                                                   (uint16_t*)u);
+                                                                   (uint16_t*)u, ldu);
   else
-    swiglu_kernel<float><<<grid_for(n, 256), 256, 0, stream>>>(M, F, part, splits, (float*)u);
+    swiglu_kernel<float><<<grid_for(n, 256), 256, 0, stream>>>(M, F, part, splits, (float*)u,
+                                                                ldu);
   return hipGetLastError();
 }
 

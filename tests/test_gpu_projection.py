@@ -135,6 +135,27 @@ def test_swiglu_fused_epilogue(M, F, K):
     _swiglu_run(M, F, K, seed=M + F)
 
 
+@pytest.mark.parametrize("M", [1, 16, 32, 33, 128, 256])
+@pytest.mark.parametrize("F,K", [(17408, 320), (16448, 256), (17400, 256)])
+def test_swiglu_split_tail(M, F, K):
+    """FFN widths whose fused grid would be whole rounds of 256 work groups
+    plus a last round at most half full (272 and 258 half column-groups;
+    17400 ends in a part-filled group): the columns of that last round take
+    the split-K kernels and the SwiGLU pass (a workspace is needed), the
+    others the fused epilogue, on the streaming kernel and both tiles."""
+    from paper_2609_36899_amd import _native as N
+    assert N.load().swiglu_projection_workspace_bytes(N.BF16, M, F, K) > 0
+    _swiglu_run(M, F, K, seed=M + F + 1)
+
+
+@pytest.mark.parametrize("M", [16, 128, 256])
+def test_swiglu_14b_shape_split_tail_sampled_rows(M):
+    """The 14B-shaped gate/up pair (F 17408, K 5120): 256 half-groups fused,
+    the last 16 split 16 ways; rows sampled."""
+    rows = sorted(set([0, M - 1] + list(np.random.default_rng(M).integers(0, M, 4))))
+    _swiglu_run(M, 17408, 5120, seed=11 + M, rows=rows)
+
+
 @pytest.mark.parametrize("M", [1, 16, 256, 512])
 def test_swiglu_8b_shape_sampled_rows(M):
     """The 8B gate/up pair (F 14336, K 4096) as the decode step runs it: the
