@@ -727,8 +727,8 @@ GluPlan plan_glu(int M, int F, int K) {
   GluPlan p{halves, 0, 1, K};
   const int tail = halves % 256;
   if (M > 256 || halves < 256 || tail == 0 || tail > 128) return p;
-  const int ksteps = K / 64;
-  const int per = (ksteps + std::min(16, 256 / tail) - 1) / std::min(16, 256 / tail);
+  const int ksteps = K / 64, want = std::min(16, 256 / tail);
+  const int per = (ksteps + want - 1) / want;  // k-steps of 64 per split
   const int splits = (ksteps + per - 1) / per;
   if (splits < 2) return p;
   return {halves - tail, tail, splits, per * 64};
