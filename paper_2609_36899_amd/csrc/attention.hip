@@ -7,10 +7,10 @@
 // streams its pages once, applies them to every query head of the GQA group,
 // and leaves an online-softmax partial (max, sum, unnormalised output) that
 // the combine pass merges.  Query rows of a block = (query, head-in-group)
-// pairs: one query (G rows) per decode block; 128/G queries per prefill
-// block for the LDS-staged prefill kernel (bf16 pages, 128-dim heads:
-// attention_prefill.hip) and 64/G for the row-wave form of the split kernel
-// here (fp8 pages, 64-dim heads).
+// pairs: one query (G rows) per decode block; 128/G or 256/G queries per
+// prefill block for the LDS-staged prefill kernel (128-dim heads, bf16 or
+// E4M3 pages: attention_prefill.hip) and 64/G for the row-wave form of the
+// split kernel here (64-dim heads).
 //
 // bf16 path: both products run on MFMA (v_mfma_f32_16x16x32_bf16).  Scores are
 // computed transposed, S^T = K Q^T, so that each lane's output column is one
